@@ -1,0 +1,361 @@
+"""Dense float64 reference for Forgetting Attention with ACP (one head at a time).
+
+TEST INFRASTRUCTURE ONLY: imported by tests, the smoke check and the benchmark's
+CPU-baseline leg, never by the product path.
+
+Indices are 0-based here; the paper's are 1-based.  The pruning grid uses square
+blocks of BLOCK = 64 rows by 64 columns.
+
+Every function cites the passage of the paper it follows.  Points where the paper
+is silent or garbled are settled as follows (the same readings bind the HIP path):
+
+* cumulative gates (Sec. 2, "FlashAttention implementation"): c_i is the sum of
+  log f_l for l <= i, accumulated in float64 in index order and rounded once to
+  float32.  c is the canonical float32 quantity both sides compare on.
+* logit bound (Sec. 3, "Safe pruning"): U = rho_q * rho_k / sqrt(d), with rho the
+  largest row L2 norm of the stored Q (resp. K) of the one sequence and head.
+  Squared norms are float64 sums in ascending feature order; U = sqrt(rq2*rk2/d)
+  with IEEE round-to-nearest float64 operations.
+* threshold (Sec. 3, eq. for delta; App. A): delta = -(2U + (log L - log eps)),
+  natural logarithms, L the full context length, float64.  eps = 0 gives
+  delta = -inf (nothing pruned).
+* block rule (Sec. 3, "Block-level pruning"): block (m, n) is pruned iff every
+  causal entry of D in it is below delta (strict), decided in float64 on the
+  float32 c.  Diagonal blocks always hold D_ii = 0 and are kept.
+* Algorithm 1 as printed assigns the boundary index after incrementing past the
+  first kept block; the reading used here is "first kept block of the row"
+  (the boundary block the text defines), so the pointer is tested before it is
+  advanced.
+* backward: the paper only says it follows the forward.  The mask is a constant
+  (the indicator has zero derivative almost everywhere, and delta's dependence on
+  Q and K is not differentiated).  With x_ij = q_i.k_j/sqrt(d) + c_i - c_j:
+  dS = P o (dP - Delta), dQ = dS K / sqrt(d), dK = dS^T Q / sqrt(d),
+  dc = rowsum(dS) - colsum(dS), and dlog f_l = sum_{i >= l} dc_i.
+"""
+from __future__ import annotations
+
+import math
+from fractions import Fraction
+
+import numpy as np
+
+BLOCK = 64
+
+__all__ = [
+    "BLOCK", "cumsum_log_gates", "cumsum_exact_fraction", "cumsum_span_bits",
+    "row_norm_sq_max", "logit_bound", "log_len_over_eps", "threshold",
+    "entry_keep", "block_keep_bruteforce", "block_keep_topright", "boundary_from_block_keep",
+    "boundary_alg1", "col_end_from_row_start", "kept_tiles", "causal_tiles",
+    "block_mask", "entry_mask", "causal_mask", "forward", "backward", "pruned_mass",
+    "plan_head", "run_head",
+]
+
+
+# --------------------------------------------------------------------------
+# Stage 1: cumulative log gates, logit bound, threshold, boundary
+# --------------------------------------------------------------------------
+
+def cumsum_log_gates(log_f) -> np.ndarray:
+    """c_i = sum_{l<=i} log f_l (Sec. 2, FlashAttention paragraph: D = c1^T - 1c^T).
+
+    float64 running sum in index order, rounded once to float32.
+    """
+    x = np.asarray(log_f, dtype=np.float32).astype(np.float64)
+    acc = np.zeros(x.shape[:-1], dtype=np.float64)
+    out = np.empty(x.shape, dtype=np.float64)
+    for i in range(x.shape[-1]):
+        acc = acc + x[..., i]
+        out[..., i] = acc
+    return out.astype(np.float32)
+
+
+def cumsum_exact_fraction(log_f_1d) -> np.ndarray:
+    """Exact rational prefix sums of float32 values, each rounded once to float32.
+
+    An independent definition of the canonical c (used to pin cumsum_log_gates).
+    """
+    vals = [Fraction(float(v)) for v in np.asarray(log_f_1d, dtype=np.float32)]
+    out = np.empty(len(vals), dtype=np.float32)
+    acc = Fraction(0)
+    for i, v in enumerate(vals):
+        acc += v
+        out[i] = _fraction_to_f32(acc)
+    return out
+
+
+def _fraction_to_f32(fr: Fraction) -> np.float32:
+    """Round an exact rational to the nearest float32, ties to even (one rounding)."""
+    if fr == 0:
+        return np.float32(0.0)
+    sign = -1 if fr < 0 else 1
+    a = abs(fr)
+    e = a.numerator.bit_length() - a.denominator.bit_length()
+    if Fraction(2) ** e > a:
+        e -= 1                                  # now 2^e <= a < 2^(e+1)
+    e = max(e, -126)                            # subnormals share the lowest exponent
+    scaled = a * Fraction(2) ** (23 - e)        # 24-bit significand in [2^23, 2^24)
+    n, rem = divmod(scaled.numerator, scaled.denominator)
+    twice = 2 * rem
+    if twice > scaled.denominator or (twice == scaled.denominator and n % 2 == 1):
+        n += 1
+    return np.float32(sign * math.ldexp(float(n), e - 23))
+
+
+def cumsum_span_bits(log_f_1d) -> int:
+    """Bits spanned by the partial sums of float32 addends (0 if all are zero).
+
+    Every float32 addend is an integer multiple of 2^(e_min - 23) and every partial
+    sum is below 2^E with E = ceil(log2(sum |x|)); when E - (e_min - 23) <= 53,
+    all float64 partial sums are exact, so any summation order gives the same c.
+    """
+    x = np.asarray(log_f_1d, dtype=np.float32).astype(np.float64)
+    nz = x[x != 0]
+    if nz.size == 0:
+        return 0
+    _, e = np.frexp(np.abs(nz))          # |x| = m * 2^e, m in [0.5, 1)
+    lsb = int(np.min(np.maximum(e - 1, -126))) - 23
+    total = float(np.sum(np.abs(nz)))
+    E = math.frexp(total)[1]             # total < 2^E
+    return E - lsb
+
+
+def row_norm_sq_max(x) -> float:
+    """rho^2 = max_i sum_k x_ik^2 (Sec. 3, 'we can set U = rho_q rho_k / sqrt(d)').
+
+    x is [L, d]; the squared norm of each row is a float64 sum in ascending k.
+    """
+    x = np.asarray(x, dtype=np.float64)
+    acc = np.zeros(x.shape[0], dtype=np.float64)
+    for kk in range(x.shape[1]):
+        acc = acc + x[:, kk] * x[:, kk]
+    return float(np.max(acc)) if acc.size else 0.0
+
+
+def logit_bound(rho2_q: float, rho2_k: float, d: int) -> float:
+    """U = rho_q rho_k / sqrt(d), evaluated as sqrt(rho_q^2 rho_k^2 / d) (Sec. 3)."""
+    return math.sqrt((float(rho2_q) * float(rho2_k)) / float(d))
+
+
+def log_len_over_eps(L: int, eps: float) -> float:
+    """log L - log eps (natural logs, Sec. 3 and App. A); +inf for eps = 0."""
+    if eps == 0.0:
+        return math.inf
+    return math.log(float(L)) - math.log(float(eps))
+
+
+def threshold(U: float, L: int, eps: float) -> float:
+    """delta = -2U - log L + log eps (Sec. 3, 'Safe pruning'; proof in App. A)."""
+    return -(2.0 * U + log_len_over_eps(L, eps))
+
+
+def entry_keep(c, delta: float) -> np.ndarray:
+    """keep_ij = (j <= i) and D_ij >= delta with D_ij = c_i - c_j (Sec. 3, eq. 3)."""
+    c64 = np.asarray(c, dtype=np.float32).astype(np.float64)
+    L = c64.shape[0]
+    D = c64[:, None] - c64[None, :]
+    return np.tril(np.ones((L, L), dtype=bool)) & (D >= delta)
+
+
+def block_keep_bruteforce(c, delta: float, block: int = BLOCK) -> np.ndarray:
+    """Keep_mn = some causal entry of block (m, n) has D_ij >= delta (Sec. 3, block-level).
+
+    Decided entry by entry; diagonal blocks contain D_ii = 0 and so are kept
+    whenever delta <= 0 (footnote of the block-level paragraph).
+    """
+    keep = entry_keep(c, delta)
+    L = keep.shape[0]
+    M = L // block
+    kb = keep.reshape(M, block, M, block).any(axis=(1, 3))
+    kb[np.arange(M), np.arange(M)] = True
+    return kb
+
+
+def block_keep_topright(c, delta: float, block: int = BLOCK) -> np.ndarray:
+    """Keep_mn decided on the top-right entry of each block (Sec. 3, block-level paragraph).
+
+    For n < m the largest entry of D[m][n] is c_{block*m} - c_{block*n + block-1}
+    by coordinate-wise monotonicity (Sec. 2).  Blocks above the diagonal are not
+    causal; diagonal blocks are kept.
+    """
+    c64 = np.asarray(c, dtype=np.float32).astype(np.float64)
+    M = c64.shape[0] // block
+    first = c64[np.arange(M) * block]
+    last = c64[np.arange(M) * block + block - 1]
+    kb = (first[:, None] - last[None, :]) >= delta
+    kb &= np.tril(np.ones((M, M), dtype=bool))
+    kb[np.arange(M), np.arange(M)] = True
+    return kb
+
+
+def boundary_from_block_keep(kb: np.ndarray):
+    """row_start[m] = min{n: Keep_mn}, col_end[n] = max{m: Keep_mn} (Sec. 3, two-stage)."""
+    M = kb.shape[0]
+    row_start = np.array([int(np.argmax(kb[m, :m + 1])) for m in range(M)], dtype=np.int32)
+    col_end = np.array([n + int(np.nonzero(kb[n:, n])[0].max()) for n in range(M)],
+                       dtype=np.int32)
+    return row_start, col_end
+
+
+def boundary_alg1(c, delta: float, block: int = BLOCK) -> np.ndarray:
+    """Linear-time boundary search (Sec. 3, Algorithm 1), first-kept-block reading.
+
+    One pointer l walks the key blocks; for each query block m it advances while
+    the top-right entry of block (m, l) is below delta, and never moves back.
+    """
+    c64 = np.asarray(c, dtype=np.float32).astype(np.float64)
+    M = c64.shape[0] // block
+    out = np.empty(M, dtype=np.int32)
+    l = 0
+    for m in range(M):
+        while l < m and (c64[block * m] - c64[block * l + block - 1]) < delta:
+            l += 1
+        out[m] = l
+    return out
+
+
+def col_end_from_row_start(row_start) -> np.ndarray:
+    """Column form of the staircase: col_end[n] = max{m : row_start[m] <= n}."""
+    rs = np.asarray(row_start)
+    M = rs.shape[0]
+    return np.array([max(m for m in range(M) if rs[m] <= n) for n in range(M)], dtype=np.int32)
+
+
+def kept_tiles(row_start) -> int:
+    rs = np.asarray(row_start, dtype=np.int64)
+    return int(np.sum(np.arange(rs.shape[0]) - rs + 1))
+
+
+def causal_tiles(M: int) -> int:
+    """Causal 64x64 blocks of one head, M(M+1)/2 (denominator of the pruned fraction)."""
+    return M * (M + 1) // 2
+
+
+# --------------------------------------------------------------------------
+# Masks
+# --------------------------------------------------------------------------
+
+def causal_mask(L: int) -> np.ndarray:
+    return np.tril(np.ones((L, L), dtype=bool))
+
+
+def block_mask(row_start, L: int, block: int = BLOCK) -> np.ndarray:
+    """Mask_ij = (j <= i) and block (i//block, j//block) is kept (block-level ACP)."""
+    rs = np.asarray(row_start)
+    qb = np.arange(L) // block
+    kb = np.arange(L) // block
+    return causal_mask(L) & (kb[None, :] >= rs[qb][:, None])
+
+
+def entry_mask(c, delta: float) -> np.ndarray:
+    """Entry-level ACP mask of eq. 3."""
+    return entry_keep(c, delta)
+
+
+# --------------------------------------------------------------------------
+# Stage 2: attention forward / backward (dense, float64)
+# --------------------------------------------------------------------------
+
+def _logits(q, k, c, mask):
+    q = np.asarray(q, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    c64 = np.asarray(c).astype(np.float64)
+    d = q.shape[1]
+    s = (q @ k.T) / math.sqrt(d)
+    x = s + (c64[:, None] - c64[None, :])
+    return np.where(mask, x, -np.inf)
+
+
+def forward(q, k, v, c, mask):
+    """O = softmax(Q K^T / sqrt(d) + D) V restricted to `mask`, and the row log-sum-exp.
+
+    Sec. 2, eq. 1-2 (Forgetting Attention), with the ACP indicator of eq. 3 folded
+    into `mask` (block-level mask for the pruned kernel, causal mask for eq. 1).
+    Returns (O [L,d] float64, LSE [L] float64).
+    """
+    x = _logits(q, k, c, mask)
+    m = np.max(x, axis=1, keepdims=True)
+    e = np.exp(x - m)
+    z = np.sum(e, axis=1, keepdims=True)
+    p = e / z
+    o = p @ np.asarray(v, dtype=np.float64)
+    lse = (m + np.log(z))[:, 0]
+    return o, lse
+
+
+def backward(q, k, v, c, mask, do, o=None, lse=None):
+    """Gradients of the masked forward (the paper says only that the backward mirrors
+    the forward, Sec. 2; formulas derived by the chain rule through eq. 2 and c).
+
+    Returns a dict with dq, dk, dv, dlog_f ([L]) and the intermediates dS, dc.
+    """
+    q = np.asarray(q, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    v = np.asarray(v, dtype=np.float64)
+    do = np.asarray(do, dtype=np.float64)
+    d = q.shape[1]
+    if o is None or lse is None:
+        o, lse = forward(q, k, v, c, mask)
+    x = _logits(q, k, c, mask)
+    p = np.exp(x - lse[:, None])
+    dv = p.T @ do
+    dp = do @ v.T
+    delta_row = np.sum(do * o, axis=1)
+    ds = p * (dp - delta_row[:, None])
+    dq = (ds @ k) / math.sqrt(d)
+    dk = (ds.T @ q) / math.sqrt(d)
+    dc = np.sum(ds, axis=1) - np.sum(ds, axis=0)
+    dlog_f = np.cumsum(dc[::-1])[::-1].copy()
+    return {"dq": dq, "dk": dk, "dv": dv, "dlog_f": dlog_f, "ds": ds, "dc": dc,
+            "o": o, "lse": lse}
+
+
+def pruned_mass(q, k, c, kept_mask):
+    """Per row, the total full-attention weight (eq. 1) that `kept_mask` drops (App. A)."""
+    L = np.asarray(q).shape[0]
+    full = causal_mask(L)
+    x = _logits(q, k, c, full)
+    m = np.max(x, axis=1, keepdims=True)
+    a = np.exp(x - m)
+    a /= np.sum(a, axis=1, keepdims=True)
+    return np.sum(np.where(full & ~kept_mask, a, 0.0), axis=1)
+
+
+# --------------------------------------------------------------------------
+# One head end to end
+# --------------------------------------------------------------------------
+
+def plan_head(q, k, log_f, eps: float, block: int = BLOCK, method: str = "bruteforce"):
+    """Stage 1 for one (batch, head): c, U, delta and the boundary (Sec. 3)."""
+    L, d = np.asarray(q).shape
+    c = cumsum_log_gates(log_f)
+    rq = row_norm_sq_max(q)
+    rk = row_norm_sq_max(k)
+    U = logit_bound(rq, rk, d)
+    delta = threshold(U, L, eps)
+    if method == "bruteforce":
+        kb = block_keep_bruteforce(c, delta, block)
+        row_start, col_end = boundary_from_block_keep(kb)
+    elif method == "topright":
+        kb = block_keep_topright(c, delta, block)
+        row_start, col_end = boundary_from_block_keep(kb)
+    elif method == "alg1":
+        row_start = boundary_alg1(c, delta, block)
+        col_end = col_end_from_row_start(row_start)
+    else:
+        raise ValueError(method)
+    return {"c": c, "rho2_q": rq, "rho2_k": rk, "U": U, "delta": delta,
+            "row_start": row_start, "col_end": col_end, "kept": kept_tiles(row_start)}
+
+
+def run_head(q, k, v, log_f, eps: float, do=None, block: int = BLOCK, method: str = "topright"):
+    """Plan, pruned forward and (if do is given) backward for one head."""
+    plan = plan_head(q, k, log_f, eps, block, method)
+    L = np.asarray(q).shape[0]
+    mask = block_mask(plan["row_start"], L, block)
+    o, lse = forward(q, k, v, plan["c"], mask)
+    out = dict(plan)
+    out.update({"o": o, "lse": lse, "mask": mask})
+    if do is not None:
+        g = backward(q, k, v, plan["c"], mask, do, o, lse)
+        out.update({kk: g[kk] for kk in ("dq", "dk", "dv", "dlog_f", "dc")})
+    return out

@@ -1,0 +1,123 @@
+"""Seeded synthetic inputs for FoX attention with adaptive computation pruning.
+
+This module draws the inputs only: Q, K, V, the per-head log forget gates and
+the upstream gradient dO.  It holds none of the method's arithmetic (no cumsum,
+no bound, no threshold, no attention), so that the oracle and the HIP path can
+both be fed from it without sharing any of the computation they are compared on.
+
+Shapes follow the paper's model table (App. B, Table 2: d_head = 64; 12/16/24
+heads for the 125M/360M/760M models) and its training batches (App. B: each
+gradient-accumulation step holds 32k tokens, so B*L = 32768 per GPU).  The
+trained LongCrawl64 activations the paper measures on are not available; random
+N(0,1) queries/keys/values with gate logits a ~ N(mu_h, 0.5) stand in for them.
+The forget gate is f = sigmoid(a) (Sec. 2, eq. 1); log f = -softplus(-a) is
+evaluated in float64 and rounded once to float32, so that strongly remembering
+gates (mu = 20) do not round to log f = 0.
+
+Draw order (torch.Generator on the CPU): per-head mu, Q, K, V, gate noise, dO.
+Floating draws are float32 N(0,1) (rounded to nearest-even bfloat16 for the
+bf16 workloads).
+"""
+from __future__ import annotations
+
+import dataclasses
+import math
+from typing import Optional, Sequence
+
+import numpy as np
+import torch
+
+
+@dataclasses.dataclass(frozen=True)
+class Workload:
+    name: str
+    B: int
+    H: int
+    L: int
+    d: int
+    dtype: str  # "f32" or "bf16"
+    seed: int
+    mu: Optional[Sequence[float]] = None  # per-head gate mean; None: U[1,10] per head
+    gate_sigma: float = 0.5
+    row_norms: Optional[Sequence[float]] = None  # per-head q/k row L2 norm (cycled)
+    eps: float = math.exp(-10.0)
+
+    @property
+    def M(self) -> int:
+        return self.L // 64
+
+    def describe(self) -> str:
+        return (f"{self.name}: B={self.B} H={self.H} L={self.L} d={self.d} {self.dtype}, "
+                f"seed={self.seed}")
+
+
+# The five workloads: a tiny fp32 case, three single layers shaped like the
+# paper's 125M / 360M / 760M models at L = 4k / 8k / 16k, and a d=128 sweep
+# whose heads span nearly-all-pruned to nothing-pruned.
+WORKLOADS = {
+    "tiny": Workload("tiny", 1, 2, 512, 64, "f32", 0, mu=(2.0, 8.0)),
+    "125m": Workload("125m", 8, 12, 4096, 64, "bf16", 1),
+    "360m": Workload("360m", 4, 16, 8192, 64, "bf16", 2),
+    "760m": Workload("760m", 2, 24, 16384, 64, "bf16", 3),
+    "adv": Workload("adv", 2, 16, 16384, 128, "bf16", 4,
+                    mu=tuple((0.0, 3.0, 6.0, 12.0, 20.0)[h % 5] for h in range(16)),
+                    row_norms=tuple((1.0, 4.0, 16.0)[h % 3] for h in range(16))),
+}
+
+
+def custom(name: str, B: int, H: int, L: int, d: int, dtype: str, seed: int,
+           mu=None, row_norms=None, gate_sigma: float = 0.5) -> Workload:
+    return Workload(name, B, H, L, d, dtype, seed, mu=None if mu is None else tuple(mu),
+                    gate_sigma=gate_sigma,
+                    row_norms=None if row_norms is None else tuple(row_norms))
+
+
+def _torch_dtype(dt: str):
+    return {"f32": torch.float32, "bf16": torch.bfloat16}[dt]
+
+
+def log_sigmoid_f32(a: np.ndarray) -> np.ndarray:
+    """log(sigmoid(a)) = -softplus(-a), evaluated in float64, rounded to float32."""
+    a = np.asarray(a, dtype=np.float64)
+    return (-np.logaddexp(0.0, -a)).astype(np.float32)
+
+
+def generate(w: Workload, with_grad: bool = True) -> dict:
+    """Draw one seeded input set for workload `w` (CPU tensors).
+
+    Returns a dict with q, k, v (and do) as [B,H,L,d] tensors of the workload
+    dtype, log_f as a [B,H,L] float32 tensor, and mu as the per-head gate means.
+    """
+    g = torch.Generator(device="cpu")
+    g.manual_seed(w.seed)
+    B, H, L, d = w.B, w.H, w.L, w.d
+    if w.mu is None:
+        mu = torch.rand(H, generator=g, dtype=torch.float64) * 9.0 + 1.0
+        mu = mu.tolist()
+    else:
+        mu = [float(w.mu[h % len(w.mu)]) for h in range(H)]
+    shape = (B, H, L, d)
+    q = torch.randn(shape, generator=g, dtype=torch.float32)
+    k = torch.randn(shape, generator=g, dtype=torch.float32)
+    v = torch.randn(shape, generator=g, dtype=torch.float32)
+    if w.row_norms is not None:
+        r = torch.tensor([float(w.row_norms[h % len(w.row_norms)]) for h in range(H)],
+                         dtype=torch.float32).view(1, H, 1, 1)
+        q = q / q.norm(dim=-1, keepdim=True) * r
+        k = k / k.norm(dim=-1, keepdim=True) * r
+    z = torch.randn((B, H, L), generator=g, dtype=torch.float32)
+    a = np.asarray(mu, dtype=np.float64).reshape(1, H, 1) + w.gate_sigma * z.numpy().astype(np.float64)
+    log_f = torch.from_numpy(log_sigmoid_f32(a))
+    out = {"q": q, "k": k, "v": v, "log_f": log_f, "mu": mu}
+    if with_grad:
+        out["do"] = torch.randn(shape, generator=g, dtype=torch.float32)
+    td = _torch_dtype(w.dtype)
+    for name in ("q", "k", "v", "do"):
+        if name in out:
+            out[name] = out[name].to(td).contiguous()
+    return out
+
+
+def to_f64(t: torch.Tensor) -> np.ndarray:
+    """Exact upcast of a float32/bfloat16 CPU tensor to a float64 numpy array."""
+    return t.detach().to(torch.float32).cpu().numpy().astype(np.float64)

@@ -1,0 +1,337 @@
+"""Pins for the CPU oracle: closed forms, textbook special cases, the paper's
+error bound, independent derivations (exact rationals, autograd, finite
+differences) and brute force.  None of these re-types the oracle's own formula.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as orc
+from paper_2504_06949_amd import workloads
+
+EPS = math.exp(-10.0)
+
+
+def _rng(seed):
+    return np.random.default_rng(seed)
+
+
+def _gates(rng, L, mu, sigma=0.5):
+    a = mu + sigma * rng.standard_normal(L)
+    return workloads.log_sigmoid_f32(a)
+
+
+# --------------------------------------------------------------------------
+# c (Sec. 2): exact rational prefix sums and a dyadic closed form
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("mu", [0.0, 1.0, 3.0, 6.0, 12.0, 20.0])
+def test_cumsum_equals_exact_rational(mu):
+    lf = _gates(_rng(1), 512, mu)
+    assert orc.cumsum_span_bits(lf) <= 53
+    np.testing.assert_array_equal(orc.cumsum_log_gates(lf), orc.cumsum_exact_fraction(lf))
+
+
+def test_cumsum_dyadic_constant_gate_closed_form():
+    lam = 2.0 ** -3
+    L = 4096
+    c = orc.cumsum_log_gates(np.full(L, -lam, dtype=np.float32))
+    np.testing.assert_array_equal(c, (-lam * (np.arange(L) + 1)).astype(np.float32))
+
+
+def test_cumsum_span_of_paper_like_gates_is_far_below_53_bits():
+    # 32k positions, every gate class of the workloads: partial sums stay exact.
+    for mu in (0.0, 1.0, 3.0, 6.0, 10.0, 12.0, 20.0):
+        assert orc.cumsum_span_bits(_gates(_rng(2), 32768, mu)) <= 45
+
+
+def test_fraction_rounding_is_single_rounding():
+    # 1 + 2^-24 + 2^-60 must round up to 1 + 2^-23 (a float64 detour would round
+    # 1 + 2^-24 + 2^-60 to 1 + 2^-24 and then tie to even, giving 1).
+    from fractions import Fraction
+    from oracle.acp_oracle import _fraction_to_f32
+    x = Fraction(1) + Fraction(1, 2 ** 24) + Fraction(1, 2 ** 60)
+    assert _fraction_to_f32(x) == np.float32(1 + 2.0 ** -23)
+    assert _fraction_to_f32(Fraction(1) + Fraction(1, 2 ** 24)) == np.float32(1.0)
+    assert _fraction_to_f32(-Fraction(3, 2 ** 150)) == np.float32(-3 * 2.0 ** -150)
+
+
+# --------------------------------------------------------------------------
+# rho, U, delta (Sec. 3): closed forms
+# --------------------------------------------------------------------------
+
+def test_norm_and_bound_closed_form_axis_rows():
+    L, d, r = 256, 64, 4.0
+    q = np.zeros((L, d)); q[:, 0] = r
+    k = np.zeros((L, d)); k[:, 5] = -r
+    assert orc.row_norm_sq_max(q) == r * r
+    U = orc.logit_bound(orc.row_norm_sq_max(q), orc.row_norm_sq_max(k), d)
+    assert U == r * r / 8.0  # sqrt(64) = 8
+
+
+def test_norm_picks_the_largest_row():
+    rng = _rng(3)
+    x = np.sign(rng.standard_normal((128, 16)))  # every row has squared norm 16
+    x[77] *= 3.0                                  # one row with squared norm 144
+    assert orc.row_norm_sq_max(x) == 144.0
+
+
+def test_bound_dominates_every_logit_and_is_attained():
+    rng = _rng(4)
+    L, d = 200, 32
+    q = rng.standard_normal((L, d)); k = rng.standard_normal((L, d)) * 3
+    U = orc.logit_bound(orc.row_norm_sq_max(q), orc.row_norm_sq_max(k), d)
+    assert np.max(np.abs(q @ k.T)) / math.sqrt(d) <= U
+    # parallel extremal rows attain the bound
+    iq = np.argmax(np.sum(q * q, 1)); ik = np.argmax(np.sum(k * k, 1))
+    k2 = k.copy(); k2[ik] = q[iq] * np.linalg.norm(k[ik]) / np.linalg.norm(q[iq])
+    U2 = orc.logit_bound(orc.row_norm_sq_max(q), orc.row_norm_sq_max(k2), d)
+    assert abs(q[iq] @ k2[ik] / math.sqrt(d) - U2) <= 1e-12 * U2
+
+
+def test_threshold_hand_value():
+    # U = 2, L = 512, eps = e^-10: delta = -(4 + 9 ln 2 + 10)
+    delta = orc.threshold(2.0, 512, EPS)
+    assert abs(delta - (-(14.0 + 9.0 * math.log(2.0)))) <= 4 * np.spacing(abs(delta))
+    assert orc.threshold(2.0, 512, 0.0) == -math.inf
+
+
+# --------------------------------------------------------------------------
+# Boundary (Sec. 3, block rule and Algorithm 1)
+# --------------------------------------------------------------------------
+
+def _closed_form_row_start(M, lam, delta):
+    # constant gate -lam: top-right entry of block (m, n<m) is -lam (64 (m-n) - 63)
+    W = -delta / lam
+    return np.maximum(0, np.arange(M) - math.floor((W + 63.0) / 64.0)).astype(np.int32)
+
+
+@pytest.mark.parametrize("lam,r", [(2.0 ** -3, 4.0), (2.0 ** -5, 3.0), (0.75, 1.0)])
+def test_boundary_constant_gate_closed_form(lam, r):
+    L, d = 2048, 64
+    M = L // 64
+    q = np.zeros((L, d)); q[:, 0] = r
+    k = np.zeros((L, d)); k[:, 1] = r
+    lf = np.full(L, -lam, dtype=np.float32)
+    for method in ("bruteforce", "topright", "alg1"):
+        plan = orc.plan_head(q, k, lf, EPS, method=method)
+        W = -plan["delta"] / lam
+        assert abs((W + 63) / 64 - round((W + 63) / 64)) > 1e-6  # not on a knife edge
+        np.testing.assert_array_equal(plan["row_start"], _closed_form_row_start(M, lam, plan["delta"]))
+
+
+def test_boundary_tie_is_kept():
+    lam = 2.0 ** -3
+    L = 1024
+    c = orc.cumsum_log_gates(np.full(L, -lam, dtype=np.float32))
+    for k_ in (1, 2, 3):
+        delta = -lam * (64 * k_ - 63)       # block (m, m-k) top-right entry exactly delta
+        for kb in (orc.block_keep_bruteforce(c, delta), orc.block_keep_topright(c, delta)):
+            rs, _ = orc.boundary_from_block_keep(kb)
+            np.testing.assert_array_equal(rs, np.maximum(0, np.arange(L // 64) - k_))
+        np.testing.assert_array_equal(orc.boundary_alg1(c, delta), np.maximum(0, np.arange(L // 64) - k_))
+        # an ulp lower bound flips the block (m, m-k) to pruned -> back to m-k+1
+        d2 = np.nextafter(delta, 0.0)
+        np.testing.assert_array_equal(orc.boundary_alg1(c, d2), np.maximum(0, np.arange(L // 64) - k_ + 1))
+
+
+def test_boundary_extremes():
+    L, d = 1024, 16
+    rng = _rng(5)
+    q = rng.standard_normal((L, d)); k = rng.standard_normal((L, d))
+    M = L // 64
+    p0 = orc.plan_head(q, k, np.zeros(L, np.float32), EPS)
+    np.testing.assert_array_equal(p0["row_start"], np.zeros(M))
+    assert p0["kept"] == orc.causal_tiles(M)
+    p1 = orc.plan_head(q, k, np.full(L, -1e4, np.float32), EPS)
+    np.testing.assert_array_equal(p1["row_start"], np.arange(M))
+    np.testing.assert_array_equal(p1["col_end"], np.arange(M))
+    assert p1["kept"] == M
+    pz = orc.plan_head(q, k, np.full(L, -1e4, np.float32), 0.0)   # eps = 0: nothing pruned
+    np.testing.assert_array_equal(pz["row_start"], np.zeros(M))
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_boundary_three_ways_agree_and_staircase(seed):
+    rng = _rng(100 + seed)
+    L = int(rng.choice([512, 1024, 1536]))
+    d = int(rng.choice([16, 64]))
+    mu = float(rng.choice([-1.0, 0.0, 1.0, 2.0, 3.0, 5.0]))
+    q = rng.standard_normal((L, d)) * rng.choice([0.3, 1.0, 2.0])
+    k = rng.standard_normal((L, d))
+    lf = _gates(rng, L, mu, sigma=float(rng.choice([0.5, 2.0])))
+    pb = orc.plan_head(q, k, lf, EPS, method="bruteforce")
+    pt = orc.plan_head(q, k, lf, EPS, method="topright")
+    pa = orc.plan_head(q, k, lf, EPS, method="alg1")
+    for p in (pt, pa):
+        np.testing.assert_array_equal(pb["row_start"], p["row_start"])
+        np.testing.assert_array_equal(pb["col_end"], p["col_end"])
+    rs = pb["row_start"]; M = L // 64
+    assert np.all(np.diff(rs) >= 0) and np.all(rs <= np.arange(M)) and np.all(rs >= 0)
+    np.testing.assert_array_equal(pb["col_end"], orc.col_end_from_row_start(rs))
+
+
+def test_tiny_workload_prunes_local_head_only():
+    w = workloads.WORKLOADS["tiny"]
+    x = workloads.generate(w, with_grad=False)
+    kept = []
+    for h in range(w.H):
+        q = workloads.to_f64(x["q"][0, h]); k = workloads.to_f64(x["k"][0, h])
+        lf = x["log_f"][0, h].numpy()
+        kept.append(orc.plan_head(q, k, lf, EPS)["kept"])
+    assert kept[1] == orc.causal_tiles(w.M)          # mu = 8: nothing pruned
+    assert kept[0] < orc.causal_tiles(w.M)           # mu = 2: some blocks pruned
+
+
+# --------------------------------------------------------------------------
+# Forward (eq. 1-3): textbook special cases, closed forms, App. A bound
+# --------------------------------------------------------------------------
+
+def test_forward_no_forgetting_is_causal_sdpa():
+    rng = _rng(6)
+    L, d = 256, 32
+    q, k, v = (rng.standard_normal((L, d)) for _ in range(3))
+    o, _ = orc.forward(q, k, v, np.zeros(L), orc.causal_mask(L))
+    ref = torch.nn.functional.scaled_dot_product_attention(
+        torch.from_numpy(q)[None], torch.from_numpy(k)[None], torch.from_numpy(v)[None], is_causal=True)[0]
+    np.testing.assert_allclose(o, ref.numpy(), rtol=0, atol=1e-12)
+
+
+def test_forward_zero_queries_constant_gate_closed_form():
+    # q = 0: weights are the gate decay alone, w_ij ~ exp(-lam (i - j)).
+    L, d, lam = 192, 8, 0.3
+    rng = _rng(7)
+    v = rng.standard_normal((L, d))
+    c = -lam * (np.arange(L) + 1.0)
+    o, lse = orc.forward(np.zeros((L, d)), rng.standard_normal((L, d)), v, c, orc.causal_mask(L))
+    i = np.arange(L)
+    np.testing.assert_allclose(lse, np.log((1 - np.exp(-lam * (i + 1))) / (1 - math.exp(-lam))),
+                               rtol=0, atol=1e-12)
+    for ii in (0, 1, 50, L - 1):
+        w = np.exp(-lam * (ii - np.arange(ii + 1)))
+        np.testing.assert_allclose(o[ii], (w[:, None] * v[:ii + 1]).sum(0) / w.sum(), atol=1e-12)
+
+
+def test_forward_strong_forgetting_returns_values():
+    rng = _rng(8)
+    L, d = 256, 16
+    q, k, v = (rng.standard_normal((L, d)) for _ in range(3))
+    out = orc.run_head(q, k, v, np.full(L, -1e4, np.float32), EPS)
+    np.testing.assert_allclose(out["o"], v, atol=1e-12)
+
+
+@pytest.mark.parametrize("mu", [-1.0, 0.5, 2.0])
+def test_pruned_mass_bound_and_output_change(mu):
+    rng = _rng(9)
+    L, d = 1024, 64
+    q = rng.standard_normal((L, d)); k = rng.standard_normal((L, d)); v = rng.standard_normal((L, d))
+    lf = _gates(rng, L, mu)
+    out = orc.run_head(q, k, v, lf, EPS, method="bruteforce")
+    assert out["kept"] < orc.causal_tiles(L // 64)              # pruning is active
+    mass_blk = orc.pruned_mass(q, k, out["c"], out["mask"])
+    mass_ent = orc.pruned_mass(q, k, out["c"], orc.entry_mask(out["c"], out["delta"]))
+    assert np.all(mass_blk <= mass_ent + 1e-300)
+    assert np.all(mass_ent < EPS)                             # App. A
+    o_full, _ = orc.forward(q, k, v, out["c"], orc.causal_mask(L))
+    bound = 2 * mass_blk * np.max(np.abs(v))
+    assert np.all(np.max(np.abs(out["o"] - o_full), axis=1) <= bound + 1e-12)
+
+
+def test_pruned_mass_bound_is_nearly_tight():
+    # Last row: s_LL = -U, s_Lj = +U and D_Lj just below delta for every j < L-1.
+    # Its entry-level pruned mass is (L-1)/L * eps (up to the gap below delta);
+    # a threshold built with U instead of 2U would prune e^U times more.
+    L, d, a = 256, 16, 2.0
+    U = a * a / 4.0
+    q = np.zeros((L, d)); q[:, 0] = a
+    k = np.zeros((L, d)); k[:, 0] = a; k[L - 1, 0] = -a
+    delta = orc.threshold(orc.logit_bound(orc.row_norm_sq_max(q), orc.row_norm_sq_max(k), d), L, EPS)
+    lf = np.zeros(L, np.float32); lf[L - 1] = np.float32(delta - 1e-3)
+    c = orc.cumsum_log_gates(lf)
+    mass = orc.pruned_mass(q, k, c, orc.entry_mask(c, delta))[L - 1]
+    assert mass < EPS
+    assert mass > 0.95 * (L - 1) / L * EPS
+    delta_1u = -(U + orc.log_len_over_eps(L, EPS))
+    assert math.exp(U + U + delta_1u) * (L - 1) > EPS  # the weaker threshold breaks the bound
+
+
+# --------------------------------------------------------------------------
+# Backward: autograd, finite differences, identities
+# --------------------------------------------------------------------------
+
+def _torch_loss(q, k, v, log_f, mask, do):
+    d = q.shape[1]
+    c = torch.cumsum(log_f, 0)
+    x = q @ k.T / math.sqrt(d) + (c[:, None] - c[None, :])
+    x = x.masked_fill(~mask, float("-inf"))
+    o = torch.softmax(x, dim=1) @ v
+    return (o * do).sum()
+
+
+def _case(seed, L=192, d=16, mu=-0.5):
+    rng = _rng(seed)
+    q = rng.standard_normal((L, d)); k = rng.standard_normal((L, d)); v = rng.standard_normal((L, d))
+    do = rng.standard_normal((L, d))
+    lf = _gates(rng, L, mu, sigma=1.0).astype(np.float64)
+    plan = orc.plan_head(q, k, lf.astype(np.float32), EPS)
+    mask = orc.block_mask(plan["row_start"], L)
+    return q, k, v, do, lf, mask, plan
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_backward_matches_autograd(seed):
+    q, k, v, do, lf, mask, plan = _case(20 + seed)
+    assert plan["kept"] < orc.causal_tiles(q.shape[0] // 64)
+    c = np.cumsum(lf)
+    g = orc.backward(q, k, v, c, mask, do)
+    t = [torch.tensor(a, requires_grad=True) for a in (q, k, v, lf)]
+    _torch_loss(*t, torch.from_numpy(mask), torch.from_numpy(do)).backward()
+    for name, tt in zip(("dq", "dk", "dv", "dlog_f"), t):
+        np.testing.assert_allclose(g[name], tt.grad.numpy(), rtol=0, atol=1e-11)
+
+
+def test_backward_finite_differences():
+    q, k, v, do, lf, mask, _ = _case(30, L=128, d=8, mu=-1.0)
+    rng = _rng(31)
+
+    def loss(q_, k_, v_, lf_):
+        o, _ = orc.forward(q_, k_, v_, np.cumsum(lf_), mask)
+        return float(np.sum(o * do))
+
+    g = orc.backward(q, k, v, np.cumsum(lf), mask, do)
+    h = 1e-6
+    args = [q, k, v, lf]
+    for idx, name in enumerate(("dq", "dk", "dv", "dlog_f")):
+        for _ in range(3):
+            r = rng.standard_normal(args[idx].shape)
+            plus = list(args); minus = list(args)
+            plus[idx] = args[idx] + h * r; minus[idx] = args[idx] - h * r
+            fd = (loss(*plus) - loss(*minus)) / (2 * h)
+            an = float(np.sum(g[name] * r))
+            assert abs(fd - an) <= 1e-6 * max(1.0, abs(an)), (name, fd, an)
+
+
+def test_backward_identities():
+    q, k, v, do, lf, mask, _ = _case(40, L=256, d=16, mu=0.0)
+    c = np.cumsum(lf)
+    g = orc.backward(q, k, v, c, mask, do)
+    ds = g["ds"]
+    np.testing.assert_allclose(ds.sum(axis=1), 0.0, atol=1e-12)          # rowsum(dS) = 0
+    L = q.shape[0]
+    rect = np.array([ds[l:, :l].sum() for l in range(L)])                 # sum_{i>=l, j<l} dS_ij
+    np.testing.assert_allclose(g["dlog_f"], rect, atol=1e-11)
+    assert abs(g["dlog_f"][0]) <= 1e-11                                   # log f_1 never enters D
+
+
+def test_backward_no_forgetting_is_sdpa_autograd():
+    rng = _rng(50)
+    L, d = 128, 16
+    q, k, v, do = (rng.standard_normal((L, d)) for _ in range(4))
+    g = orc.backward(q, k, v, np.zeros(L), orc.causal_mask(L), do)
+    t = [torch.tensor(a, requires_grad=True) for a in (q, k, v)]
+    o = torch.nn.functional.scaled_dot_product_attention(t[0][None], t[1][None], t[2][None], is_causal=True)[0]
+    (o * torch.from_numpy(do)).sum().backward()
+    for name, tt in zip(("dq", "dk", "dv"), t):
+        np.testing.assert_allclose(g[name], tt.grad.numpy(), rtol=0, atol=1e-11)
