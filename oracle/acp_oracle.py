@@ -47,7 +47,7 @@ __all__ = [
     "entry_keep", "block_keep_bruteforce", "block_keep_topright", "boundary_from_block_keep",
     "boundary_alg1", "col_end_from_row_start", "kept_tiles", "causal_tiles",
     "block_mask", "entry_mask", "causal_mask", "forward", "backward", "pruned_mass",
-    "plan_head", "run_head",
+    "plan_head", "run_head", "forward_rows", "backward_rows", "backward_cols",
 ]
 
 
@@ -359,3 +359,85 @@ def run_head(q, k, v, log_f, eps: float, do=None, block: int = BLOCK, method: st
         g = backward(q, k, v, plan["c"], mask, do, o, lse)
         out.update({kk: g[kk] for kk in ("dq", "dk", "dv", "dlog_f", "dc")})
     return out
+
+
+# --------------------------------------------------------------------------
+# Selected rows / columns of the same dense definition (for long sequences,
+# where the full L x L matrices of every head are too large to form)
+# --------------------------------------------------------------------------
+
+def _row_logits(q, k, c, row_start, i, block: int = BLOCK):
+    """Masked logits of query row i (eq. 2 with the block-level ACP mask)."""
+    q = np.asarray(q, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    c64 = np.asarray(c).astype(np.float64)
+    d = q.shape[1]
+    j = np.arange(i + 1)
+    keep = (j // block) >= int(row_start[i // block])
+    x = (k[: i + 1] @ q[i]) / math.sqrt(d) + (c64[i] - c64[: i + 1])
+    return np.where(keep, x, -np.inf)
+
+
+def forward_rows(q, k, v, c, row_start, rows, block: int = BLOCK):
+    """O and LSE of the pruned forward for the query rows `rows` (Sec. 2 eq. 1; each
+    row of eq. 1 depends only on its own logits).  Returns (O [n,d], LSE [n])."""
+    v = np.asarray(v, dtype=np.float64)
+    o = np.empty((len(rows), v.shape[1]))
+    lse = np.empty(len(rows))
+    for r, i in enumerate(rows):
+        x = _row_logits(q, k, c, row_start, i, block)
+        m = np.max(x)
+        e = np.exp(x - m)
+        z = np.sum(e)
+        o[r] = (e / z) @ v[: i + 1]
+        lse[r] = m + math.log(z)
+    return o, lse
+
+
+def backward_rows(q, k, v, c, row_start, do, rows, block: int = BLOCK):
+    """dQ and rowsum(dS) for the query rows `rows` (chain rule as in `backward`; a
+    row of dQ needs only that row of dS).  Returns (dQ [n,d], rowsum [n])."""
+    k = np.asarray(k, dtype=np.float64)
+    v = np.asarray(v, dtype=np.float64)
+    do = np.asarray(do, dtype=np.float64)
+    d = k.shape[1]
+    dq = np.empty((len(rows), d))
+    rs = np.empty(len(rows))
+    for r, i in enumerate(rows):
+        x = _row_logits(q, k, c, row_start, i, block)
+        p = np.exp(x - np.max(x))
+        p /= np.sum(p)
+        o_i = p @ v[: i + 1]
+        dp = v[: i + 1] @ do[i]
+        ds = p * (dp - do[i] @ o_i)
+        dq[r] = (ds @ k[: i + 1]) / math.sqrt(d)
+        rs[r] = np.sum(ds)
+    return dq, rs
+
+
+def backward_cols(q, k, v, c, row_start, do, cols, block: int = BLOCK):
+    """dK, dV and colsum(dS) for the key columns `cols`: column j collects dS_ij and
+    P_ij over every query row i >= j whose block keeps it, each row normalised by
+    its own softmax.  Returns (dK [n,d], dV [n,d], colsum [n])."""
+    q = np.asarray(q, dtype=np.float64)
+    v = np.asarray(v, dtype=np.float64)
+    do = np.asarray(do, dtype=np.float64)
+    L, d = q.shape
+    rs = np.asarray(row_start)
+    dk = np.zeros((len(cols), d))
+    dv = np.zeros((len(cols), d))
+    cs = np.zeros(len(cols))
+    for r, j in enumerate(cols):
+        for i in range(j, L):
+            if (j // block) < int(rs[i // block]):
+                continue
+            x = _row_logits(q, k, c, rs, i, block)
+            p = np.exp(x - np.max(x))
+            p /= np.sum(p)
+            o_i = p @ v[: i + 1]
+            dp_ij = do[i] @ v[j]
+            ds_ij = p[j] * (dp_ij - do[i] @ o_i)
+            dv[r] += p[j] * do[i]
+            dk[r] += ds_ij * q[i] / math.sqrt(d)
+            cs[r] += ds_ij
+    return dk, dv, cs

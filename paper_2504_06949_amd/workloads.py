@@ -82,6 +82,11 @@ def log_sigmoid_f32(a: np.ndarray) -> np.ndarray:
     return (-np.logaddexp(0.0, -a)).astype(np.float32)
 
 
+def log_sigmoid_f32_t(a: torch.Tensor) -> torch.Tensor:
+    """Tensor form of log_sigmoid_f32."""
+    return torch.from_numpy(log_sigmoid_f32(a.numpy()))
+
+
 def generate(w: Workload, with_grad: bool = True) -> dict:
     """Draw one seeded input set for workload `w` (CPU tensors).
 
