@@ -1,0 +1,262 @@
+"""ctypes binding of libacp.so, the HIP library behind include/acp.h.
+
+Argument marshalling only: every step of the computation runs in the library's
+kernels.  The functions named like the C entry points take raw device
+addresses; the tensor-level helpers below them (boundary, forward, backward,
+plan_views) allocate outputs with PyTorch and pass its current HIP stream.
+There is no fallback: if the library is missing, every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+import torch
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libacp.so")
+HEADER = os.path.join(os.path.dirname(PKG), "include", "acp.h")
+
+ACP_F32, ACP_BF16 = 0, 1
+ACP_OK, ACP_EINVAL, ACP_EUNSUPPORTED, ACP_EWORKSPACE, ACP_EHIP = 0, 1, 2, 3, 4
+
+FLAG_POSITIVE_GATE = 1
+FLAG_NONFINITE_GATE = 2
+FLAG_INEXACT_CUMSUM = 4
+FLAG_NONFINITE_NORM = 8
+
+
+class AcpError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(msg)
+        self.status = status
+
+
+class PlanLayout(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_size_t) for n in
+                ("c", "bound_u", "delta", "row_start", "col_end", "kept", "flags", "total")]
+
+
+K_NAMES = ("rownorm", "plan", "fwd", "dsum", "dq", "dkdv", "dlogf")
+
+
+class KernelTimes(ctypes.Structure):
+    _fields_ = [("launches", ctypes.c_int64 * len(K_NAMES)),
+                ("ms", ctypes.c_double * len(K_NAMES))]
+
+
+_lib = None
+_i, _d, _p, _sz = ctypes.c_int, ctypes.c_double, ctypes.c_void_p, ctypes.c_size_t
+
+_SIGS = {
+    "acp_workspace_size": [_i, _i, _i, _i, _i, ctypes.POINTER(_sz)],
+    "acp_plan_offsets": [_i, _i, _i, _i, _i, ctypes.POINTER(PlanLayout)],
+    "acp_boundary": [_p, _p, _p, _i, _i, _i, _i, _i, _d, _p, _p, _p, _p, _p, _p, _p, _p, _sz, _p],
+    "fox_attn_fwd": [_p, _p, _p, _p, _i, _i, _i, _i, _i, _d, _p, _p, _p, _sz, _p],
+    "fox_attn_bwd": [_p, _p, _p, _p, _i, _i, _i, _i, _i, _p, _p, _p, _p, _p, _sz, _p],
+    "acp_timing_enable": [_i],
+    "acp_timing_reset": [],
+    "acp_timing_read": [ctypes.POINTER(KernelTimes)],
+    "acp_status_string": [_i],
+    "acp_last_error": [],
+}
+
+
+def lib() -> ctypes.CDLL:
+    """Open libacp.so once; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise AcpError(-1, f"{LIB_PATH} is missing: build it with "
+                               "`python -m paper_2504_06949_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        for name, args in _SIGS.items():
+            fn = getattr(L, name)
+            fn.argtypes = args
+            fn.restype = ctypes.c_char_p if name in ("acp_status_string", "acp_last_error") else _i
+        _lib = L
+    return _lib
+
+
+def header_functions() -> list:
+    """Names of the functions include/acp.h declares."""
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return re.findall(r"^\s*(?:const\s+)?\w+\*?\s+\*?(\w+)\s*\(", text, flags=re.M)
+
+
+def acp_status_string(status: int) -> str:
+    return lib().acp_status_string(status).decode()
+
+
+def acp_last_error() -> str:
+    return lib().acp_last_error().decode()
+
+
+def _check(status: int):
+    if status != ACP_OK:
+        raise AcpError(status, f"{acp_status_string(status)}: {acp_last_error()}")
+
+
+# ---- the C entry points, raw addresses ---------------------------------------
+
+def acp_workspace_size(B, H, L, d, dt) -> int:
+    out = _sz(0)
+    _check(lib().acp_workspace_size(B, H, L, d, dt, ctypes.byref(out)))
+    return out.value
+
+
+def acp_plan_offsets(B, H, L, d, dt) -> PlanLayout:
+    out = PlanLayout()
+    _check(lib().acp_plan_offsets(B, H, L, d, dt, ctypes.byref(out)))
+    return out
+
+
+def acp_boundary(Q, K, log_f, dt, B, H, L, d, eps, c, bound_u, delta, row_start, col_end,
+                 kept, flags, ws, ws_bytes, stream) -> int:
+    return lib().acp_boundary(Q, K, log_f, dt, B, H, L, d, eps, c, bound_u, delta, row_start,
+                              col_end, kept, flags, ws, ws_bytes, stream)
+
+
+def fox_attn_fwd(Q, K, V, log_f, dt, B, H, L, d, eps, O, lse, ws, ws_bytes, stream) -> int:
+    return lib().fox_attn_fwd(Q, K, V, log_f, dt, B, H, L, d, eps, O, lse, ws, ws_bytes, stream)
+
+
+def fox_attn_bwd(Q, K, V, dO, dt, B, H, L, d, dQ, dK, dV, dlog_f, ws, ws_bytes, stream) -> int:
+    return lib().fox_attn_bwd(Q, K, V, dO, dt, B, H, L, d, dQ, dK, dV, dlog_f, ws, ws_bytes,
+                              stream)
+
+
+def acp_timing_enable(on: bool):
+    _check(lib().acp_timing_enable(1 if on else 0))
+
+
+def acp_timing_reset():
+    _check(lib().acp_timing_reset())
+
+
+def acp_timing_read() -> dict:
+    """{kernel name: (launches, summed ms)} since the last reset (waits for the GPU)."""
+    t = KernelTimes()
+    _check(lib().acp_timing_read(ctypes.byref(t)))
+    return {n: (int(t.launches[i]), float(t.ms[i])) for i, n in enumerate(K_NAMES)}
+
+
+# ---- tensor-level helpers ------------------------------------------------------
+
+def _dt(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return ACP_F32
+    if t.dtype == torch.bfloat16:
+        return ACP_BF16
+    raise TypeError(f"unsupported dtype {t.dtype}; use float32 or bfloat16")
+
+
+def _dev(*ts):
+    for t in ts:
+        if not t.is_cuda:
+            raise ValueError("tensors must live on the GPU")
+        if not t.is_contiguous():
+            raise ValueError("tensors must be contiguous")
+    return ts[0].device
+
+
+def _stream(device) -> int:
+    return torch.cuda.current_stream(device).cuda_stream
+
+
+def _shape(q: torch.Tensor):
+    if q.dim() != 4:
+        raise ValueError("Q/K/V must be [B, H, L, d]")
+    return tuple(int(s) for s in q.shape)
+
+
+def workspace(q: torch.Tensor) -> torch.Tensor:
+    B, H, L, d = _shape(q)
+    n = acp_workspace_size(B, H, L, d, _dt(q))
+    return torch.empty(n, dtype=torch.uint8, device=q.device)
+
+
+def boundary(q, k, log_f, eps: float, ws: torch.Tensor | None = None) -> dict:
+    """Stage 1 of ACP; returns c, bound_u, delta, row_start, col_end, kept, flags."""
+    dev = _dev(q, k, log_f)
+    B, H, L, d = _shape(q)
+    if k.shape != q.shape or k.dtype != q.dtype or tuple(log_f.shape) != (B, H, L) \
+            or log_f.dtype != torch.float32:
+        raise ValueError("shape/dtype mismatch")
+    ws = workspace(q) if ws is None else ws
+    M = L // 64
+    out = {
+        "c": torch.empty((B, H, L), dtype=torch.float32, device=dev),
+        "bound_u": torch.empty((B, H), dtype=torch.float64, device=dev),
+        "delta": torch.empty((B, H), dtype=torch.float64, device=dev),
+        "row_start": torch.empty((B, H, M), dtype=torch.int32, device=dev),
+        "col_end": torch.empty((B, H, M), dtype=torch.int32, device=dev),
+        "kept": torch.empty((B, H), dtype=torch.int64, device=dev),
+        "flags": torch.empty((B, H), dtype=torch.int32, device=dev),
+    }
+    _check(acp_boundary(q.data_ptr(), k.data_ptr(), log_f.data_ptr(), _dt(q), B, H, L, d, eps,
+                        out["c"].data_ptr(), out["bound_u"].data_ptr(), out["delta"].data_ptr(),
+                        out["row_start"].data_ptr(), out["col_end"].data_ptr(),
+                        out["kept"].data_ptr(), out["flags"].data_ptr(), ws.data_ptr(),
+                        ws.numel(), _stream(dev)))
+    return out
+
+
+def forward(q, k, v, log_f, eps: float, ws: torch.Tensor | None = None, out=None):
+    """Returns (O, lse, ws); ws carries the plan and state the backward needs."""
+    dev = _dev(q, k, v, log_f)
+    B, H, L, d = _shape(q)
+    if k.shape != q.shape or v.shape != q.shape or k.dtype != q.dtype or v.dtype != q.dtype:
+        raise ValueError("Q, K, V must share shape and dtype")
+    if tuple(log_f.shape) != (B, H, L) or log_f.dtype != torch.float32:
+        raise ValueError("log_f must be float32 [B, H, L]")
+    ws = workspace(q) if ws is None else ws
+    if out is None:
+        o = torch.empty_like(q)
+        lse = torch.empty((B, H, L), dtype=torch.float32, device=dev)
+    else:
+        o, lse = out
+    _check(fox_attn_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), log_f.data_ptr(), _dt(q),
+                        B, H, L, d, eps, o.data_ptr(), lse.data_ptr(), ws.data_ptr(), ws.numel(),
+                        _stream(dev)))
+    return o, lse, ws
+
+
+def backward(q, k, v, do, ws: torch.Tensor, out=None):
+    """Returns (dQ, dK, dV, dlog_f) for the forward that filled `ws`."""
+    dev = _dev(q, k, v, do)
+    B, H, L, d = _shape(q)
+    if do.shape != q.shape or do.dtype != q.dtype:
+        raise ValueError("dO must match Q")
+    if out is None:
+        dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+        dlf = torch.empty((B, H, L), dtype=torch.float32, device=dev)
+    else:
+        dq, dk, dv, dlf = out
+    _check(fox_attn_bwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), do.data_ptr(), _dt(q),
+                        B, H, L, d, dq.data_ptr(), dk.data_ptr(), dv.data_ptr(), dlf.data_ptr(),
+                        ws.data_ptr(), ws.numel(), _stream(dev)))
+    return dq, dk, dv, dlf
+
+
+def plan_views(ws: torch.Tensor, B: int, H: int, L: int, d: int, dtype) -> dict:
+    """Views into a workspace of the plan that fox_attn_fwd wrote."""
+    dt = ACP_F32 if dtype == torch.float32 else ACP_BF16
+    lay = acp_plan_offsets(B, H, L, d, dt)
+    M = L // 64
+
+    def view(off, n, t):
+        nbytes = n * torch.empty((), dtype=t).element_size()
+        return ws[off:off + nbytes].view(t)
+
+    return {
+        "c": view(lay.c, B * H * L, torch.float32).view(B, H, L),
+        "bound_u": view(lay.bound_u, B * H, torch.float64).view(B, H),
+        "delta": view(lay.delta, B * H, torch.float64).view(B, H),
+        "row_start": view(lay.row_start, B * H * M, torch.int32).view(B, H, M),
+        "col_end": view(lay.col_end, B * H * M, torch.int32).view(B, H, M),
+        "kept": view(lay.kept, B * H, torch.int64).view(B, H),
+        "flags": view(lay.flags, B * H, torch.int32).view(B, H),
+    }

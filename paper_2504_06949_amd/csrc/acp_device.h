@@ -1,0 +1,84 @@
+// Device-side helpers shared by the library's kernels (gfx950 / CDNA4 only).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace acp {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+// Largest supported sequence length: the boundary kernel keeps 3 * (L / 64)
+// words of block corners and indices in LDS.
+constexpr int kMaxBlocks = 2048;
+constexpr int kBlock = 64;  // pruning grid: 64 x 64 blocks
+
+// ---- conversions ----------------------------------------------------------
+__device__ __forceinline__ double to_f64(float x) { return (double)x; }
+__device__ __forceinline__ double to_f64(__bf16 x) { return (double)(float)x; }
+__device__ __forceinline__ float to_f32(float x) { return x; }
+__device__ __forceinline__ float to_f32(__bf16 x) { return (float)x; }
+
+template <typename T> __device__ __forceinline__ T from_f32(float x);
+template <> __device__ __forceinline__ float from_f32<float>(float x) { return x; }
+template <> __device__ __forceinline__ __bf16 from_f32<__bf16>(float x) { return (__bf16)x; }
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+__device__ __forceinline__ float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
+
+// max that lets a NaN win, so that a NaN anywhere in Q or K reaches rho^2
+__device__ __forceinline__ double nan_max(double a, double b) {
+    return (b > a || b != b) ? b : a;
+}
+
+// ---- MFMA ------------------------------------------------------------------
+// v_mfma_f32_16x16x32_bf16.  Lane l = 16 g + r (g = l / 16, r = l % 16):
+//   A[i][k]: i = r, k = 8 g + t (t = 0..7, element t of the lane's bf16x8)
+//   B[k][j]: j = r, k = 8 g + t
+//   D[i][j]: j = r, i = 4 g + t (t = 0..3)
+__device__ __forceinline__ f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+// LDS transpose read (ds_read_b64_tr_b16).  Within every group of 16 lanes,
+// lane i receives element (i % 4) of the 8-byte chunks whose addresses lanes
+// 4t + i / 4 (t = 0..3) supplied.  If lane L of the group passes the address
+// of X[r0 + L / 4][c0 + 4 (L % 4)] of a row-major 16-bit matrix X, lane i gets
+// X[r0 + t][c0 + i] for t = 0..3: four rows of one column.
+__device__ __forceinline__ s16x4 lds_read_tr16(const __bf16* p) {
+    typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+    return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(p));
+}
+
+// Eight consecutive rows r0 .. r0 + 7 of column c0 + (lane % 16) of a row-major
+// bf16 tile in LDS with row stride `ld` elements, as an MFMA operand whose k
+// index runs over the rows.
+__device__ __forceinline__ bf16x8 lds_col8(const __bf16* tile, int ld, int r0, int c0, int r16) {
+    const __bf16* p0 = tile + (r0 + (r16 >> 2)) * ld + c0 + 4 * (r16 & 3);
+    s16x4 lo = lds_read_tr16(p0);
+    s16x4 hi = lds_read_tr16(p0 + 4 * ld);
+    bf16x8 out;
+    bf16x4 lo_b = __builtin_bit_cast(bf16x4, lo);
+    bf16x4 hi_b = __builtin_bit_cast(bf16x4, hi);
+    out[0] = lo_b[0]; out[1] = lo_b[1]; out[2] = lo_b[2]; out[3] = lo_b[3];
+    out[4] = hi_b[0]; out[5] = hi_b[1]; out[6] = hi_b[2]; out[7] = hi_b[3];
+    return out;
+}
+
+// ---- workgroup -> (head, block) mapping ------------------------------------
+// Workgroups are dealt round-robin to the 8 XCDs (each with its own L2).  This
+// renumbering gives every XCD a contiguous range of logical ids, so the blocks
+// of one head share an L2.
+__device__ __forceinline__ int xcd_logical_id(int bid, int nblocks) {
+    const int q = nblocks >> 3, r = nblocks & 7;
+    const int x = bid & 7, k = bid >> 3;
+    return x * q + (x < r ? x : r) + k;
+}
+
+}  // namespace acp

@@ -1,0 +1,74 @@
+// Host-side interface between the C ABI layer and the kernel launchers.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "acp.h"
+
+namespace acp {
+
+struct PlanArgs {
+    const void* Q;
+    const void* K;
+    const float* log_f;
+    bool bf16;
+    int B, H, L, d;
+    int nchunk;               // norm partials per (head, tensor)
+    double log_l_over_eps;    // log L - log eps, +inf for eps = 0
+    double* part;             // [B*H, 2, nchunk]
+    float* c;                 // [B*H, L]
+    double* u;                // [B*H]
+    double* delta;            // [B*H]
+    int* row_start;           // [B*H, M]
+    int* col_end;             // [B*H, M]
+    long long* kept;          // [B*H]
+    int* flags;               // [B*H]
+};
+
+struct FwdArgs {
+    const void* Q;
+    const void* K;
+    const void* V;
+    bool bf16;
+    int B, H, L, d;
+    const float* c;
+    const int* row_start;
+    void* O;
+    float* O32;
+    float* lse;
+    float* lse2;
+};
+
+struct BwdArgs {
+    const void* Q;
+    const void* K;
+    const void* V;
+    const void* dO;
+    bool bf16;
+    int B, H, L, d;
+    const float* c;
+    const int* row_start;
+    const int* col_end;
+    const float* lse2;
+    const float* O32;
+    float* dsum;
+    float* rowsum;
+    float* colsum;
+    void* dQ;
+    void* dK;
+    void* dV;
+    float* dlog_f;
+};
+
+// Tracing hooks: no-ops unless acp_timing_enable(1) was called.
+void trace_begin(int kernel, hipStream_t s);
+void trace_end(int kernel, hipStream_t s);
+
+int norm_chunks(int L);
+hipError_t launch_plan(const PlanArgs& a, hipStream_t s);
+hipError_t launch_fwd(const FwdArgs& a, hipStream_t s);
+hipError_t launch_bwd(const BwdArgs& a, hipStream_t s);
+
+}  // namespace acp

@@ -1,0 +1,323 @@
+// Forgetting Attention forward over the blocks kept by ACP (paper Sec. 2,
+// eq. 1-2 and its FlashAttention paragraph; Sec. 3, "Two-stage implementation":
+// each query block starts at its boundary block, and the K/V of pruned blocks
+// are never loaded).
+//
+// Logits are kept in log2 units, in a frame local to the workgroup: with r the
+// cumulative gate at the workgroup's first query,
+//   y_ij = (q_i . k_j) * log2(e)/sqrt(d) - (c_j - r) * log2(e).
+// The row term (c_i - r) log2(e) is constant along a row and cancels in the
+// softmax; it returns only in the log-sum-exp,
+//   L_i = LSE_i log2(e) = max_j y_ij + log2(l_i) + (c_i - r) log2(e).
+// Every quantity stays of the size of the decay inside the kept window, however
+// long the sequence (c itself grows without bound).  L_i is frame-free; the
+// backward recomputes P_ij = 2^(q_i.k_j log2(e)/sqrt(d) + (c_i - c_j) log2(e) - L_i)
+// in frames of its own.
+#include "acp_device.h"
+#include "acp_internal.h"
+
+namespace acp {
+
+// ---------------------------------------------------------------------------
+// bf16 path: v_mfma_f32_16x16x32_bf16, fp32 accumulation.
+//
+// Workgroup = 4 waves = 128 queries (two 64-row pruning blocks); wave w owns
+// 32 queries that all sit in one pruning row, so a pruned or non-causal tile is
+// skipped wave-uniformly and no pruned entry is ever computed.  Key/value tiles
+// of 64 rows are double-buffered in LDS (row-major, padded); V^T operands come
+// from LDS transpose reads.
+//
+// S^T = K Q^T is computed (keys x queries) so that each lane holds one query and
+// eight consecutive keys of P afterwards, which is exactly the B operand of
+// O^T = V^T P^T.  For that, the A-operand rows of S^T are read from K in the
+// order krow(kt, r) = 32 (kt / 2) + 8 (r / 4) + 4 (kt % 2) + r % 4.
+// ---------------------------------------------------------------------------
+
+constexpr int kFwdThreads = 256;
+constexpr int kFwdRows = 128;
+
+template <int D>
+struct alignas(16) FwdSmem {
+    static constexpr int LD = D + 8;
+    alignas(16) __bf16 k[2][64 * LD];
+    __bf16 v[2][64 * LD];
+    float kb[2][64];   // key bias -(c_j - r) log2(e)
+};
+
+template <int D>
+__global__ __launch_bounds__(kFwdThreads) void fwd_bf16_kernel(
+    const __bf16* __restrict__ Q, const __bf16* __restrict__ K, const __bf16* __restrict__ V,
+    const float* __restrict__ cg, const int* __restrict__ row_start,
+    __bf16* __restrict__ O, float* __restrict__ O32, float* __restrict__ lse,
+    float* __restrict__ lse2, int L, int M, int nqb, int nblocks, float kscale) {
+    constexpr int LD = D + 8;
+    constexpr int NDS = D / 32;                     // k-steps over the head dim
+    constexpr int NDT = D / 16;                     // output tiles over the head dim
+    constexpr int CPR = D / 8;                      // 16-byte pieces per row
+    constexpr int CH = 64 * CPR / kFwdThreads;      // pieces per thread per tile
+    __shared__ FwdSmem<D> sm;
+
+    const int lid = xcd_logical_id(blockIdx.x, nblocks);
+    const int bh = lid / nqb;
+    const int qb = nqb - 1 - (lid % nqb);           // longest rows first
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int g = lane >> 4, r16 = lane & 15;
+    const int q0 = qb * kFwdRows;
+    const int wq0 = q0 + 32 * w;
+    const bool wave_on = wq0 < L;
+    const int mw = wq0 / 64;
+    const int m0 = q0 / 64;
+    const size_t head = (size_t)bh * L;
+    const int n_lo = row_start[(size_t)bh * M + m0];
+    const int n_hi = min(m0 + 1, M - 1);
+    const int w_lo = wave_on ? row_start[(size_t)bh * M + mw] : (1 << 30);
+    const float cref = cg[head + q0];
+
+    bf16x8 qf[2][NDS];
+    if (wave_on) {
+#pragma unroll
+        for (int qt = 0; qt < 2; ++qt)
+#pragma unroll
+            for (int ds = 0; ds < NDS; ++ds)
+                qf[qt][ds] = *reinterpret_cast<const bf16x8*>(
+                    Q + (head + wq0 + 16 * qt + r16) * D + 32 * ds + 8 * g);
+    }
+
+    uint4 kreg[CH], vreg[CH];
+    float4 nreg = make_float4(0.f, 0.f, 0.f, 0.f);
+    auto gload = [&](int n) {
+        const __bf16* kb = K + (head + (size_t)64 * n) * D;
+        const __bf16* vb = V + (head + (size_t)64 * n) * D;
+#pragma unroll
+        for (int c = 0; c < CH; ++c) {
+            const int i = tid + kFwdThreads * c;
+            kreg[c] = *reinterpret_cast<const uint4*>(kb + i * 8);
+            vreg[c] = *reinterpret_cast<const uint4*>(vb + i * 8);
+        }
+        if (tid < 16) nreg = *reinterpret_cast<const float4*>(cg + head + 64 * n + 4 * tid);
+    };
+    auto sstore = [&](int buf) {
+#pragma unroll
+        for (int c = 0; c < CH; ++c) {
+            const int i = tid + kFwdThreads * c;
+            const int row = i / CPR, ch = i % CPR;
+            *reinterpret_cast<uint4*>(&sm.k[buf][row * LD + 8 * ch]) = kreg[c];
+            *reinterpret_cast<uint4*>(&sm.v[buf][row * LD + 8 * ch]) = vreg[c];
+        }
+        if (tid < 16) {
+            const float4 b = make_float4(-((nreg.x - cref) * kLog2e), -((nreg.y - cref) * kLog2e),
+                                         -((nreg.z - cref) * kLog2e), -((nreg.w - cref) * kLog2e));
+            *reinterpret_cast<float4*>(&sm.kb[buf][4 * tid]) = b;
+        }
+    };
+
+    f32x4 acc[2][NDT];
+#pragma unroll
+    for (int qt = 0; qt < 2; ++qt)
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt) acc[qt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    float mrun[2] = {-INFINITY, -INFINITY};
+    float lrun[2] = {0.f, 0.f};
+
+    gload(n_lo);
+    sstore(0);
+    int buf = 0;
+    for (int n = n_lo; n <= n_hi; ++n) {
+        __syncthreads();
+        const bool more = n < n_hi;
+        if (more) gload(n + 1);
+        if (n >= w_lo && n <= mw) {
+            const __bf16* ktile = sm.k[buf];
+            const __bf16* vtile = sm.v[buf];
+            const float* nc = sm.kb[buf];
+            // S^T tiles: s[kt][qt] = K[krow(kt)] Q^T
+            f32x4 s[4][2];
+#pragma unroll
+            for (int kt = 0; kt < 4; ++kt) {
+                const int krow = 32 * (kt >> 1) + 8 * (r16 >> 2) + 4 * (kt & 1) + (r16 & 3);
+                s[kt][0] = f32x4{0.f, 0.f, 0.f, 0.f};
+                s[kt][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int ds = 0; ds < NDS; ++ds) {
+                    const bf16x8 a = *reinterpret_cast<const bf16x8*>(ktile + krow * LD + 32 * ds + 8 * g);
+                    s[kt][0] = mfma16(a, qf[0][ds], s[kt][0]);
+                    s[kt][1] = mfma16(a, qf[1][ds], s[kt][1]);
+                }
+            }
+            // the lane's keys are 32 ks + 8 g + j, j = 0..7 (j < 4 from tile 2ks)
+            float nk[2][8];
+#pragma unroll
+            for (int ks = 0; ks < 2; ++ks) {
+                const float4 lo = *reinterpret_cast<const float4*>(nc + 32 * ks + 8 * g);
+                const float4 hi = *reinterpret_cast<const float4*>(nc + 32 * ks + 8 * g + 4);
+                nk[ks][0] = lo.x; nk[ks][1] = lo.y; nk[ks][2] = lo.z; nk[ks][3] = lo.w;
+                nk[ks][4] = hi.x; nk[ks][5] = hi.y; nk[ks][6] = hi.z; nk[ks][7] = hi.w;
+            }
+            const bool diag = (n == mw);
+            bf16x8 pf[2][2];
+#pragma unroll
+            for (int qt = 0; qt < 2; ++qt) {
+                const int query = wq0 + 16 * qt + r16;
+                float y[2][8];
+                float mx = -INFINITY;
+#pragma unroll
+                for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) {
+                        float v = __builtin_fmaf(s[2 * ks + (j >> 2)][qt][j & 3], kscale, nk[ks][j]);
+                        if (diag && (64 * n + 32 * ks + 8 * g + j) > query) v = -INFINITY;
+                        y[ks][j] = v;
+                        mx = fmaxf(mx, v);
+                    }
+                mx = fmaxf(mx, __shfl_xor(mx, 16));
+                mx = fmaxf(mx, __shfl_xor(mx, 32));
+                const float mnew = fmaxf(mrun[qt], mx);
+                const float alpha = fast_exp2(mrun[qt] - mnew);
+                mrun[qt] = mnew;
+                float l = lrun[qt] * alpha;
+#pragma unroll
+                for (int dt = 0; dt < NDT; ++dt) acc[qt][dt] *= alpha;
+#pragma unroll
+                for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) {
+                        const float p = fast_exp2(y[ks][j] - mnew);
+                        l += p;
+                        pf[qt][ks][j] = (__bf16)p;
+                    }
+                lrun[qt] = l;
+            }
+            // O^T += V^T P^T
+#pragma unroll
+            for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+                for (int ks = 0; ks < 2; ++ks) {
+                    const bf16x8 a = lds_col8(vtile, LD, 32 * ks + 8 * g, 16 * dt, r16);
+                    acc[0][dt] = mfma16(a, pf[0][ks], acc[0][dt]);
+                    acc[1][dt] = mfma16(a, pf[1][ks], acc[1][dt]);
+                }
+        }
+        if (more) sstore(buf ^ 1);
+        buf ^= 1;
+    }
+
+    if (!wave_on) return;
+#pragma unroll
+    for (int qt = 0; qt < 2; ++qt) {
+        float lt = lrun[qt];
+        lt += __shfl_xor(lt, 16);
+        lt += __shfl_xor(lt, 32);
+        const float inv = 1.0f / lt;
+        const int query = wq0 + 16 * qt + r16;
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt) {
+            const f32x4 o = acc[qt][dt] * inv;
+            const size_t off = (head + query) * D + 16 * dt + 4 * g;
+            *reinterpret_cast<f32x4*>(O32 + off) = o;
+            bf16x4 ob;
+            ob[0] = (__bf16)o[0]; ob[1] = (__bf16)o[1]; ob[2] = (__bf16)o[2]; ob[3] = (__bf16)o[3];
+            *reinterpret_cast<bf16x4*>(O + off) = ob;
+        }
+        if (g == 0) {
+            const float l2 = mrun[qt] + fast_log2(lt) + (cg[head + query] - cref) * kLog2e;
+            lse2[head + query] = l2;
+            lse[head + query] = l2 * kLn2;
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// fp32 path: plain VALU arithmetic, one thread per query, 64 queries (one
+// pruning row) per workgroup; K/V tiles staged in LDS.
+// ---------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(64) void fwd_f32_kernel(
+    const float* __restrict__ Q, const float* __restrict__ K, const float* __restrict__ V,
+    const float* __restrict__ cg, const int* __restrict__ row_start,
+    float* __restrict__ O, float* __restrict__ O32, float* __restrict__ lse,
+    float* __restrict__ lse2, int L, int M, float kscale) {
+    __shared__ float ks[64 * D];
+    __shared__ float vs[64 * D];
+    __shared__ float nc[64];
+    const int bh = blockIdx.x / M, m = blockIdx.x % M, t = threadIdx.x;
+    const size_t head = (size_t)bh * L;
+    const int query = 64 * m + t;
+    const float cref = cg[head + 64 * m];
+    float q[D], acc[D];
+#pragma unroll
+    for (int k = 0; k < D; ++k) { q[k] = Q[(head + query) * D + k]; acc[k] = 0.f; }
+    float mrun = -INFINITY, lrun = 0.f;
+    const int n0 = row_start[(size_t)bh * M + m];
+    for (int n = n0; n <= m; ++n) {
+        __syncthreads();
+        for (int i = t; i < 64 * D; i += 64) {
+            ks[i] = K[(head + 64 * n) * D + i];
+            vs[i] = V[(head + 64 * n) * D + i];
+        }
+        nc[t] = -((cg[head + 64 * n + t] - cref) * kLog2e);
+        __syncthreads();
+        const int jmax = (n == m) ? t : 63;
+        for (int j = 0; j <= jmax; ++j) {
+            float s = 0.f;
+#pragma unroll
+            for (int k = 0; k < D; ++k) s = __builtin_fmaf(q[k], ks[j * D + k], s);
+            const float y = __builtin_fmaf(s, kscale, nc[j]);
+            if (y > mrun) {
+                const float alpha = fast_exp2(mrun - y);
+                lrun *= alpha;
+#pragma unroll
+                for (int k = 0; k < D; ++k) acc[k] *= alpha;
+                mrun = y;
+            }
+            const float p = fast_exp2(y - mrun);
+            lrun += p;
+#pragma unroll
+            for (int k = 0; k < D; ++k) acc[k] = __builtin_fmaf(p, vs[j * D + k], acc[k]);
+        }
+    }
+    const float inv = 1.0f / lrun;
+#pragma unroll
+    for (int k = 0; k < D; ++k) {
+        const float o = acc[k] * inv;
+        O[(head + query) * D + k] = o;
+        O32[(head + query) * D + k] = o;
+    }
+    const float l2 = mrun + fast_log2(lrun) + (cg[head + query] - cref) * kLog2e;
+    lse2[head + query] = l2;
+    lse[head + query] = l2 * kLn2;
+}
+
+// ---------------------------------------------------------------------------
+hipError_t launch_fwd(const FwdArgs& a, hipStream_t s) {
+    const int BH = a.B * a.H, M = a.L / 64;
+    const float kscale = kLog2e / sqrtf((float)a.d);
+    trace_begin(ACP_K_FWD, s);
+    if (a.bf16) {
+        const int nqb = (a.L + kFwdRows - 1) / kFwdRows;
+        const int nblocks = BH * nqb;
+        if (a.d == 64)
+            hipLaunchKernelGGL(fwd_bf16_kernel<64>, dim3(nblocks), dim3(kFwdThreads), 0, s,
+                               (const __bf16*)a.Q, (const __bf16*)a.K, (const __bf16*)a.V, a.c,
+                               a.row_start, (__bf16*)a.O, a.O32, a.lse, a.lse2, a.L, M, nqb,
+                               nblocks, kscale);
+        else
+            hipLaunchKernelGGL(fwd_bf16_kernel<128>, dim3(nblocks), dim3(kFwdThreads), 0, s,
+                               (const __bf16*)a.Q, (const __bf16*)a.K, (const __bf16*)a.V, a.c,
+                               a.row_start, (__bf16*)a.O, a.O32, a.lse, a.lse2, a.L, M, nqb,
+                               nblocks, kscale);
+    } else {
+        if (a.d == 64)
+            hipLaunchKernelGGL(fwd_f32_kernel<64>, dim3(BH * M), dim3(64), 0, s,
+                               (const float*)a.Q, (const float*)a.K, (const float*)a.V, a.c,
+                               a.row_start, (float*)a.O, a.O32, a.lse, a.lse2, a.L, M, kscale);
+        else
+            hipLaunchKernelGGL(fwd_f32_kernel<128>, dim3(BH * M), dim3(64), 0, s,
+                               (const float*)a.Q, (const float*)a.K, (const float*)a.V, a.c,
+                               a.row_start, (float*)a.O, a.O32, a.lse, a.lse2, a.L, M, kscale);
+    }
+    const hipError_t e = hipGetLastError();
+    trace_end(ACP_K_FWD, s);
+    return e;
+}
+
+}  // namespace acp

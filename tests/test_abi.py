@@ -1,0 +1,117 @@
+"""The C ABI on the CPU: the library loads, exports what include/acp.h declares,
+and rejects bad arguments on the host before launching anything."""
+import ctypes
+import math
+
+import pytest
+
+from paper_2504_06949_amd import acp
+from tests._helpers import ensure_built
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _lib():
+    ensure_built()
+
+
+def test_every_declared_symbol_is_exported():
+    names = acp.header_functions()
+    assert set(names) == {"acp_workspace_size", "acp_plan_offsets", "acp_boundary",
+                          "fox_attn_fwd", "fox_attn_bwd", "acp_timing_enable",
+                          "acp_timing_reset", "acp_timing_read", "acp_status_string",
+                          "acp_last_error"}
+    lib = ctypes.CDLL(acp.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_status_strings():
+    assert acp.acp_status_string(acp.ACP_OK) == "ok"
+    for s in (acp.ACP_EINVAL, acp.ACP_EUNSUPPORTED, acp.ACP_EWORKSPACE, acp.ACP_EHIP):
+        assert acp.acp_status_string(s) not in ("ok", "unknown status")
+    assert acp.acp_status_string(99) == "unknown status"
+
+
+def test_workspace_size_and_layout():
+    n = acp.acp_workspace_size(8, 12, 4096, 64, acp.ACP_BF16)
+    lay = acp.acp_plan_offsets(8, 12, 4096, 64, acp.ACP_BF16)
+    assert lay.total == n
+    offs = [lay.c, lay.bound_u, lay.delta, lay.row_start, lay.col_end, lay.kept,
+            lay.flags]
+    assert all(o % 256 == 0 for o in offs)
+    assert offs == sorted(offs) and len(set(offs)) == len(offs)
+    BHL = 8 * 12 * 4096
+    assert lay.bound_u - lay.c >= 4 * BHL
+    # the float32 copy of O dominates: at least B*H*L*d*4 bytes
+    assert n >= BHL * 64 * 4
+    assert acp.acp_workspace_size(8, 12, 4096, 128, acp.ACP_BF16) > n
+
+
+@pytest.mark.parametrize("args,status", [
+    ((0, 1, 64, 64), acp.ACP_EINVAL),
+    ((1, -2, 64, 64), acp.ACP_EINVAL),
+    ((1, 1, 64, 96), acp.ACP_EUNSUPPORTED),
+    ((1, 1, 100, 64), acp.ACP_EUNSUPPORTED),
+    ((1, 1, 64 * 2049, 64), acp.ACP_EUNSUPPORTED),
+    ((256, 256, 64, 64), acp.ACP_EUNSUPPORTED),
+])
+def test_shape_validation(args, status):
+    with pytest.raises(acp.AcpError) as e:
+        acp.acp_workspace_size(*args, acp.ACP_BF16)
+    assert e.value.status == status
+
+
+def _fwd(**kw):
+    a = dict(Q=16, K=16, V=16, log_f=16, dt=acp.ACP_BF16, B=1, H=1, L=64, d=64, eps=1e-4,
+             O=16, lse=16, ws=16, ws_bytes=1 << 40, stream=None)
+    a.update(kw)
+    return acp.fox_attn_fwd(*a.values())
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(Q=0), acp.ACP_EINVAL),
+    (dict(V=8), acp.ACP_EINVAL),              # misaligned
+    (dict(lse=0), acp.ACP_EINVAL),
+    (dict(eps=-1e-3), acp.ACP_EINVAL),
+    (dict(eps=1.0), acp.ACP_EINVAL),
+    (dict(eps=math.nan), acp.ACP_EINVAL),
+    (dict(eps=math.inf), acp.ACP_EINVAL),
+    (dict(dt=7), acp.ACP_EINVAL),
+    (dict(d=32), acp.ACP_EUNSUPPORTED),
+    (dict(L=96), acp.ACP_EUNSUPPORTED),
+    (dict(ws_bytes=1000), acp.ACP_EWORKSPACE),
+    (dict(ws=0), acp.ACP_EINVAL),
+])
+def test_forward_rejects_before_launch(kw, status):
+    assert _fwd(**kw) == status
+    assert acp.acp_last_error() != ""
+
+
+def test_backward_and_boundary_reject_before_launch():
+    st = acp.fox_attn_bwd(16, 16, 16, 0, acp.ACP_BF16, 1, 1, 64, 64, 16, 16, 16, 16, 16,
+                          1 << 40, None)
+    assert st == acp.ACP_EINVAL and "dO" in acp.acp_last_error()
+    st = acp.fox_attn_bwd(16, 16, 16, 16, acp.ACP_BF16, 1, 1, 64, 64, 16, 16, 16, 16, 16, 8,
+                          None)
+    assert st == acp.ACP_EWORKSPACE
+    st = acp.acp_boundary(16, 16, 16, acp.ACP_F32, 1, 1, 64, 64, 0.5, 16, 16, 16, 16, 16, 0, 16,
+                          16, 1 << 40, None)
+    assert st == acp.ACP_EINVAL and "kept" in acp.acp_last_error()
+    st = acp.acp_boundary(16, 16, 16, acp.ACP_F32, 1, 1, 64, 64, 1.5, 16, 16, 16, 16, 16, 16,
+                          16, 16, 1 << 40, None)
+    assert st == acp.ACP_EINVAL
+
+
+def test_tensor_helpers_refuse_cpu_tensors():
+    import torch
+    q = torch.zeros(1, 1, 64, 64)
+    with pytest.raises(ValueError):
+        acp.forward(q, q, q, torch.zeros(1, 1, 64), 1e-4)
+
+
+def test_timing_state_without_launches():
+    acp.acp_timing_reset()
+    t = acp.acp_timing_read()
+    assert set(t) == set(acp.K_NAMES) and all(v == (0, 0.0) for v in t.values())
+    acp.acp_timing_enable(True)
+    acp.acp_timing_enable(False)

@@ -1,0 +1,120 @@
+"""Stage 1 on the GPU against the oracle: c, U, delta, row_start, col_end and the
+kept-block count must be bit-identical, for every head of every workload."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as orc
+from paper_2504_06949_amd import acp, workloads
+from tests._helpers import EPS, ensure_built, to_gpu
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _lib():
+    ensure_built()
+
+
+def _gpu_plan(x, eps):
+    g = to_gpu({n: x[n] for n in ("q", "k", "log_f")})
+    out = acp.boundary(g["q"], g["k"], g["log_f"], eps)
+    torch.cuda.synchronize()
+    return {n: t.cpu().numpy() for n, t in out.items()}
+
+
+def _check_plan(x, got, eps, brute_heads=()):
+    B, H, L, d = x["q"].shape
+    lf = x["log_f"].numpy()
+    c_ref = orc.cumsum_log_gates(lf)
+    np.testing.assert_array_equal(got["c"], c_ref)
+    for b in range(B):
+        for h in range(H):
+            q = x["q"][b, h].float().numpy()
+            k = x["k"][b, h].float().numpy()
+            rq, rk = orc.row_norm_sq_max(q), orc.row_norm_sq_max(k)
+            U = orc.logit_bound(rq, rk, d)
+            delta = orc.threshold(U, L, eps)
+            assert got["bound_u"][b, h] == U, (b, h)
+            assert got["delta"][b, h] == delta, (b, h)
+            method = "bruteforce" if (b, h) in brute_heads else "topright"
+            kb = (orc.block_keep_bruteforce if method == "bruteforce" else
+                  orc.block_keep_topright)(c_ref[b, h], delta)
+            rs, ce = orc.boundary_from_block_keep(kb)
+            np.testing.assert_array_equal(got["row_start"][b, h], rs, err_msg=f"{b},{h}")
+            np.testing.assert_array_equal(got["col_end"][b, h], ce, err_msg=f"{b},{h}")
+            assert got["kept"][b, h] == orc.kept_tiles(rs)
+            assert got["flags"][b, h] == 0
+
+
+@pytest.mark.parametrize("name", ["tiny", "125m", "360m", "760m", "adv"])
+def test_boundary_bit_exact(name):
+    w = workloads.WORKLOADS[name]
+    print(f"case: boundary {w.describe()}", flush=True)
+    x = workloads.generate(w, with_grad=False)
+    got = _gpu_plan(x, w.eps)
+    brute = {(0, 0), (0, 1)} if w.L <= 4096 else set()
+    _check_plan(x, got, w.eps, brute_heads=brute)
+    if name == "adv":
+        # the sweep spans nothing-pruned to nearly-all-pruned heads
+        frac = 1.0 - got["kept"] / orc.causal_tiles(w.M)
+        assert frac.min() == 0.0 and frac.max() > 0.9
+
+
+def test_boundary_many_heads_exercise_sqrt_and_division():
+    # 4096 heads of one block each, Q/K rows scaled per head over six decades:
+    # U and delta must match the host's IEEE float64 arithmetic bit for bit.
+    g = torch.Generator().manual_seed(11)
+    B, H, L, d = 2, 2048, 64, 64
+    sq = torch.exp(torch.randn(B, H, 1, 1, generator=g, dtype=torch.float64) * 3).float()
+    sk = torch.exp(torch.randn(B, H, 1, 1, generator=g, dtype=torch.float64) * 3).float()
+    x = {"q": (torch.randn(B, H, L, d, generator=g) * sq).bfloat16(),
+         "k": (torch.randn(B, H, L, d, generator=g) * sk).bfloat16(),
+         "log_f": workloads.log_sigmoid_f32_t(torch.randn(B, H, L, generator=g) + 1.0)}
+    got = _gpu_plan(x, EPS)
+    _check_plan(x, got, EPS)
+
+
+def test_boundary_eps_zero_and_extremes():
+    w = workloads.custom("ext", 1, 3, 1024, 64, "bf16", 5, mu=(0.0, 2.0, 4.0))
+    x = workloads.generate(w, with_grad=False)
+    got = _gpu_plan(x, 0.0)
+    assert np.all(got["row_start"] == 0)
+    assert np.all(got["delta"] == -np.inf)
+    _check_plan(x, got, 0.0)
+    x["log_f"] = torch.full_like(x["log_f"], -1e4)
+    got = _gpu_plan(x, EPS)
+    assert np.all(got["row_start"] == np.arange(16))
+    _check_plan(x, got, EPS)
+    x["log_f"] = torch.zeros_like(x["log_f"])
+    got = _gpu_plan(x, EPS)
+    assert np.all(got["row_start"] == 0)
+
+
+def test_boundary_flags_bad_gates():
+    w = workloads.custom("flags", 1, 4, 256, 64, "f32", 6, mu=(2.0,))
+    x = workloads.generate(w, with_grad=False)
+    lf = x["log_f"].clone()
+    lf[0, 1, 17] = 0.25           # f > 1
+    lf[0, 2, 100] = float("nan")
+    lf[0, 3, 0] = -1e-30          # tiny gate next to ordinary ones: sums not exact
+    x["log_f"] = lf
+    got = _gpu_plan(x, EPS)
+    assert got["flags"][0, 0] == 0
+    assert got["flags"][0, 1] & acp.FLAG_POSITIVE_GATE
+    assert got["flags"][0, 2] & acp.FLAG_NONFINITE_GATE
+    assert got["flags"][0, 3] & acp.FLAG_INEXACT_CUMSUM
+    # span check agrees with the oracle's own bound
+    assert orc.cumsum_span_bits(lf[0, 3].numpy()) > 53
+    assert orc.cumsum_span_bits(lf[0, 0].numpy()) <= 52
+
+
+def test_boundary_is_deterministic():
+    w = workloads.WORKLOADS["125m"]
+    x = workloads.generate(w, with_grad=False)
+    a = _gpu_plan(x, w.eps)
+    b = _gpu_plan(x, w.eps)
+    for n in a:
+        np.testing.assert_array_equal(a[n], b[n])
