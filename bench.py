@@ -37,7 +37,7 @@ def _flops(w, kept_tiles):
     }
 
 
-def run_workload(name: str, steps: int, warmup: int, eps_override=None):
+def run_workload(name: str, steps: int, warmup: int, eps_override=None, unpruned=True):
     import torch
     from paper_2504_06949_amd import acp, workloads
 
@@ -69,7 +69,7 @@ def run_workload(name: str, steps: int, warmup: int, eps_override=None):
         torch.cuda.synchronize()
         return t0.elapsed_time(t1) / steps
 
-    ms_dense = timed(0.0)
+    ms_dense = timed(0.0) if unpruned else float("nan")
     ms = timed(eps)
     kept = int(acp.plan_views(ws, w.B, w.H, w.L, w.d, g["q"].dtype)["kept"].sum().item())
     # per-kernel durations from HIP events the library records on this stream
@@ -123,6 +123,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="125m")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--skip-unpruned", action="store_true",
+                    help="do not time the eps = 0 (nothing pruned) reference run")
     ap.add_argument("--extra", action="store_true",
                     help="also time the 360M/760M-shaped and adversarial layers")
     args = ap.parse_args()
@@ -137,7 +139,7 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
 
-    res = run_workload(args.workload, args.steps, args.warmup)
+    res = run_workload(args.workload, args.steps, args.warmup, unpruned=not args.skip_unpruned)
     w = res["w"]
     fl = _flops(w, res["kept"])
     pk = res["per_kernel_ms"]
@@ -164,8 +166,8 @@ def main():
         "executed_tflops": round(fl["executed"] / (res["ms"] * 1e-3) / 1e12, 2),
         "mfma_frac_executed": round(fl["executed"] / (res["ms"] * 1e-3) / 1e12
                                     / PEAK_BF16_TFLOPS, 4),
-        "ms_unpruned": round(res["ms_dense"], 4),
-        "speedup_vs_unpruned": round(res["ms_dense"] / res["ms"], 3),
+        "ms_unpruned": None if args.skip_unpruned else round(res["ms_dense"], 4),
+        "speedup_vs_unpruned": None if args.skip_unpruned else round(res["ms_dense"] / res["ms"], 3),
         "per_kernel_ms": {k: round(v, 4) for k, v in pk.items()},
         "boundary_share": round((pk["rownorm"] + pk["plan"]) / res["ms"], 4),
         "roofline": {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 2),

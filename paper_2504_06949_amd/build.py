@@ -20,12 +20,15 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libacp.so")
 BUILD_DIR = os.path.join(PKG, "_build")
 
-SOURCES = ["acp_api.cpp", "acp_plan.hip", "fox_fwd.hip", "fox_bwd.hip"]
+SOURCES = ["acp_api.cpp", "acp_plan.hip", "fox_fwd.hip", "fox_bwd.hip", "fox_bwd_mfma.hip"]
 
 COMMON = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
     # keep hipcc from forming packed fp32 VALU ops (v_pk_*_f32)
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # MFMA results in ordinary VGPRs: the softmax reads them directly, with no
+    # copies between the accumulation and architectural register files
+    "-mllvm", "-amdgpu-mfma-vgpr-form=1",
     "-Wno-unused-command-line-argument",
     "-I", INCLUDE, "-I", CSRC,
 ]

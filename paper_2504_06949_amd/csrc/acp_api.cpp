@@ -279,6 +279,7 @@ acp_status fox_attn_fwd(const void* Q, const void* K, const void* V, const float
     f.B = B; f.H = H; f.L = L; f.d = d;
     f.c = (const float*)(w + y.c);
     f.row_start = (const int*)(w + y.rs);
+    f.u = (const double*)(w + y.u);
     f.O = O;
     f.O32 = (float*)(w + y.o32);
     f.lse = lse;

@@ -35,6 +35,7 @@ struct FwdArgs {
     int B, H, L, d;
     const float* c;
     const int* row_start;
+    const double* u;          // [B*H] logit bound U
     void* O;
     float* O32;
     float* lse;
@@ -70,5 +71,7 @@ int norm_chunks(int L);
 hipError_t launch_plan(const PlanArgs& a, hipStream_t s);
 hipError_t launch_fwd(const FwdArgs& a, hipStream_t s);
 hipError_t launch_bwd(const BwdArgs& a, hipStream_t s);
+hipError_t launch_dq_bf16(const BwdArgs& a, hipStream_t s);
+hipError_t launch_dkdv_bf16(const BwdArgs& a, hipStream_t s);
 
 }  // namespace acp

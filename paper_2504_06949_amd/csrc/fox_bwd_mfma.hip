@@ -1,0 +1,466 @@
+// bf16 backward passes of Forgetting Attention over the blocks kept by ACP
+// (v_mfma_f32_16x16x32_bf16, fp32 accumulation).  The formulas are the chain
+// rule through eq. 2 and the cumulative gates (see fox_bwd.hip); P is
+// recomputed from the forward's frame-free log-sum-exp L_i = LSE_i log2(e):
+//   P_ij = 2^(q_i.k_j log2(e)/sqrt(d) + (c_i - c_j) log2(e) - L_i),
+// in a frame r local to each workgroup (the cumulative gate at its first row),
+// so that P_ij = 2^(fma(q.k, log2(e)/sqrt(d), -(c_j - r) log2(e)) + a_i) with
+// a_i = (c_i - r) log2(e) - L_i.
+//
+// Both passes use 4 waves of 32 rows (two 64-row pruning blocks per workgroup),
+// so a pruned or non-causal tile is skipped wave-uniformly, and work through
+// each 64-row tile of the other operand in two halves of 32 to keep register
+// pressure low.  Tiles are double-buffered in LDS (row-major, padded); operands
+// whose contraction runs over sequence positions come from LDS transpose reads.
+#include <type_traits>
+
+#include "acp_device.h"
+#include "acp_internal.h"
+
+namespace acp {
+
+constexpr int kBwdThreads = 256;
+constexpr int kBwdRows = 128;
+
+// ---------------------------------------------------------------------------
+// dQ pass: one workgroup per 128 queries, loop over kept key blocks.
+// S^T = K Q^T and dP^T = V dO^T are formed keys x queries so that dS^T lands
+// in the B-operand layout of dQ^T = K^T dS^T.  The A-operand rows are read in
+// the order krow = 32 h + 8 (r / 4) + 4 t + r % 4 (half h, subtile t).
+// ---------------------------------------------------------------------------
+template <int D>
+struct alignas(16) DqSmem {
+    static constexpr int LD = D + 8;
+    alignas(16) __bf16 k[2][64 * LD];
+    __bf16 v[2][64 * LD];
+    float kb[2][64];   // key bias -(c_j - r) log2(e)
+};
+
+template <int D>
+__global__ __launch_bounds__(kBwdThreads) void dq_bf16_kernel(
+    const __bf16* __restrict__ Q, const __bf16* __restrict__ K, const __bf16* __restrict__ V,
+    const __bf16* __restrict__ dO, const float* __restrict__ cg,
+    const int* __restrict__ row_start, const float* __restrict__ lse2,
+    float* __restrict__ dsum, __bf16* __restrict__ dQ, float* __restrict__ rowsum,
+    int L, int M, int nqb, int nblocks, float kscale, float qscale) {
+    constexpr int LD = D + 8;
+    constexpr int NDS = D / 32;
+    constexpr int NDT = D / 16;
+    constexpr int CPR = D / 8;
+    constexpr int CH = 64 * CPR / kBwdThreads;
+    __shared__ DqSmem<D> sm;
+
+    const int lid = xcd_logical_id(blockIdx.x, nblocks);
+    const int bh = lid / nqb;
+    const int qb = nqb - 1 - (lid % nqb);
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int g = lane >> 4, r16 = lane & 15;
+    const int q0 = qb * kBwdRows;
+    const int wq0 = q0 + 32 * w;
+    const bool wave_on = wq0 < L;
+    const int mw = wq0 / 64;
+    const int m0 = q0 / 64;
+    const size_t head = (size_t)bh * L;
+    const int n_lo = row_start[(size_t)bh * M + m0];
+    const int n_hi = min(m0 + 1, M - 1);
+    const int w_lo = wave_on ? row_start[(size_t)bh * M + mw] : (1 << 30);
+    const float cref = cg[head + q0];
+
+    bf16x8 qf[2][NDS], dof[2][NDS];
+    float aq[2] = {0.f, 0.f}, dl[2] = {0.f, 0.f};
+    if (wave_on) {
+#pragma unroll
+        for (int qt = 0; qt < 2; ++qt) {
+            const size_t row = head + wq0 + 16 * qt + r16;
+#pragma unroll
+            for (int ds = 0; ds < NDS; ++ds) {
+                qf[qt][ds] = *reinterpret_cast<const bf16x8*>(Q + row * D + 32 * ds + 8 * g);
+                dof[qt][ds] = *reinterpret_cast<const bf16x8*>(dO + row * D + 32 * ds + 8 * g);
+            }
+            aq[qt] = (cg[row] - cref) * kLog2e - lse2[row];
+            dl[qt] = dsum[row];
+        }
+    }
+
+    struct Stage {
+        uint4 k[CH], v[CH];
+        float4 c;
+    };
+    auto gload = [&](int n) __attribute__((always_inline)) {
+        Stage st;
+        const __bf16* kb = K + (head + (size_t)64 * n) * D;
+        const __bf16* vb = V + (head + (size_t)64 * n) * D;
+#pragma unroll
+        for (int c = 0; c < CH; ++c) {
+            const int i = tid + kBwdThreads * c;
+            st.k[c] = *reinterpret_cast<const uint4*>(kb + i * 8);
+            st.v[c] = *reinterpret_cast<const uint4*>(vb + i * 8);
+        }
+        st.c = tid < 16 ? *reinterpret_cast<const float4*>(cg + head + 64 * n + 4 * tid)
+                        : make_float4(0.f, 0.f, 0.f, 0.f);
+        return st;
+    };
+    auto sstore = [&](const Stage st, int buf) __attribute__((always_inline)) {
+#pragma unroll
+        for (int c = 0; c < CH; ++c) {
+            const int i = tid + kBwdThreads * c;
+            const int row = i / CPR, ch = i % CPR;
+            *reinterpret_cast<uint4*>(&sm.k[buf][row * LD + 8 * ch]) = st.k[c];
+            *reinterpret_cast<uint4*>(&sm.v[buf][row * LD + 8 * ch]) = st.v[c];
+        }
+        if (tid < 16) {
+            const float4 b = make_float4(-((st.c.x - cref) * kLog2e), -((st.c.y - cref) * kLog2e),
+                                         -((st.c.z - cref) * kLog2e), -((st.c.w - cref) * kLog2e));
+            *reinterpret_cast<float4*>(&sm.kb[buf][4 * tid]) = b;
+        }
+    };
+
+    f32x4 acc[2][NDT];
+#pragma unroll
+    for (int qt = 0; qt < 2; ++qt)
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt) acc[qt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    float pdp[2] = {0.f, 0.f};   // sum_j P_ij dP_ij (lane partial)
+    float psum[2] = {0.f, 0.f};  // sum_j P_ij (lane partial)
+    const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
+
+    auto tile = [&](auto diag_tag, int buf) __attribute__((always_inline)) {
+        constexpr bool kDiag = decltype(diag_tag)::value;
+        const __bf16* ktile = sm.k[buf];
+        const __bf16* vtile = sm.v[buf];
+        const float* nc = sm.kb[buf];
+#pragma unroll 1
+        for (int h = 0; h < 2; ++h) {          // keys 32 h .. 32 h + 31
+            f32x4 s[2][2], dp[2][2];
+#pragma unroll
+            for (int t = 0; t < 2; ++t) {
+                const int krow = 32 * h + 8 * (r16 >> 2) + 4 * t + (r16 & 3);
+#pragma unroll
+                for (int ds = 0; ds < NDS; ++ds) {
+                    const bf16x8 a = *reinterpret_cast<const bf16x8*>(ktile + krow * LD + 32 * ds + 8 * g);
+                    const bf16x8 b = *reinterpret_cast<const bf16x8*>(vtile + krow * LD + 32 * ds + 8 * g);
+#pragma unroll
+                    for (int qt = 0; qt < 2; ++qt) {
+                        s[t][qt] = mfma16(a, qf[qt][ds], ds == 0 ? zero : s[t][qt]);
+                        dp[t][qt] = mfma16(b, dof[qt][ds], ds == 0 ? zero : dp[t][qt]);
+                    }
+                }
+            }
+            const float4 lo = *reinterpret_cast<const float4*>(nc + 32 * h + 8 * g);
+            const float4 hi = *reinterpret_cast<const float4*>(nc + 32 * h + 8 * g + 4);
+            const float nk[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+            bf16x8 dsf[2];
+#pragma unroll
+            for (int qt = 0; qt < 2; ++qt) {
+                const int qloc = 32 * (w & 1) + 16 * qt + r16;   // query row within a diagonal tile
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    const int t = j >> 2, u = j & 3;
+                    float p = fast_exp2(__builtin_fmaf(s[t][qt][u], kscale, nk[j]) + aq[qt]);
+                    if (kDiag && (32 * h + 8 * g + j) > qloc) p = 0.f;
+                    const float dpv = dp[t][qt][u];
+                    pdp[qt] = __builtin_fmaf(p, dpv, pdp[qt]);
+                    psum[qt] += p;
+                    dsf[qt][j] = (__bf16)(p * (dpv - dl[qt]));
+                }
+            }
+            // dQ^T += K^T dS^T over these 32 keys
+#pragma unroll
+            for (int dt = 0; dt < NDT; ++dt) {
+                const bf16x8 a = lds_col8(ktile, LD, 32 * h + 8 * g, 16 * dt, r16);
+                acc[0][dt] = mfma16(a, dsf[0], acc[0][dt]);
+                acc[1][dt] = mfma16(a, dsf[1], acc[1][dt]);
+            }
+        }
+    };
+
+    sstore(gload(n_lo), 0);
+    int buf = 0;
+    for (int n = n_lo; n <= n_hi; ++n) {
+        __syncthreads();
+        const bool more = n < n_hi;
+        Stage next;
+        if (more) next = gload(n + 1);
+        if (n >= w_lo && n <= mw) {
+            if (n == mw) tile(std::true_type{}, buf);
+            else tile(std::false_type{}, buf);
+        }
+        if (more) sstore(next, buf ^ 1);
+        buf ^= 1;
+    }
+
+    if (!wave_on) return;
+#pragma unroll
+    for (int qt = 0; qt < 2; ++qt) {
+        const int query = wq0 + 16 * qt + r16;
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt) {
+            const f32x4 o = acc[qt][dt] * qscale;
+            bf16x4 ob;
+            ob[0] = (__bf16)o[0]; ob[1] = (__bf16)o[1]; ob[2] = (__bf16)o[2]; ob[3] = (__bf16)o[3];
+            *reinterpret_cast<bf16x4*>(dQ + (head + query) * D + 16 * dt + 4 * g) = ob;
+        }
+        // Delta'_i = sum_j P_ij dP_ij from the float32 P and dP of this pass: it is
+        // what rowdot(dO, O) equals for the exact O, free of the rounding of P to
+        // bfloat16 in the forward's PV product.  The dK/dV pass and both sums of
+        // dS use it; rowsum(dS) is then Delta' (1 - sum_j P_ij).
+        float a = pdp[qt], z = psum[qt];
+        a += __shfl_xor(a, 16);
+        a += __shfl_xor(a, 32);
+        z += __shfl_xor(z, 16);
+        z += __shfl_xor(z, 32);
+        if (g == 0) {
+            dsum[head + query] = a;
+            rowsum[head + query] = a - a * z;
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// dK/dV pass: one workgroup per 128 keys (wave w's 32 keys lie in one pruning
+// column), looping over query blocks m = first column .. col_end[last column].
+// S = Q K^T and dP = dO V^T are formed queries x keys so that P and dS land in
+// the B-operand layout of dV^T = dO^T P and dK^T = Q^T dS.  The A-operand rows
+// (queries) are read in the order qrow = 32 h + 8 (r / 4) + 4 t + r % 4.
+// ---------------------------------------------------------------------------
+template <int D>
+struct alignas(16) DkvSmem {
+    static constexpr int LD = D + 8;
+    alignas(16) __bf16 q[2][64 * LD];
+    __bf16 o[2][64 * LD];   // dO
+    float la[2][64];        // a_i = (c_i - r) log2(e) - L_i
+    float dl[2][64];        // Delta'_i
+};
+
+template <int D>
+__global__ __launch_bounds__(kBwdThreads) void dkdv_bf16_kernel(
+    const __bf16* __restrict__ Q, const __bf16* __restrict__ K, const __bf16* __restrict__ V,
+    const __bf16* __restrict__ dO, const float* __restrict__ cg,
+    const int* __restrict__ col_end, const float* __restrict__ lse2,
+    const float* __restrict__ dsum, __bf16* __restrict__ dK, __bf16* __restrict__ dV,
+    float* __restrict__ colsum, int L, int M, int nkb, int nblocks, float kscale,
+    float qscale) {
+    constexpr int LD = D + 8;
+    constexpr int NDS = D / 32;
+    constexpr int NDT = D / 16;
+    constexpr int CPR = D / 8;
+    constexpr int CH = 64 * CPR / kBwdThreads;
+    __shared__ DkvSmem<D> sm;
+
+    const int lid = xcd_logical_id(blockIdx.x, nblocks);
+    const int bh = lid / nkb;
+    const int kb = lid % nkb;                       // first key blocks have the most work
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int g = lane >> 4, r16 = lane & 15;
+    const int k0 = kb * kBwdRows;
+    const int wk0 = k0 + 32 * w;
+    const bool wave_on = wk0 < L;
+    const int nw = wk0 / 64;
+    const int n0 = k0 / 64;
+    const size_t head = (size_t)bh * L;
+    const int m_lo = n0;
+    const int m_hi = col_end[(size_t)bh * M + min(n0 + 1, M - 1)];
+    const int w_hi = wave_on ? col_end[(size_t)bh * M + nw] : -1;
+    const float cref = cg[head + k0];
+
+    bf16x8 kf[2][NDS], vf[2][NDS];
+    float nk[2] = {0.f, 0.f};
+    if (wave_on) {
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt) {
+            const size_t row = head + wk0 + 16 * kt + r16;
+#pragma unroll
+            for (int ds = 0; ds < NDS; ++ds) {
+                kf[kt][ds] = *reinterpret_cast<const bf16x8*>(K + row * D + 32 * ds + 8 * g);
+                vf[kt][ds] = *reinterpret_cast<const bf16x8*>(V + row * D + 32 * ds + 8 * g);
+            }
+            nk[kt] = -((cg[row] - cref) * kLog2e);
+        }
+    }
+
+    struct Stage {
+        uint4 q[CH], o[CH];
+        float la, dl;
+    };
+    auto gload = [&](int m) __attribute__((always_inline)) {
+        Stage st;
+        const __bf16* qb = Q + (head + (size_t)64 * m) * D;
+        const __bf16* ob = dO + (head + (size_t)64 * m) * D;
+#pragma unroll
+        for (int c = 0; c < CH; ++c) {
+            const int i = tid + kBwdThreads * c;
+            st.q[c] = *reinterpret_cast<const uint4*>(qb + i * 8);
+            st.o[c] = *reinterpret_cast<const uint4*>(ob + i * 8);
+        }
+        st.la = 0.f;
+        st.dl = 0.f;
+        if (tid < 64) {
+            const size_t row = head + 64 * m + tid;
+            st.la = (cg[row] - cref) * kLog2e - lse2[row];
+            st.dl = dsum[row];
+        }
+        return st;
+    };
+    auto sstore = [&](const Stage st, int buf) __attribute__((always_inline)) {
+#pragma unroll
+        for (int c = 0; c < CH; ++c) {
+            const int i = tid + kBwdThreads * c;
+            const int row = i / CPR, ch = i % CPR;
+            *reinterpret_cast<uint4*>(&sm.q[buf][row * LD + 8 * ch]) = st.q[c];
+            *reinterpret_cast<uint4*>(&sm.o[buf][row * LD + 8 * ch]) = st.o[c];
+        }
+        if (tid < 64) {
+            sm.la[buf][tid] = st.la;
+            sm.dl[buf][tid] = st.dl;
+        }
+    };
+
+    f32x4 dk[2][NDT], dv[2][NDT];
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt) {
+            dk[kt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+            dv[kt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+    float csum[2] = {0.f, 0.f};
+    const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
+
+    auto tile = [&](auto diag_tag, int buf) __attribute__((always_inline)) {
+        constexpr bool kDiag = decltype(diag_tag)::value;
+        const __bf16* qtile = sm.q[buf];
+        const __bf16* otile = sm.o[buf];
+#pragma unroll 1
+        for (int h = 0; h < 2; ++h) {          // queries 32 h .. 32 h + 31
+            f32x4 s[2][2], dp[2][2];
+#pragma unroll
+            for (int t = 0; t < 2; ++t) {
+                const int qrow = 32 * h + 8 * (r16 >> 2) + 4 * t + (r16 & 3);
+#pragma unroll
+                for (int ds = 0; ds < NDS; ++ds) {
+                    const bf16x8 a = *reinterpret_cast<const bf16x8*>(qtile + qrow * LD + 32 * ds + 8 * g);
+                    const bf16x8 b = *reinterpret_cast<const bf16x8*>(otile + qrow * LD + 32 * ds + 8 * g);
+#pragma unroll
+                    for (int kt = 0; kt < 2; ++kt) {
+                        s[t][kt] = mfma16(a, kf[kt][ds], ds == 0 ? zero : s[t][kt]);
+                        dp[t][kt] = mfma16(b, vf[kt][ds], ds == 0 ? zero : dp[t][kt]);
+                    }
+                }
+            }
+            // the lane's queries: 32 h + 8 g + j, j = 0..7 (j < 4 from subtile 0)
+            const float4 a0 = *reinterpret_cast<const float4*>(&sm.la[buf][32 * h + 8 * g]);
+            const float4 a1 = *reinterpret_cast<const float4*>(&sm.la[buf][32 * h + 8 * g + 4]);
+            const float4 b0 = *reinterpret_cast<const float4*>(&sm.dl[buf][32 * h + 8 * g]);
+            const float4 b1 = *reinterpret_cast<const float4*>(&sm.dl[buf][32 * h + 8 * g + 4]);
+            const float l8[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+            const float d8[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
+            bf16x8 pb[2], db[2];
+#pragma unroll
+            for (int kt = 0; kt < 2; ++kt) {
+                const int kloc = 32 * (w & 1) + 16 * kt + r16;   // key column within a diagonal tile
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    const int t = j >> 2, u = j & 3;
+                    float p = fast_exp2(__builtin_fmaf(s[t][kt][u], kscale, nk[kt]) + l8[j]);
+                    if (kDiag && kloc > (32 * h + 8 * g + j)) p = 0.f;
+                    const float dsv = p * (dp[t][kt][u] - d8[j]);
+                    csum[kt] += dsv;
+                    pb[kt][j] = (__bf16)p;
+                    db[kt][j] = (__bf16)dsv;
+                }
+            }
+            // dV^T += dO^T P,  dK^T += Q^T dS over these 32 queries
+#pragma unroll
+            for (int dt = 0; dt < NDT; ++dt) {
+                const bf16x8 ao = lds_col8(otile, LD, 32 * h + 8 * g, 16 * dt, r16);
+                const bf16x8 aq = lds_col8(qtile, LD, 32 * h + 8 * g, 16 * dt, r16);
+#pragma unroll
+                for (int kt = 0; kt < 2; ++kt) {
+                    dv[kt][dt] = mfma16(ao, pb[kt], dv[kt][dt]);
+                    dk[kt][dt] = mfma16(aq, db[kt], dk[kt][dt]);
+                }
+            }
+        }
+    };
+
+    sstore(gload(m_lo), 0);
+    int buf = 0;
+    for (int m = m_lo; m <= m_hi; ++m) {
+        __syncthreads();
+        const bool more = m < m_hi;
+        Stage next;
+        if (more) next = gload(m + 1);
+        if (m >= nw && m <= w_hi) {
+            if (m == nw) tile(std::true_type{}, buf);
+            else tile(std::false_type{}, buf);
+        }
+        if (more) sstore(next, buf ^ 1);
+        buf ^= 1;
+    }
+
+    if (!wave_on) return;
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt) {
+        const int key = wk0 + 16 * kt + r16;
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt) {
+            const f32x4 a = dk[kt][dt] * qscale;
+            const f32x4 b = dv[kt][dt];
+            bf16x4 ab, bb;
+            ab[0] = (__bf16)a[0]; ab[1] = (__bf16)a[1]; ab[2] = (__bf16)a[2]; ab[3] = (__bf16)a[3];
+            bb[0] = (__bf16)b[0]; bb[1] = (__bf16)b[1]; bb[2] = (__bf16)b[2]; bb[3] = (__bf16)b[3];
+            const size_t off = (head + key) * D + 16 * dt + 4 * g;
+            *reinterpret_cast<bf16x4*>(dK + off) = ab;
+            *reinterpret_cast<bf16x4*>(dV + off) = bb;
+        }
+        float c = csum[kt];
+        c += __shfl_xor(c, 16);
+        c += __shfl_xor(c, 32);
+        if (g == 0) colsum[head + key] = c;
+    }
+}
+
+// ---------------------------------------------------------------------------
+hipError_t launch_dq_bf16(const BwdArgs& a, hipStream_t s) {
+    const int BH = a.B * a.H, M = a.L / 64;
+    const float kscale = kLog2e / sqrtf((float)a.d);
+    const float qscale = 1.0f / sqrtf((float)a.d);
+    const int nqb = (a.L + kBwdRows - 1) / kBwdRows;
+    const int nblocks = BH * nqb;
+    if (a.d == 64)
+        hipLaunchKernelGGL(dq_bf16_kernel<64>, dim3(nblocks), dim3(kBwdThreads), 0, s,
+                           (const __bf16*)a.Q, (const __bf16*)a.K, (const __bf16*)a.V,
+                           (const __bf16*)a.dO, a.c, a.row_start, a.lse2, a.dsum,
+                           (__bf16*)a.dQ, a.rowsum, a.L, M, nqb, nblocks, kscale, qscale);
+    else
+        hipLaunchKernelGGL(dq_bf16_kernel<128>, dim3(nblocks), dim3(kBwdThreads), 0, s,
+                           (const __bf16*)a.Q, (const __bf16*)a.K, (const __bf16*)a.V,
+                           (const __bf16*)a.dO, a.c, a.row_start, a.lse2, a.dsum,
+                           (__bf16*)a.dQ, a.rowsum, a.L, M, nqb, nblocks, kscale, qscale);
+    return hipGetLastError();
+}
+
+hipError_t launch_dkdv_bf16(const BwdArgs& a, hipStream_t s) {
+    const int BH = a.B * a.H, M = a.L / 64;
+    const float kscale = kLog2e / sqrtf((float)a.d);
+    const float qscale = 1.0f / sqrtf((float)a.d);
+    const int nkb = (a.L + kBwdRows - 1) / kBwdRows;
+    const int nblocks = BH * nkb;
+    if (a.d == 64)
+        hipLaunchKernelGGL(dkdv_bf16_kernel<64>, dim3(nblocks), dim3(kBwdThreads), 0, s,
+                           (const __bf16*)a.Q, (const __bf16*)a.K, (const __bf16*)a.V,
+                           (const __bf16*)a.dO, a.c, a.col_end, a.lse2, a.dsum,
+                           (__bf16*)a.dK, (__bf16*)a.dV, a.colsum, a.L, M, nkb, nblocks,
+                           kscale, qscale);
+    else
+        hipLaunchKernelGGL(dkdv_bf16_kernel<128>, dim3(nblocks), dim3(kBwdThreads), 0, s,
+                           (const __bf16*)a.Q, (const __bf16*)a.K, (const __bf16*)a.V,
+                           (const __bf16*)a.dO, a.c, a.col_end, a.lse2, a.dsum,
+                           (__bf16*)a.dK, (__bf16*)a.dV, a.colsum, a.L, M, nkb, nblocks,
+                           kscale, qscale);
+    return hipGetLastError();
+}
+
+}  // namespace acp

@@ -7,16 +7,32 @@
 // cumulative gate at the workgroup's first query,
 //   y_ij = (q_i . k_j) * log2(e)/sqrt(d) - (c_j - r) * log2(e).
 // The row term (c_i - r) log2(e) is constant along a row and cancels in the
-// softmax; it returns only in the log-sum-exp,
-//   L_i = LSE_i log2(e) = max_j y_ij + log2(l_i) + (c_i - r) log2(e).
-// Every quantity stays of the size of the decay inside the kept window, however
-// long the sequence (c itself grows without bound).  L_i is frame-free; the
-// backward recomputes P_ij = 2^(q_i.k_j log2(e)/sqrt(d) + (c_i - c_j) log2(e) - L_i)
-// in frames of its own.
+// softmax; it returns only in the log-sum-exp L_i = LSE_i log2(e).  Every
+// quantity stays of the size of the decay inside the kept window, however long
+// the sequence (c itself grows without bound).  L_i is frame-free; the backward
+// recomputes P_ij = 2^(q_i.k_j log2(e)/sqrt(d) + (c_i - c_j) log2(e) - L_i) in
+// frames of its own.
+//
+// Softmax stabiliser.  ACP already bounds every logit of the head: |q.k|/sqrt(d)
+// <= U and c_i - c_j <= 0, so each row's true logits are <= U, while the
+// diagonal logit is >= -U.  Subtracting the per-row constant
+//   m_i = U log2(e) + (r - c_i) log2(e)
+// from y therefore keeps every exponent <= 0 and the largest term >= e^(-2U).
+// For U <= kUFixedMax that largest term is a normal float32 and the online
+// running maximum (and its rescaling of the accumulators) is not needed: the
+// constant is folded into the MFMA accumulator initialisation, and each logit
+// costs one FMA and one exp2.  Heads with a larger U take the online-maximum
+// variant.  Both variants are launched; each skips the heads of the other.
+#include <type_traits>
+
 #include "acp_device.h"
 #include "acp_internal.h"
 
 namespace acp {
+
+constexpr int kFwdThreads = 256;
+constexpr int kFwdRows = 128;
+constexpr double kUFixedMax = 32.0;
 
 // ---------------------------------------------------------------------------
 // bf16 path: v_mfma_f32_16x16x32_bf16, fp32 accumulation.
@@ -33,9 +49,6 @@ namespace acp {
 // order krow(kt, r) = 32 (kt / 2) + 8 (r / 4) + 4 (kt % 2) + r % 4.
 // ---------------------------------------------------------------------------
 
-constexpr int kFwdThreads = 256;
-constexpr int kFwdRows = 128;
-
 template <int D>
 struct alignas(16) FwdSmem {
     static constexpr int LD = D + 8;
@@ -44,12 +57,13 @@ struct alignas(16) FwdSmem {
     float kb[2][64];   // key bias -(c_j - r) log2(e)
 };
 
-template <int D>
+template <int D, bool kFixed>
 __global__ __launch_bounds__(kFwdThreads) void fwd_bf16_kernel(
     const __bf16* __restrict__ Q, const __bf16* __restrict__ K, const __bf16* __restrict__ V,
     const float* __restrict__ cg, const int* __restrict__ row_start,
-    __bf16* __restrict__ O, float* __restrict__ O32, float* __restrict__ lse,
-    float* __restrict__ lse2, int L, int M, int nqb, int nblocks, float kscale) {
+    const double* __restrict__ bound_u, __bf16* __restrict__ O, float* __restrict__ O32,
+    float* __restrict__ lse, float* __restrict__ lse2, int L, int M, int nqb, int nblocks,
+    float kscale) {
     constexpr int LD = D + 8;
     constexpr int NDS = D / 32;                     // k-steps over the head dim
     constexpr int NDT = D / 16;                     // output tiles over the head dim
@@ -59,8 +73,11 @@ __global__ __launch_bounds__(kFwdThreads) void fwd_bf16_kernel(
 
     const int lid = xcd_logical_id(blockIdx.x, nblocks);
     const int bh = lid / nqb;
+    const double u_head = bound_u[bh];
+    if ((u_head <= kUFixedMax) != kFixed) return;   // the other variant's head
     const int qb = nqb - 1 - (lid % nqb);           // longest rows first
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int g = lane >> 4, r16 = lane & 15;
     const int q0 = qb * kFwdRows;
     const int wq0 = q0 + 32 * w;
@@ -72,41 +89,59 @@ __global__ __launch_bounds__(kFwdThreads) void fwd_bf16_kernel(
     const int n_hi = min(m0 + 1, M - 1);
     const int w_lo = wave_on ? row_start[(size_t)bh * M + mw] : (1 << 30);
     const float cref = cg[head + q0];
+    const float uf = (float)u_head;
+    const float sqrt_d = sqrtf((float)D);
 
     bf16x8 qf[2][NDS];
+    f32x4 sinit[2];   // fixed stabiliser folded into the S accumulator start
+    float cq[2] = {0.f, 0.f};
     if (wave_on) {
 #pragma unroll
-        for (int qt = 0; qt < 2; ++qt)
+        for (int qt = 0; qt < 2; ++qt) {
 #pragma unroll
             for (int ds = 0; ds < NDS; ++ds)
                 qf[qt][ds] = *reinterpret_cast<const bf16x8*>(
                     Q + (head + wq0 + 16 * qt + r16) * D + 32 * ds + 8 * g);
+            cq[qt] = cg[head + wq0 + 16 * qt + r16];
+        }
+    }
+#pragma unroll
+    for (int qt = 0; qt < 2; ++qt) {
+        const float init = kFixed ? -(uf + (cref - cq[qt])) * sqrt_d : 0.f;
+        sinit[qt] = f32x4{init, init, init, init};
     }
 
-    uint4 kreg[CH], vreg[CH];
-    float4 nreg = make_float4(0.f, 0.f, 0.f, 0.f);
-    auto gload = [&](int n) {
+    // K/V tile n staged through registers: loaded one tile ahead, stored to LDS
+    // after the current tile's compute.
+    struct Stage {
+        uint4 k[CH], v[CH];
+        float4 c;
+    };
+    auto gload = [&](int n) __attribute__((always_inline)) {
+        Stage st;
         const __bf16* kb = K + (head + (size_t)64 * n) * D;
         const __bf16* vb = V + (head + (size_t)64 * n) * D;
 #pragma unroll
         for (int c = 0; c < CH; ++c) {
             const int i = tid + kFwdThreads * c;
-            kreg[c] = *reinterpret_cast<const uint4*>(kb + i * 8);
-            vreg[c] = *reinterpret_cast<const uint4*>(vb + i * 8);
+            st.k[c] = *reinterpret_cast<const uint4*>(kb + i * 8);
+            st.v[c] = *reinterpret_cast<const uint4*>(vb + i * 8);
         }
-        if (tid < 16) nreg = *reinterpret_cast<const float4*>(cg + head + 64 * n + 4 * tid);
+        st.c = tid < 16 ? *reinterpret_cast<const float4*>(cg + head + 64 * n + 4 * tid)
+                        : make_float4(0.f, 0.f, 0.f, 0.f);
+        return st;
     };
-    auto sstore = [&](int buf) {
+    auto sstore = [&](const Stage st, int buf) __attribute__((always_inline)) {
 #pragma unroll
         for (int c = 0; c < CH; ++c) {
             const int i = tid + kFwdThreads * c;
             const int row = i / CPR, ch = i % CPR;
-            *reinterpret_cast<uint4*>(&sm.k[buf][row * LD + 8 * ch]) = kreg[c];
-            *reinterpret_cast<uint4*>(&sm.v[buf][row * LD + 8 * ch]) = vreg[c];
+            *reinterpret_cast<uint4*>(&sm.k[buf][row * LD + 8 * ch]) = st.k[c];
+            *reinterpret_cast<uint4*>(&sm.v[buf][row * LD + 8 * ch]) = st.v[c];
         }
         if (tid < 16) {
-            const float4 b = make_float4(-((nreg.x - cref) * kLog2e), -((nreg.y - cref) * kLog2e),
-                                         -((nreg.z - cref) * kLog2e), -((nreg.w - cref) * kLog2e));
+            const float4 b = make_float4(-((st.c.x - cref) * kLog2e), -((st.c.y - cref) * kLog2e),
+                                         -((st.c.z - cref) * kLog2e), -((st.c.w - cref) * kLog2e));
             *reinterpret_cast<float4*>(&sm.kb[buf][4 * tid]) = b;
         }
     };
@@ -117,47 +152,56 @@ __global__ __launch_bounds__(kFwdThreads) void fwd_bf16_kernel(
 #pragma unroll
         for (int dt = 0; dt < NDT; ++dt) acc[qt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
     float mrun[2] = {-INFINITY, -INFINITY};
-    float lrun[2] = {0.f, 0.f};
+    float lrun[2] = {0.f, 0.f};   // sum of the float32 weights (for the log-sum-exp)
+    float lbf[2] = {0.f, 0.f};    // sum of the bfloat16 weights that enter P V
 
-    gload(n_lo);
-    sstore(0);
-    int buf = 0;
-    for (int n = n_lo; n <= n_hi; ++n) {
-        __syncthreads();
-        const bool more = n < n_hi;
-        if (more) gload(n + 1);
-        if (n >= w_lo && n <= mw) {
-            const __bf16* ktile = sm.k[buf];
-            const __bf16* vtile = sm.v[buf];
-            const float* nc = sm.kb[buf];
-            // S^T tiles: s[kt][qt] = K[krow(kt)] Q^T
-            f32x4 s[4][2];
+    // One 64-key tile for this wave; kDiag masks keys after the query.
+    auto tile = [&](auto diag_tag, int n, int buf) __attribute__((always_inline)) {
+        constexpr bool kDiag = decltype(diag_tag)::value;
+        const __bf16* ktile = sm.k[buf];
+        const __bf16* vtile = sm.v[buf];
+        const float* nc = sm.kb[buf];
+        f32x4 s[4][2];
 #pragma unroll
-            for (int kt = 0; kt < 4; ++kt) {
-                const int krow = 32 * (kt >> 1) + 8 * (r16 >> 2) + 4 * (kt & 1) + (r16 & 3);
-                s[kt][0] = f32x4{0.f, 0.f, 0.f, 0.f};
-                s[kt][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int kt = 0; kt < 4; ++kt) {
+            const int krow = 32 * (kt >> 1) + 8 * (r16 >> 2) + 4 * (kt & 1) + (r16 & 3);
 #pragma unroll
-                for (int ds = 0; ds < NDS; ++ds) {
-                    const bf16x8 a = *reinterpret_cast<const bf16x8*>(ktile + krow * LD + 32 * ds + 8 * g);
-                    s[kt][0] = mfma16(a, qf[0][ds], s[kt][0]);
-                    s[kt][1] = mfma16(a, qf[1][ds], s[kt][1]);
+            for (int ds = 0; ds < NDS; ++ds) {
+                const bf16x8 a = *reinterpret_cast<const bf16x8*>(ktile + krow * LD + 32 * ds + 8 * g);
+                s[kt][0] = mfma16(a, qf[0][ds], ds == 0 ? sinit[0] : s[kt][0]);
+                s[kt][1] = mfma16(a, qf[1][ds], ds == 0 ? sinit[1] : s[kt][1]);
+            }
+        }
+        // the lane's keys are 32 ks + 8 g + j, j = 0..7 (j < 4 from tile 2ks)
+        float nk[2][8];
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+            const float4 lo = *reinterpret_cast<const float4*>(nc + 32 * ks + 8 * g);
+            const float4 hi = *reinterpret_cast<const float4*>(nc + 32 * ks + 8 * g + 4);
+            nk[ks][0] = lo.x; nk[ks][1] = lo.y; nk[ks][2] = lo.z; nk[ks][3] = lo.w;
+            nk[ks][4] = hi.x; nk[ks][5] = hi.y; nk[ks][6] = hi.z; nk[ks][7] = hi.w;
+        }
+        bf16x8 pf[2][2];
+#pragma unroll
+        for (int qt = 0; qt < 2; ++qt) {
+            const int qloc = 32 * w + 16 * qt + r16 - 64 * (n - m0);   // query within tile rows
+            if constexpr (kFixed) {
+                float l = lrun[qt], lb = lbf[qt];
+#pragma unroll
+                for (int ks = 0; ks < 2; ++ks) {
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) {
+                        float p = fast_exp2(
+                            __builtin_fmaf(s[2 * ks + (j >> 2)][qt][j & 3], kscale, nk[ks][j]));
+                        if (kDiag && (32 * ks + 8 * g + j) > qloc) p = 0.f;
+                        l += p;
+                        pf[qt][ks][j] = (__bf16)p;
+                    }
+                    lb = sum_bf16x8(pf[qt][ks], lb);
                 }
-            }
-            // the lane's keys are 32 ks + 8 g + j, j = 0..7 (j < 4 from tile 2ks)
-            float nk[2][8];
-#pragma unroll
-            for (int ks = 0; ks < 2; ++ks) {
-                const float4 lo = *reinterpret_cast<const float4*>(nc + 32 * ks + 8 * g);
-                const float4 hi = *reinterpret_cast<const float4*>(nc + 32 * ks + 8 * g + 4);
-                nk[ks][0] = lo.x; nk[ks][1] = lo.y; nk[ks][2] = lo.z; nk[ks][3] = lo.w;
-                nk[ks][4] = hi.x; nk[ks][5] = hi.y; nk[ks][6] = hi.z; nk[ks][7] = hi.w;
-            }
-            const bool diag = (n == mw);
-            bf16x8 pf[2][2];
-#pragma unroll
-            for (int qt = 0; qt < 2; ++qt) {
-                const int query = wq0 + 16 * qt + r16;
+                lrun[qt] = l;
+                lbf[qt] = lb;
+            } else {
                 float y[2][8];
                 float mx = -INFINITY;
 #pragma unroll
@@ -165,7 +209,7 @@ __global__ __launch_bounds__(kFwdThreads) void fwd_bf16_kernel(
 #pragma unroll
                     for (int j = 0; j < 8; ++j) {
                         float v = __builtin_fmaf(s[2 * ks + (j >> 2)][qt][j & 3], kscale, nk[ks][j]);
-                        if (diag && (64 * n + 32 * ks + 8 * g + j) > query) v = -INFINITY;
+                        if (kDiag && (32 * ks + 8 * g + j) > qloc) v = -INFINITY;
                         y[ks][j] = v;
                         mx = fmaxf(mx, v);
                     }
@@ -187,17 +231,30 @@ __global__ __launch_bounds__(kFwdThreads) void fwd_bf16_kernel(
                     }
                 lrun[qt] = l;
             }
-            // O^T += V^T P^T
-#pragma unroll
-            for (int dt = 0; dt < NDT; ++dt)
-#pragma unroll
-                for (int ks = 0; ks < 2; ++ks) {
-                    const bf16x8 a = lds_col8(vtile, LD, 32 * ks + 8 * g, 16 * dt, r16);
-                    acc[0][dt] = mfma16(a, pf[0][ks], acc[0][dt]);
-                    acc[1][dt] = mfma16(a, pf[1][ks], acc[1][dt]);
-                }
         }
-        if (more) sstore(buf ^ 1);
+        // O^T += V^T P^T
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+            for (int ks = 0; ks < 2; ++ks) {
+                const bf16x8 a = lds_col8(vtile, LD, 32 * ks + 8 * g, 16 * dt, r16);
+                acc[0][dt] = mfma16(a, pf[0][ks], acc[0][dt]);
+                acc[1][dt] = mfma16(a, pf[1][ks], acc[1][dt]);
+            }
+    };
+
+    sstore(gload(n_lo), 0);
+    int buf = 0;
+    for (int n = n_lo; n <= n_hi; ++n) {
+        __syncthreads();
+        const bool more = n < n_hi;
+        Stage next;
+        if (more) next = gload(n + 1);
+        if (n >= w_lo && n <= mw) {
+            if (n == mw) tile(std::true_type{}, n, buf);
+            else tile(std::false_type{}, n, buf);
+        }
+        if (more) sstore(next, buf ^ 1);
         buf ^= 1;
     }
 
@@ -207,7 +264,15 @@ __global__ __launch_bounds__(kFwdThreads) void fwd_bf16_kernel(
         float lt = lrun[qt];
         lt += __shfl_xor(lt, 16);
         lt += __shfl_xor(lt, 32);
-        const float inv = 1.0f / lt;
+        // O is normalised by the sum of the weights it was built from: with the
+        // fixed stabiliser the largest weight is not 1, and normalising the
+        // bfloat16-weighted sum by the float32 sum would leave its rounding in O.
+        float lo = kFixed ? lbf[qt] : lt;
+        if (kFixed) {
+            lo += __shfl_xor(lo, 16);
+            lo += __shfl_xor(lo, 32);
+        }
+        const float inv = 1.0f / lo;
         const int query = wq0 + 16 * qt + r16;
 #pragma unroll
         for (int dt = 0; dt < NDT; ++dt) {
@@ -219,7 +284,10 @@ __global__ __launch_bounds__(kFwdThreads) void fwd_bf16_kernel(
             *reinterpret_cast<bf16x4*>(O + off) = ob;
         }
         if (g == 0) {
-            const float l2 = mrun[qt] + fast_log2(lt) + (cg[head + query] - cref) * kLog2e;
+            // L_i = LSE_i log2(e): fixed variant  U log2(e) + log2(l_i);
+            // online variant  max_j y_ij + log2(l_i) + (c_i - r) log2(e)
+            const float l2 = kFixed ? uf * kLog2e + fast_log2(lt)
+                                    : mrun[qt] + fast_log2(lt) + (cq[qt] - cref) * kLog2e;
             lse2[head + query] = l2;
             lse[head + query] = l2 * kLn2;
         }
@@ -228,7 +296,7 @@ __global__ __launch_bounds__(kFwdThreads) void fwd_bf16_kernel(
 
 // ---------------------------------------------------------------------------
 // fp32 path: plain VALU arithmetic, one thread per query, 64 queries (one
-// pruning row) per workgroup; K/V tiles staged in LDS.
+// pruning row) per workgroup; K/V tiles staged in LDS; online maximum.
 // ---------------------------------------------------------------------------
 template <int D>
 __global__ __launch_bounds__(64) void fwd_f32_kernel(
@@ -288,23 +356,28 @@ __global__ __launch_bounds__(64) void fwd_f32_kernel(
 }
 
 // ---------------------------------------------------------------------------
+template <int D>
+static void launch_fwd_bf16(const FwdArgs& a, int M, float kscale, hipStream_t s) {
+    const int BH = a.B * a.H;
+    const int nqb = (a.L + kFwdRows - 1) / kFwdRows;
+    const int nblocks = BH * nqb;
+    hipLaunchKernelGGL((fwd_bf16_kernel<D, true>), dim3(nblocks), dim3(kFwdThreads), 0, s,
+                       (const __bf16*)a.Q, (const __bf16*)a.K, (const __bf16*)a.V, a.c,
+                       a.row_start, a.u, (__bf16*)a.O, a.O32, a.lse, a.lse2, a.L, M, nqb,
+                       nblocks, kscale);
+    hipLaunchKernelGGL((fwd_bf16_kernel<D, false>), dim3(nblocks), dim3(kFwdThreads), 0, s,
+                       (const __bf16*)a.Q, (const __bf16*)a.K, (const __bf16*)a.V, a.c,
+                       a.row_start, a.u, (__bf16*)a.O, a.O32, a.lse, a.lse2, a.L, M, nqb,
+                       nblocks, kscale);
+}
+
 hipError_t launch_fwd(const FwdArgs& a, hipStream_t s) {
     const int BH = a.B * a.H, M = a.L / 64;
     const float kscale = kLog2e / sqrtf((float)a.d);
     trace_begin(ACP_K_FWD, s);
     if (a.bf16) {
-        const int nqb = (a.L + kFwdRows - 1) / kFwdRows;
-        const int nblocks = BH * nqb;
-        if (a.d == 64)
-            hipLaunchKernelGGL(fwd_bf16_kernel<64>, dim3(nblocks), dim3(kFwdThreads), 0, s,
-                               (const __bf16*)a.Q, (const __bf16*)a.K, (const __bf16*)a.V, a.c,
-                               a.row_start, (__bf16*)a.O, a.O32, a.lse, a.lse2, a.L, M, nqb,
-                               nblocks, kscale);
-        else
-            hipLaunchKernelGGL(fwd_bf16_kernel<128>, dim3(nblocks), dim3(kFwdThreads), 0, s,
-                               (const __bf16*)a.Q, (const __bf16*)a.K, (const __bf16*)a.V, a.c,
-                               a.row_start, (__bf16*)a.O, a.O32, a.lse, a.lse2, a.L, M, nqb,
-                               nblocks, kscale);
+        if (a.d == 64) launch_fwd_bf16<64>(a, M, kscale, s);
+        else launch_fwd_bf16<128>(a, M, kscale, s);
     } else {
         if (a.d == 64)
             hipLaunchKernelGGL(fwd_f32_kernel<64>, dim3(BH * M), dim3(64), 0, s,
