@@ -67,13 +67,32 @@ __device__ __forceinline__ s16x4 lds_read_tr16(const __bf16* p) {
     return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(p));
 }
 
-// Eight consecutive rows r0 .. r0 + 7 of column c0 + (lane % 16) of a row-major
-// bf16 tile in LDS with row stride `ld` elements, as an MFMA operand whose k
-// index runs over the rows.
-__device__ __forceinline__ bf16x8 lds_col8(const __bf16* tile, int ld, int r0, int c0, int r16) {
-    const __bf16* p0 = tile + (r0 + (r16 >> 2)) * ld + c0 + 4 * (r16 & 3);
-    s16x4 lo = lds_read_tr16(p0);
-    s16x4 hi = lds_read_tr16(p0 + 4 * ld);
+// ---- LDS tiles of 64 rows x D bf16 columns ----------------------------------
+// Stored as D/64 column panels of 64 x 64 elements (128-byte rows).  Inside a
+// row, 16-byte chunk c sits at position c ^ swz(row).  With this swizzle the
+// fragment reads below (ds_read_b128 of one chunk from rows {0-3, 8-11, ...},
+// and the transpose reads of 4 rows x 32 bytes) are free of bank conflicts on
+// gfx950 (measured); padded rows cost twice as much.  Each 1 KB stretch of a
+// panel (8 rows) is written by one wave-wide 16-byte-per-lane DMA load.
+__device__ __forceinline__ int tile_swz(int row) { return (row & 3) | (((row >> 3) & 1) << 2); }
+
+// byte offset of element (row, col); col % 8 selects the position in the chunk
+__device__ __forceinline__ int tile_off(int row, int col) {
+    return (((col >> 6) << 6) + row) * 128 + ((((col & 63) >> 3) ^ tile_swz(row)) << 4) +
+           ((col & 7) << 1);
+}
+
+// 8 bf16 of row `row`, columns col .. col + 7 (col % 8 == 0)
+__device__ __forceinline__ bf16x8 tile_row8(const unsigned char* tile, int row, int col) {
+    return *reinterpret_cast<const bf16x8*>(tile + tile_off(row, col));
+}
+
+// Eight consecutive rows r0 .. r0 + 7 of column c0 + (lane % 16) of a tile, as an
+// MFMA operand whose k index runs over the rows (two LDS transpose reads).
+__device__ __forceinline__ bf16x8 tile_col8(const unsigned char* tile, int r0, int c0, int r16) {
+    const int col = c0 + 4 * (r16 & 3);
+    s16x4 lo = lds_read_tr16(reinterpret_cast<const __bf16*>(tile + tile_off(r0 + (r16 >> 2), col)));
+    s16x4 hi = lds_read_tr16(reinterpret_cast<const __bf16*>(tile + tile_off(r0 + 4 + (r16 >> 2), col)));
     bf16x8 out;
     bf16x4 lo_b = __builtin_bit_cast(bf16x4, lo);
     bf16x4 hi_b = __builtin_bit_cast(bf16x4, hi);
@@ -81,6 +100,43 @@ __device__ __forceinline__ bf16x8 lds_col8(const __bf16* tile, int ld, int r0, i
     out[4] = hi_b[0]; out[5] = hi_b[1]; out[6] = hi_b[2]; out[7] = hi_b[3];
     return out;
 }
+
+// tile_col8 with the lane's address precomputed: p = tile + tile_off(r0 + (lane % 16) / 4,
+// c0 + 4 (lane % 4)); rows r0 + 4 .. r0 + 7 sit 512 bytes further (the swizzle of
+// a row does not change when 4 is added to a row whose bit 2 is clear).
+__device__ __forceinline__ bf16x8 tile_col8_at(const unsigned char* p) {
+    s16x4 lo = lds_read_tr16(reinterpret_cast<const __bf16*>(p));
+    s16x4 hi = lds_read_tr16(reinterpret_cast<const __bf16*>(p + 512));
+    bf16x8 out;
+    bf16x4 lo_b = __builtin_bit_cast(bf16x4, lo);
+    bf16x4 hi_b = __builtin_bit_cast(bf16x4, hi);
+    out[0] = lo_b[0]; out[1] = lo_b[1]; out[2] = lo_b[2]; out[3] = lo_b[3];
+    out[4] = hi_b[0]; out[5] = hi_b[1]; out[6] = hi_b[2]; out[7] = hi_b[3];
+    return out;
+}
+
+// Issue this wave's share of the DMA loads that fill `tile` (LDS, 64 x D bf16)
+// from rows src[0 .. 63] (row-major, D columns).  Instruction i writes LDS bytes
+// [1024 i, 1024 i + 1024): panel i / 8, rows 8 (i % 8) .. + 7; lane L brings the
+// 16-byte chunk that belongs at position L % 8 of row 8 (i % 8) + L / 8.
+// Completion is tracked by vmcnt (wait before the barrier that publishes it).
+template <int D, int NWAVES>
+__device__ __forceinline__ void tile_dma(unsigned char* tile, const __bf16* src, int wave, int lane) {
+    typedef __attribute__((address_space(3))) void lds_void;
+    constexpr int kInst = 64 * D * 2 / 1024;
+#pragma unroll
+    for (int k = 0; k < kInst / NWAVES; ++k) {
+        const int i = wave + NWAVES * k;
+        const int row = 8 * (i & 7) + (lane >> 3);
+        const int chunk = (lane & 7) ^ tile_swz(row);
+        const __bf16* g = src + row * D + ((i >> 3) << 6) + 8 * chunk;
+        __builtin_amdgcn_global_load_lds(g, (lds_void*)(tile + 1024 * i), 16, 0, 0);
+    }
+}
+
+// s_waitcnt vmcnt(0): this wave's outstanding vector-memory loads (including DMA
+// writes into LDS) have completed.
+__device__ __forceinline__ void wait_vmcnt0() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
 // ---- workgroup -> (head, block) mapping ------------------------------------
 // Workgroups are dealt round-robin to the 8 XCDs (each with its own L2).  This

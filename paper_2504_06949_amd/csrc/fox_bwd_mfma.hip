@@ -10,8 +10,9 @@
 // Both passes use 4 waves of 32 rows (two 64-row pruning blocks per workgroup),
 // so a pruned or non-causal tile is skipped wave-uniformly, and work through
 // each 64-row tile of the other operand in two halves of 32 to keep register
-// pressure low.  Tiles are double-buffered in LDS (row-major, padded); operands
-// whose contraction runs over sequence positions come from LDS transpose reads.
+// pressure low.  Tiles are double-buffered in LDS (swizzled panels filled by DMA
+// loads while the previous tile is computed); operands whose contraction runs
+// over sequence positions come from LDS transpose reads.
 #include <type_traits>
 
 #include "acp_device.h"
@@ -29,11 +30,10 @@ constexpr int kBwdRows = 128;
 // the order krow = 32 h + 8 (r / 4) + 4 t + r % 4 (half h, subtile t).
 // ---------------------------------------------------------------------------
 template <int D>
-struct alignas(16) DqSmem {
-    static constexpr int LD = D + 8;
-    alignas(16) __bf16 k[2][64 * LD];
-    __bf16 v[2][64 * LD];
-    float kb[2][64];   // key bias -(c_j - r) log2(e)
+struct alignas(1024) DqSmem {
+    unsigned char k[2][128 * D];   // 64 x D bf16 tiles (see tile_off)
+    unsigned char v[2][128 * D];
+    float kb[2][64];               // key bias -(c_j - r) log2(e)
 };
 
 template <int D>
@@ -43,11 +43,8 @@ __global__ __launch_bounds__(kBwdThreads) void dq_bf16_kernel(
     const int* __restrict__ row_start, const float* __restrict__ lse2,
     float* __restrict__ dsum, __bf16* __restrict__ dQ, float* __restrict__ rowsum,
     int L, int M, int nqb, int nblocks, float kscale, float qscale) {
-    constexpr int LD = D + 8;
     constexpr int NDS = D / 32;
     constexpr int NDT = D / 16;
-    constexpr int CPR = D / 8;
-    constexpr int CH = 64 * CPR / kBwdThreads;
     __shared__ DqSmem<D> sm;
 
     const int lid = xcd_logical_id(blockIdx.x, nblocks);
@@ -83,38 +80,25 @@ __global__ __launch_bounds__(kBwdThreads) void dq_bf16_kernel(
         }
     }
 
-    struct Stage {
-        uint4 k[CH], v[CH];
-        float4 c;
-    };
-    auto gload = [&](int n) __attribute__((always_inline)) {
-        Stage st;
-        const __bf16* kb = K + (head + (size_t)64 * n) * D;
-        const __bf16* vb = V + (head + (size_t)64 * n) * D;
-#pragma unroll
-        for (int c = 0; c < CH; ++c) {
-            const int i = tid + kBwdThreads * c;
-            st.k[c] = *reinterpret_cast<const uint4*>(kb + i * 8);
-            st.v[c] = *reinterpret_cast<const uint4*>(vb + i * 8);
-        }
-        st.c = tid < 16 ? *reinterpret_cast<const float4*>(cg + head + 64 * n + 4 * tid)
+    auto issue = [&](int n, int buf) __attribute__((always_inline)) {
+        tile_dma<D, 4>(sm.k[buf], K + (head + (size_t)64 * n) * D, w, lane);
+        tile_dma<D, 4>(sm.v[buf], V + (head + (size_t)64 * n) * D, w, lane);
+        return tid < 16 ? *reinterpret_cast<const float4*>(cg + head + 64 * n + 4 * tid)
                         : make_float4(0.f, 0.f, 0.f, 0.f);
-        return st;
     };
-    auto sstore = [&](const Stage st, int buf) __attribute__((always_inline)) {
-#pragma unroll
-        for (int c = 0; c < CH; ++c) {
-            const int i = tid + kBwdThreads * c;
-            const int row = i / CPR, ch = i % CPR;
-            *reinterpret_cast<uint4*>(&sm.k[buf][row * LD + 8 * ch]) = st.k[c];
-            *reinterpret_cast<uint4*>(&sm.v[buf][row * LD + 8 * ch]) = st.v[c];
-        }
+    auto put_kb = [&](float4 c, int buf) __attribute__((always_inline)) {
         if (tid < 16) {
-            const float4 b = make_float4(-((st.c.x - cref) * kLog2e), -((st.c.y - cref) * kLog2e),
-                                         -((st.c.z - cref) * kLog2e), -((st.c.w - cref) * kLog2e));
+            const float4 b = make_float4(-((c.x - cref) * kLog2e), -((c.y - cref) * kLog2e),
+                                         -((c.z - cref) * kLog2e), -((c.w - cref) * kLog2e));
             *reinterpret_cast<float4*>(&sm.kb[buf][4 * tid]) = b;
         }
     };
+    // per-lane LDS offsets (the swizzle of a fragment row depends only on the lane)
+    int roff[NDS], coff[NDT];
+#pragma unroll
+    for (int ds = 0; ds < NDS; ++ds) roff[ds] = tile_off(8 * (r16 >> 2) + (r16 & 3), 32 * ds + 8 * g);
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt) coff[dt] = tile_off(8 * g + (r16 >> 2), 16 * dt + 4 * (r16 & 3));
 
     f32x4 acc[2][NDT];
 #pragma unroll
@@ -127,19 +111,20 @@ __global__ __launch_bounds__(kBwdThreads) void dq_bf16_kernel(
 
     auto tile = [&](auto diag_tag, int buf) __attribute__((always_inline)) {
         constexpr bool kDiag = decltype(diag_tag)::value;
-        const __bf16* ktile = sm.k[buf];
-        const __bf16* vtile = sm.v[buf];
+        const unsigned char* ktile = sm.k[buf];
+        const unsigned char* vtile = sm.v[buf];
         const float* nc = sm.kb[buf];
 #pragma unroll 1
         for (int h = 0; h < 2; ++h) {          // keys 32 h .. 32 h + 31
             f32x4 s[2][2], dp[2][2];
 #pragma unroll
             for (int t = 0; t < 2; ++t) {
-                const int krow = 32 * h + 8 * (r16 >> 2) + 4 * t + (r16 & 3);
+                // row 32 h + 4 t + (row of roff)
+                const int rstep = 128 * (32 * h + 4 * t);
 #pragma unroll
                 for (int ds = 0; ds < NDS; ++ds) {
-                    const bf16x8 a = *reinterpret_cast<const bf16x8*>(ktile + krow * LD + 32 * ds + 8 * g);
-                    const bf16x8 b = *reinterpret_cast<const bf16x8*>(vtile + krow * LD + 32 * ds + 8 * g);
+                    const bf16x8 a = *reinterpret_cast<const bf16x8*>(ktile + roff[ds] + rstep);
+                    const bf16x8 b = *reinterpret_cast<const bf16x8*>(vtile + roff[ds] + rstep);
 #pragma unroll
                     for (int qt = 0; qt < 2; ++qt) {
                         s[t][qt] = mfma16(a, qf[qt][ds], ds == 0 ? zero : s[t][qt]);
@@ -153,7 +138,8 @@ __global__ __launch_bounds__(kBwdThreads) void dq_bf16_kernel(
             bf16x8 dsf[2];
 #pragma unroll
             for (int qt = 0; qt < 2; ++qt) {
-                const int qloc = 32 * (w & 1) + 16 * qt + r16;   // query row within a diagonal tile
+                int qloc = 32 * (w & 1) + 16 * qt + r16;   // query row within a diagonal tile
+                if constexpr (kDiag) asm volatile("" : "+v"(qloc));
 #pragma unroll
                 for (int j = 0; j < 8; ++j) {
                     const int t = j >> 2, u = j & 3;
@@ -168,25 +154,27 @@ __global__ __launch_bounds__(kBwdThreads) void dq_bf16_kernel(
             // dQ^T += K^T dS^T over these 32 keys
 #pragma unroll
             for (int dt = 0; dt < NDT; ++dt) {
-                const bf16x8 a = lds_col8(ktile, LD, 32 * h + 8 * g, 16 * dt, r16);
+                const bf16x8 a = tile_col8_at(ktile + coff[dt] + 128 * 32 * h);
                 acc[0][dt] = mfma16(a, dsf[0], acc[0][dt]);
                 acc[1][dt] = mfma16(a, dsf[1], acc[1][dt]);
             }
         }
     };
 
-    sstore(gload(n_lo), 0);
+    put_kb(issue(n_lo, 0), 0);
+    wait_vmcnt0();
     int buf = 0;
     for (int n = n_lo; n <= n_hi; ++n) {
-        __syncthreads();
+        __syncthreads();   // tile n is in LDS; every wave is done with tile n - 1
         const bool more = n < n_hi;
-        Stage next;
-        if (more) next = gload(n + 1);
+        float4 cnext = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (more) cnext = issue(n + 1, buf ^ 1);
         if (n >= w_lo && n <= mw) {
             if (n == mw) tile(std::true_type{}, buf);
             else tile(std::false_type{}, buf);
         }
-        if (more) sstore(next, buf ^ 1);
+        if (more) put_kb(cnext, buf ^ 1);
+        wait_vmcnt0();
         buf ^= 1;
     }
 
@@ -225,12 +213,11 @@ __global__ __launch_bounds__(kBwdThreads) void dq_bf16_kernel(
 // (queries) are read in the order qrow = 32 h + 8 (r / 4) + 4 t + r % 4.
 // ---------------------------------------------------------------------------
 template <int D>
-struct alignas(16) DkvSmem {
-    static constexpr int LD = D + 8;
-    alignas(16) __bf16 q[2][64 * LD];
-    __bf16 o[2][64 * LD];   // dO
-    float la[2][64];        // a_i = (c_i - r) log2(e) - L_i
-    float dl[2][64];        // Delta'_i
+struct alignas(1024) DkvSmem {
+    unsigned char q[2][128 * D];   // 64 x D bf16 tiles (see tile_off)
+    unsigned char o[2][128 * D];   // dO
+    float la[2][64];               // a_i = (c_i - r) log2(e) - L_i
+    float dl[2][64];               // Delta'_i
 };
 
 template <int D>
@@ -241,11 +228,8 @@ __global__ __launch_bounds__(kBwdThreads) void dkdv_bf16_kernel(
     const float* __restrict__ dsum, __bf16* __restrict__ dK, __bf16* __restrict__ dV,
     float* __restrict__ colsum, int L, int M, int nkb, int nblocks, float kscale,
     float qscale) {
-    constexpr int LD = D + 8;
     constexpr int NDS = D / 32;
     constexpr int NDT = D / 16;
-    constexpr int CPR = D / 8;
-    constexpr int CH = 64 * CPR / kBwdThreads;
     __shared__ DkvSmem<D> sm;
 
     const int lid = xcd_logical_id(blockIdx.x, nblocks);
@@ -280,42 +264,28 @@ __global__ __launch_bounds__(kBwdThreads) void dkdv_bf16_kernel(
         }
     }
 
-    struct Stage {
-        uint4 q[CH], o[CH];
-        float la, dl;
-    };
-    auto gload = [&](int m) __attribute__((always_inline)) {
-        Stage st;
-        const __bf16* qb = Q + (head + (size_t)64 * m) * D;
-        const __bf16* ob = dO + (head + (size_t)64 * m) * D;
-#pragma unroll
-        for (int c = 0; c < CH; ++c) {
-            const int i = tid + kBwdThreads * c;
-            st.q[c] = *reinterpret_cast<const uint4*>(qb + i * 8);
-            st.o[c] = *reinterpret_cast<const uint4*>(ob + i * 8);
-        }
-        st.la = 0.f;
-        st.dl = 0.f;
+    auto issue = [&](int m, int buf) __attribute__((always_inline)) {
+        tile_dma<D, 4>(sm.q[buf], Q + (head + (size_t)64 * m) * D, w, lane);
+        tile_dma<D, 4>(sm.o[buf], dO + (head + (size_t)64 * m) * D, w, lane);
+        float2 r = make_float2(0.f, 0.f);
         if (tid < 64) {
             const size_t row = head + 64 * m + tid;
-            st.la = (cg[row] - cref) * kLog2e - lse2[row];
-            st.dl = dsum[row];
+            r.x = (cg[row] - cref) * kLog2e - lse2[row];
+            r.y = dsum[row];
         }
-        return st;
+        return r;
     };
-    auto sstore = [&](const Stage st, int buf) __attribute__((always_inline)) {
-#pragma unroll
-        for (int c = 0; c < CH; ++c) {
-            const int i = tid + kBwdThreads * c;
-            const int row = i / CPR, ch = i % CPR;
-            *reinterpret_cast<uint4*>(&sm.q[buf][row * LD + 8 * ch]) = st.q[c];
-            *reinterpret_cast<uint4*>(&sm.o[buf][row * LD + 8 * ch]) = st.o[c];
-        }
+    auto put_rows = [&](float2 r, int buf) __attribute__((always_inline)) {
         if (tid < 64) {
-            sm.la[buf][tid] = st.la;
-            sm.dl[buf][tid] = st.dl;
+            sm.la[buf][tid] = r.x;
+            sm.dl[buf][tid] = r.y;
         }
     };
+    int roff[NDS], coff[NDT];
+#pragma unroll
+    for (int ds = 0; ds < NDS; ++ds) roff[ds] = tile_off(8 * (r16 >> 2) + (r16 & 3), 32 * ds + 8 * g);
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt) coff[dt] = tile_off(8 * g + (r16 >> 2), 16 * dt + 4 * (r16 & 3));
 
     f32x4 dk[2][NDT], dv[2][NDT];
 #pragma unroll
@@ -330,18 +300,19 @@ __global__ __launch_bounds__(kBwdThreads) void dkdv_bf16_kernel(
 
     auto tile = [&](auto diag_tag, int buf) __attribute__((always_inline)) {
         constexpr bool kDiag = decltype(diag_tag)::value;
-        const __bf16* qtile = sm.q[buf];
-        const __bf16* otile = sm.o[buf];
+        const unsigned char* qtile = sm.q[buf];
+        const unsigned char* otile = sm.o[buf];
 #pragma unroll 1
         for (int h = 0; h < 2; ++h) {          // queries 32 h .. 32 h + 31
             f32x4 s[2][2], dp[2][2];
 #pragma unroll
             for (int t = 0; t < 2; ++t) {
-                const int qrow = 32 * h + 8 * (r16 >> 2) + 4 * t + (r16 & 3);
+                // row 32 h + 4 t + (row of roff)
+                const int rstep = 128 * (32 * h + 4 * t);
 #pragma unroll
                 for (int ds = 0; ds < NDS; ++ds) {
-                    const bf16x8 a = *reinterpret_cast<const bf16x8*>(qtile + qrow * LD + 32 * ds + 8 * g);
-                    const bf16x8 b = *reinterpret_cast<const bf16x8*>(otile + qrow * LD + 32 * ds + 8 * g);
+                    const bf16x8 a = *reinterpret_cast<const bf16x8*>(qtile + roff[ds] + rstep);
+                    const bf16x8 b = *reinterpret_cast<const bf16x8*>(otile + roff[ds] + rstep);
 #pragma unroll
                     for (int kt = 0; kt < 2; ++kt) {
                         s[t][kt] = mfma16(a, kf[kt][ds], ds == 0 ? zero : s[t][kt]);
@@ -359,7 +330,8 @@ __global__ __launch_bounds__(kBwdThreads) void dkdv_bf16_kernel(
             bf16x8 pb[2], db[2];
 #pragma unroll
             for (int kt = 0; kt < 2; ++kt) {
-                const int kloc = 32 * (w & 1) + 16 * kt + r16;   // key column within a diagonal tile
+                int kloc = 32 * (w & 1) + 16 * kt + r16;   // key column within a diagonal tile
+                if constexpr (kDiag) asm volatile("" : "+v"(kloc));
 #pragma unroll
                 for (int j = 0; j < 8; ++j) {
                     const int t = j >> 2, u = j & 3;
@@ -374,8 +346,8 @@ __global__ __launch_bounds__(kBwdThreads) void dkdv_bf16_kernel(
             // dV^T += dO^T P,  dK^T += Q^T dS over these 32 queries
 #pragma unroll
             for (int dt = 0; dt < NDT; ++dt) {
-                const bf16x8 ao = lds_col8(otile, LD, 32 * h + 8 * g, 16 * dt, r16);
-                const bf16x8 aq = lds_col8(qtile, LD, 32 * h + 8 * g, 16 * dt, r16);
+                const bf16x8 ao = tile_col8_at(otile + coff[dt] + 128 * 32 * h);
+                const bf16x8 aq = tile_col8_at(qtile + coff[dt] + 128 * 32 * h);
 #pragma unroll
                 for (int kt = 0; kt < 2; ++kt) {
                     dv[kt][dt] = mfma16(ao, pb[kt], dv[kt][dt]);
@@ -385,18 +357,20 @@ __global__ __launch_bounds__(kBwdThreads) void dkdv_bf16_kernel(
         }
     };
 
-    sstore(gload(m_lo), 0);
+    put_rows(issue(m_lo, 0), 0);
+    wait_vmcnt0();
     int buf = 0;
     for (int m = m_lo; m <= m_hi; ++m) {
-        __syncthreads();
+        __syncthreads();   // tile m is in LDS; every wave is done with tile m - 1
         const bool more = m < m_hi;
-        Stage next;
-        if (more) next = gload(m + 1);
+        float2 rnext = make_float2(0.f, 0.f);
+        if (more) rnext = issue(m + 1, buf ^ 1);
         if (m >= nw && m <= w_hi) {
             if (m == nw) tile(std::true_type{}, buf);
             else tile(std::false_type{}, buf);
         }
-        if (more) sstore(next, buf ^ 1);
+        if (more) put_rows(rnext, buf ^ 1);
+        wait_vmcnt0();
         buf ^= 1;
     }
 

@@ -40,7 +40,8 @@ constexpr double kUFixedMax = 32.0;
 // Workgroup = 4 waves = 128 queries (two 64-row pruning blocks); wave w owns
 // 32 queries that all sit in one pruning row, so a pruned or non-causal tile is
 // skipped wave-uniformly and no pruned entry is ever computed.  Key/value tiles
-// of 64 rows are double-buffered in LDS (row-major, padded); V^T operands come
+// of 64 rows are double-buffered in LDS (swizzled panels, filled by DMA loads
+// straight from HBM/L2 while the previous tile is computed); V^T operands come
 // from LDS transpose reads.
 //
 // S^T = K Q^T is computed (keys x queries) so that each lane holds one query and
@@ -50,11 +51,10 @@ constexpr double kUFixedMax = 32.0;
 // ---------------------------------------------------------------------------
 
 template <int D>
-struct alignas(16) FwdSmem {
-    static constexpr int LD = D + 8;
-    alignas(16) __bf16 k[2][64 * LD];
-    __bf16 v[2][64 * LD];
-    float kb[2][64];   // key bias -(c_j - r) log2(e)
+struct alignas(1024) FwdSmem {
+    unsigned char k[2][128 * D];   // 64 x D bf16 tiles (see tile_off)
+    unsigned char v[2][128 * D];
+    float kb[2][64];               // key bias -(c_j - r) log2(e)
 };
 
 template <int D, bool kFixed>
@@ -64,11 +64,8 @@ __global__ __launch_bounds__(kFwdThreads) void fwd_bf16_kernel(
     const double* __restrict__ bound_u, __bf16* __restrict__ O, float* __restrict__ O32,
     float* __restrict__ lse, float* __restrict__ lse2, int L, int M, int nqb, int nblocks,
     float kscale) {
-    constexpr int LD = D + 8;
     constexpr int NDS = D / 32;                     // k-steps over the head dim
     constexpr int NDT = D / 16;                     // output tiles over the head dim
-    constexpr int CPR = D / 8;                      // 16-byte pieces per row
-    constexpr int CH = 64 * CPR / kFwdThreads;      // pieces per thread per tile
     __shared__ FwdSmem<D> sm;
 
     const int lid = xcd_logical_id(blockIdx.x, nblocks);
@@ -111,37 +108,17 @@ __global__ __launch_bounds__(kFwdThreads) void fwd_bf16_kernel(
         sinit[qt] = f32x4{init, init, init, init};
     }
 
-    // K/V tile n staged through registers: loaded one tile ahead, stored to LDS
-    // after the current tile's compute.
-    struct Stage {
-        uint4 k[CH], v[CH];
-        float4 c;
-    };
-    auto gload = [&](int n) __attribute__((always_inline)) {
-        Stage st;
-        const __bf16* kb = K + (head + (size_t)64 * n) * D;
-        const __bf16* vb = V + (head + (size_t)64 * n) * D;
-#pragma unroll
-        for (int c = 0; c < CH; ++c) {
-            const int i = tid + kFwdThreads * c;
-            st.k[c] = *reinterpret_cast<const uint4*>(kb + i * 8);
-            st.v[c] = *reinterpret_cast<const uint4*>(vb + i * 8);
-        }
-        st.c = tid < 16 ? *reinterpret_cast<const float4*>(cg + head + 64 * n + 4 * tid)
+    // Tile n: K and V by DMA into LDS, the 64 gate values through registers.
+    auto issue = [&](int n, int buf) __attribute__((always_inline)) {
+        tile_dma<D, 4>(sm.k[buf], K + (head + (size_t)64 * n) * D, w, lane);
+        tile_dma<D, 4>(sm.v[buf], V + (head + (size_t)64 * n) * D, w, lane);
+        return tid < 16 ? *reinterpret_cast<const float4*>(cg + head + 64 * n + 4 * tid)
                         : make_float4(0.f, 0.f, 0.f, 0.f);
-        return st;
     };
-    auto sstore = [&](const Stage st, int buf) __attribute__((always_inline)) {
-#pragma unroll
-        for (int c = 0; c < CH; ++c) {
-            const int i = tid + kFwdThreads * c;
-            const int row = i / CPR, ch = i % CPR;
-            *reinterpret_cast<uint4*>(&sm.k[buf][row * LD + 8 * ch]) = st.k[c];
-            *reinterpret_cast<uint4*>(&sm.v[buf][row * LD + 8 * ch]) = st.v[c];
-        }
+    auto put_kb = [&](float4 c, int buf) __attribute__((always_inline)) {
         if (tid < 16) {
-            const float4 b = make_float4(-((st.c.x - cref) * kLog2e), -((st.c.y - cref) * kLog2e),
-                                         -((st.c.z - cref) * kLog2e), -((st.c.w - cref) * kLog2e));
+            const float4 b = make_float4(-((c.x - cref) * kLog2e), -((c.y - cref) * kLog2e),
+                                         -((c.z - cref) * kLog2e), -((c.w - cref) * kLog2e));
             *reinterpret_cast<float4*>(&sm.kb[buf][4 * tid]) = b;
         }
     };
@@ -155,19 +132,28 @@ __global__ __launch_bounds__(kFwdThreads) void fwd_bf16_kernel(
     float lrun[2] = {0.f, 0.f};   // sum of the float32 weights (for the log-sum-exp)
     float lbf[2] = {0.f, 0.f};    // sum of the bfloat16 weights that enter P V
 
+    // Per-lane LDS offsets.  The swizzle of a fragment row depends only on the
+    // lane, so the tile-row steps below are compile-time offsets.
+    int koff[NDS], voff[NDT];
+#pragma unroll
+    for (int ds = 0; ds < NDS; ++ds) koff[ds] = tile_off(8 * (r16 >> 2) + (r16 & 3), 32 * ds + 8 * g);
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt) voff[dt] = tile_off(8 * g + (r16 >> 2), 16 * dt + 4 * (r16 & 3));
+
     // One 64-key tile for this wave; kDiag masks keys after the query.
     auto tile = [&](auto diag_tag, int n, int buf) __attribute__((always_inline)) {
         constexpr bool kDiag = decltype(diag_tag)::value;
-        const __bf16* ktile = sm.k[buf];
-        const __bf16* vtile = sm.v[buf];
+        const unsigned char* ktile = sm.k[buf];
+        const unsigned char* vtile = sm.v[buf];
         const float* nc = sm.kb[buf];
         f32x4 s[4][2];
 #pragma unroll
         for (int kt = 0; kt < 4; ++kt) {
-            const int krow = 32 * (kt >> 1) + 8 * (r16 >> 2) + 4 * (kt & 1) + (r16 & 3);
 #pragma unroll
             for (int ds = 0; ds < NDS; ++ds) {
-                const bf16x8 a = *reinterpret_cast<const bf16x8*>(ktile + krow * LD + 32 * ds + 8 * g);
+                // row krow = 32 (kt / 2) + 4 (kt % 2) + (row of koff)
+                const bf16x8 a = *reinterpret_cast<const bf16x8*>(
+                    ktile + koff[ds] + 128 * (32 * (kt >> 1) + 4 * (kt & 1)));
                 s[kt][0] = mfma16(a, qf[0][ds], ds == 0 ? sinit[0] : s[kt][0]);
                 s[kt][1] = mfma16(a, qf[1][ds], ds == 0 ? sinit[1] : s[kt][1]);
             }
@@ -184,7 +170,10 @@ __global__ __launch_bounds__(kFwdThreads) void fwd_bf16_kernel(
         bf16x8 pf[2][2];
 #pragma unroll
         for (int qt = 0; qt < 2; ++qt) {
-            const int qloc = 32 * w + 16 * qt + r16 - 64 * (n - m0);   // query within tile rows
+            // query row within a diagonal tile; the empty asm keeps the mask
+            // comparisons inside this (rare) tile instead of hoisted into SGPRs
+            int qloc = 32 * (w & 1) + 16 * qt + r16;
+            if constexpr (kDiag) asm volatile("" : "+v"(qloc));
             if constexpr (kFixed) {
                 float l = lrun[qt], lb = lbf[qt];
 #pragma unroll
@@ -237,24 +226,26 @@ __global__ __launch_bounds__(kFwdThreads) void fwd_bf16_kernel(
         for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
             for (int ks = 0; ks < 2; ++ks) {
-                const bf16x8 a = lds_col8(vtile, LD, 32 * ks + 8 * g, 16 * dt, r16);
+                const bf16x8 a = tile_col8_at(vtile + voff[dt] + 128 * 32 * ks);
                 acc[0][dt] = mfma16(a, pf[0][ks], acc[0][dt]);
                 acc[1][dt] = mfma16(a, pf[1][ks], acc[1][dt]);
             }
     };
 
-    sstore(gload(n_lo), 0);
+    put_kb(issue(n_lo, 0), 0);
+    wait_vmcnt0();
     int buf = 0;
     for (int n = n_lo; n <= n_hi; ++n) {
-        __syncthreads();
+        __syncthreads();   // tile n is in LDS; every wave is done with tile n - 1
         const bool more = n < n_hi;
-        Stage next;
-        if (more) next = gload(n + 1);
+        float4 cnext = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (more) cnext = issue(n + 1, buf ^ 1);
         if (n >= w_lo && n <= mw) {
             if (n == mw) tile(std::true_type{}, n, buf);
             else tile(std::false_type{}, n, buf);
         }
-        if (more) sstore(next, buf ^ 1);
+        if (more) put_kb(cnext, buf ^ 1);
+        wait_vmcnt0();
         buf ^= 1;
     }
 
