@@ -37,6 +37,25 @@ def _flops(w, kept_tiles):
     }
 
 
+def measured_traffic(kernel: str, workload: str):
+    """HBM bytes per launch of `kernel` on `workload` from the committed rocprofv3
+    summaries (FETCH_SIZE + WRITE_SIZE, copy-calibrated), or None when none exists
+    or the kernel's source changed since the counters were taken."""
+    import glob
+    import hashlib
+    for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*.md"))):
+        for line in open(path):
+            f = line.split()
+            if len(f) == 5 and f[0] == "traffic" and f[1] == kernel and f[2] == workload:
+                src, digest = f[4].split(":")
+                src_path = os.path.join(ROOT, "paper_2504_06949_amd", "csrc", src)
+                if not os.path.exists(src_path):
+                    return None
+                now = hashlib.sha1(open(src_path, "rb").read()).hexdigest()[:12]
+                return int(f[3]) if now == digest else None
+    return None
+
+
 def run_workload(name: str, steps: int, warmup: int, eps_override=None, unpruned=True):
     import torch
     from paper_2504_06949_amd import acp, workloads
@@ -125,6 +144,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--skip-unpruned", action="store_true",
                     help="do not time the eps = 0 (nothing pruned) reference run")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
+                    help="first run one plain device-to-device copy of MIB MiB (a known "
+                         "byte count for calibrating HBM traffic counters under a profiler)")
     ap.add_argument("--extra", action="store_true",
                     help="also time the 360M/760M-shaped and adversarial layers")
     args = ap.parse_args()
@@ -139,6 +161,14 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
 
+    if args.copy_probe > 0:
+        n = args.copy_probe * (1 << 20) // 4
+        a = torch.ones(n, dtype=torch.float32, device="cuda:0")
+        b = torch.empty_like(a)
+        torch.cuda.synchronize()
+        b.copy_(a)
+        torch.cuda.synchronize()
+        del a, b
     res = run_workload(args.workload, args.steps, args.warmup, unpruned=not args.skip_unpruned)
     w = res["w"]
     fl = _flops(w, res["kept"])
@@ -172,7 +202,8 @@ def main():
         "boundary_share": round((pk["rownorm"] + pk["plan"]) / res["ms"], 4),
         "roofline": {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 2),
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None},
+                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                     "traffic": measured_traffic(dom, args.workload)},
     }
     if args.extra:
         extra = {}
