@@ -120,19 +120,52 @@ __device__ __forceinline__ bf16x8 tile_col8_at(const unsigned char* p) {
 // [1024 i, 1024 i + 1024): panel i / 8, rows 8 (i % 8) .. + 7; lane L brings the
 // 16-byte chunk that belongs at position L % 8 of row 8 (i % 8) + L / 8.
 // Completion is tracked by vmcnt (wait before the barrier that publishes it).
+// The per-lane source offsets do not depend on the tile, so they are computed
+// once and held for the whole kernel: each load is a uniform (scalar) tile base
+// plus a fixed 32-bit lane offset, and its address registers are never reused
+// (which would force a wait for the loads in flight).
 template <int D, int NWAVES>
-__device__ __forceinline__ void tile_dma(unsigned char* tile, const __bf16* src, int wave, int lane) {
-    typedef __attribute__((address_space(3))) void lds_void;
-    constexpr int kInst = 64 * D * 2 / 1024;
+struct TileDma {
+    static constexpr int kInst = 64 * D * 2 / 1024;   // 1 KB wave instructions per tile
+    static constexpr int kPer = kInst / NWAVES;
+    unsigned off[kPer];
+
+    __device__ __forceinline__ void init(int wave, int lane) {
 #pragma unroll
-    for (int k = 0; k < kInst / NWAVES; ++k) {
-        const int i = wave + NWAVES * k;
-        const int row = 8 * (i & 7) + (lane >> 3);
-        const int chunk = (lane & 7) ^ tile_swz(row);
-        const __bf16* g = src + row * D + ((i >> 3) << 6) + 8 * chunk;
-        __builtin_amdgcn_global_load_lds(g, (lds_void*)(tile + 1024 * i), 16, 0, 0);
+        for (int k = 0; k < kPer; ++k) {
+            const int i = wave + NWAVES * k;
+            const int row = 8 * (i & 7) + (lane >> 3);
+            const int chunk = (lane & 7) ^ tile_swz(row);
+            off[k] = (unsigned)(2 * (row * D + ((i >> 3) << 6) + 8 * chunk));
+        }
     }
-}
+    // src: first element of the 64-row source tile (row-major, D columns).  The
+    // loads are written out (scalar base + lane offset, LDS destination in M0) so
+    // that the compiler neither recomputes their addresses nor, not knowing they
+    // write LDS, places conservative waits before unrelated LDS reads; their
+    // completion is awaited explicitly (wait_vmcnt0) before the barrier that
+    // publishes the tile, and nothing the compiler waits on is issued after them
+    // inside the tile compute.
+    __device__ __forceinline__ void issue(unsigned char* tile, const __bf16* src, int wave) const {
+        typedef __attribute__((address_space(3))) unsigned char lds_u8;
+        const unsigned long long p = reinterpret_cast<unsigned long long>(src);
+        const unsigned lo = __builtin_amdgcn_readfirstlane((unsigned)p);
+        const unsigned hi = __builtin_amdgcn_readfirstlane((unsigned)(p >> 32));
+        const unsigned long long base = ((unsigned long long)hi << 32) | lo;
+#pragma unroll
+        for (int k = 0; k < kPer; ++k) {
+            const int i = wave + NWAVES * k;
+            const unsigned lds = __builtin_amdgcn_readfirstlane(
+                (unsigned)(unsigned long long)(const lds_u8*)(tile + 1024 * i));
+            asm volatile(
+                "s_mov_b32 m0, %0\n\t"
+                "global_load_lds_dwordx4 %1, %2"
+                :
+                : "s"(lds), "v"(off[k]), "s"(base)
+                : "memory", "m0");
+        }
+    }
+};
 
 // s_waitcnt vmcnt(0): this wave's outstanding vector-memory loads (including DMA
 // writes into LDS) have completed.

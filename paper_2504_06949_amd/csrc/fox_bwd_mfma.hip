@@ -80,11 +80,16 @@ __global__ __launch_bounds__(kBwdThreads) void dq_bf16_kernel(
         }
     }
 
+    // The small per-tile loads go first: vmcnt retires in order, so waiting for
+    // them later does not wait for the tile's DMA.
+    TileDma<D, 4> dma;
+    dma.init(w, lane);
     auto issue = [&](int n, int buf) __attribute__((always_inline)) {
-        tile_dma<D, 4>(sm.k[buf], K + (head + (size_t)64 * n) * D, w, lane);
-        tile_dma<D, 4>(sm.v[buf], V + (head + (size_t)64 * n) * D, w, lane);
-        return tid < 16 ? *reinterpret_cast<const float4*>(cg + head + 64 * n + 4 * tid)
-                        : make_float4(0.f, 0.f, 0.f, 0.f);
+        const float4 c = tid < 16 ? *reinterpret_cast<const float4*>(cg + head + 64 * n + 4 * tid)
+                                  : make_float4(0.f, 0.f, 0.f, 0.f);
+        dma.issue(sm.k[buf], K + (head + (size_t)64 * n) * D, w);
+        dma.issue(sm.v[buf], V + (head + (size_t)64 * n) * D, w);
+        return c;
     };
     auto put_kb = [&](float4 c, int buf) __attribute__((always_inline)) {
         if (tid < 16) {
@@ -264,21 +269,24 @@ __global__ __launch_bounds__(kBwdThreads) void dkdv_bf16_kernel(
         }
     }
 
+    // The small per-row loads go first and are combined only after the tile's
+    // compute: vmcnt retires in order, so using them does not wait for the DMA.
+    TileDma<D, 4> dma;
+    dma.init(w, lane);
     auto issue = [&](int m, int buf) __attribute__((always_inline)) {
-        tile_dma<D, 4>(sm.q[buf], Q + (head + (size_t)64 * m) * D, w, lane);
-        tile_dma<D, 4>(sm.o[buf], dO + (head + (size_t)64 * m) * D, w, lane);
-        float2 r = make_float2(0.f, 0.f);
+        float3 r = make_float3(0.f, 0.f, 0.f);
         if (tid < 64) {
             const size_t row = head + 64 * m + tid;
-            r.x = (cg[row] - cref) * kLog2e - lse2[row];
-            r.y = dsum[row];
+            r = make_float3(cg[row], lse2[row], dsum[row]);
         }
+        dma.issue(sm.q[buf], Q + (head + (size_t)64 * m) * D, w);
+        dma.issue(sm.o[buf], dO + (head + (size_t)64 * m) * D, w);
         return r;
     };
-    auto put_rows = [&](float2 r, int buf) __attribute__((always_inline)) {
+    auto put_rows = [&](float3 r, int buf) __attribute__((always_inline)) {
         if (tid < 64) {
-            sm.la[buf][tid] = r.x;
-            sm.dl[buf][tid] = r.y;
+            sm.la[buf][tid] = (r.x - cref) * kLog2e - r.y;
+            sm.dl[buf][tid] = r.z;
         }
     };
     int roff[NDS], coff[NDT];
@@ -363,7 +371,7 @@ __global__ __launch_bounds__(kBwdThreads) void dkdv_bf16_kernel(
     for (int m = m_lo; m <= m_hi; ++m) {
         __syncthreads();   // tile m is in LDS; every wave is done with tile m - 1
         const bool more = m < m_hi;
-        float2 rnext = make_float2(0.f, 0.f);
+        float3 rnext = make_float3(0.f, 0.f, 0.f);
         if (more) rnext = issue(m + 1, buf ^ 1);
         if (m >= nw && m <= w_hi) {
             if (m == nw) tile(std::true_type{}, buf);

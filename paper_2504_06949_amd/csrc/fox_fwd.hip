@@ -109,11 +109,16 @@ __global__ __launch_bounds__(kFwdThreads) void fwd_bf16_kernel(
     }
 
     // Tile n: K and V by DMA into LDS, the 64 gate values through registers.
+    // The gate load goes first: vmcnt retires in order, so waiting for it later
+    // does not wait for the tile's DMA.
+    TileDma<D, 4> dma;
+    dma.init(w, lane);
     auto issue = [&](int n, int buf) __attribute__((always_inline)) {
-        tile_dma<D, 4>(sm.k[buf], K + (head + (size_t)64 * n) * D, w, lane);
-        tile_dma<D, 4>(sm.v[buf], V + (head + (size_t)64 * n) * D, w, lane);
-        return tid < 16 ? *reinterpret_cast<const float4*>(cg + head + 64 * n + 4 * tid)
-                        : make_float4(0.f, 0.f, 0.f, 0.f);
+        const float4 c = tid < 16 ? *reinterpret_cast<const float4*>(cg + head + 64 * n + 4 * tid)
+                                  : make_float4(0.f, 0.f, 0.f, 0.f);
+        dma.issue(sm.k[buf], K + (head + (size_t)64 * n) * D, w);
+        dma.issue(sm.v[buf], V + (head + (size_t)64 * n) * D, w);
+        return c;
     };
     auto put_kb = [&](float4 c, int buf) __attribute__((always_inline)) {
         if (tid < 16) {
