@@ -110,9 +110,18 @@ __global__ __launch_bounds__(kBwdThreads) void dq_bf16_kernel(
     for (int qt = 0; qt < 2; ++qt)
 #pragma unroll
         for (int dt = 0; dt < NDT; ++dt) acc[qt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
-    float pdp[2] = {0.f, 0.f};   // sum_j P_ij dP_ij (lane partial)
+    // Row terms folded into the MFMA accumulator starts: S starts at a_i / k' so
+    // that fma(S, k', key bias) is the exponent, and dP starts at -Delta_i so that
+    // it comes out as dP - Delta.
+    f32x4 sinit[2], dinit[2];
+#pragma unroll
+    for (int qt = 0; qt < 2; ++qt) {
+        const float a = aq[qt] / kscale, b = -dl[qt];
+        sinit[qt] = f32x4{a, a, a, a};
+        dinit[qt] = f32x4{b, b, b, b};
+    }
+    float sds[2] = {0.f, 0.f};   // sum_j dS_ij (lane partial)
     float psum[2] = {0.f, 0.f};  // sum_j P_ij (lane partial)
-    const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
 
     auto tile = [&](auto diag_tag, int buf) __attribute__((always_inline)) {
         constexpr bool kDiag = decltype(diag_tag)::value;
@@ -132,8 +141,8 @@ __global__ __launch_bounds__(kBwdThreads) void dq_bf16_kernel(
                     const bf16x8 b = *reinterpret_cast<const bf16x8*>(vtile + roff[ds] + rstep);
 #pragma unroll
                     for (int qt = 0; qt < 2; ++qt) {
-                        s[t][qt] = mfma16(a, qf[qt][ds], ds == 0 ? zero : s[t][qt]);
-                        dp[t][qt] = mfma16(b, dof[qt][ds], ds == 0 ? zero : dp[t][qt]);
+                        s[t][qt] = mfma16(a, qf[qt][ds], ds == 0 ? sinit[qt] : s[t][qt]);
+                        dp[t][qt] = mfma16(b, dof[qt][ds], ds == 0 ? dinit[qt] : dp[t][qt]);
                     }
                 }
             }
@@ -148,12 +157,12 @@ __global__ __launch_bounds__(kBwdThreads) void dq_bf16_kernel(
 #pragma unroll
                 for (int j = 0; j < 8; ++j) {
                     const int t = j >> 2, u = j & 3;
-                    float p = fast_exp2(__builtin_fmaf(s[t][qt][u], kscale, nk[j]) + aq[qt]);
+                    float p = fast_exp2(__builtin_fmaf(s[t][qt][u], kscale, nk[j]));
                     if (kDiag && (32 * h + 8 * g + j) > qloc) p = 0.f;
-                    const float dpv = dp[t][qt][u];
-                    pdp[qt] = __builtin_fmaf(p, dpv, pdp[qt]);
+                    const float dsv = p * dp[t][qt][u];
+                    sds[qt] += dsv;
                     psum[qt] += p;
-                    dsf[qt][j] = (__bf16)(p * (dpv - dl[qt]));
+                    dsf[qt][j] = (__bf16)dsv;
                 }
             }
             // dQ^T += K^T dS^T over these 32 keys
@@ -194,18 +203,20 @@ __global__ __launch_bounds__(kBwdThreads) void dq_bf16_kernel(
             ob[0] = (__bf16)o[0]; ob[1] = (__bf16)o[1]; ob[2] = (__bf16)o[2]; ob[3] = (__bf16)o[3];
             *reinterpret_cast<bf16x4*>(dQ + (head + query) * D + 16 * dt + 4 * g) = ob;
         }
-        // Delta'_i = sum_j P_ij dP_ij from the float32 P and dP of this pass: it is
-        // what rowdot(dO, O) equals for the exact O, free of the rounding of P to
-        // bfloat16 in the forward's PV product.  The dK/dV pass and both sums of
-        // dS use it; rowsum(dS) is then Delta' (1 - sum_j P_ij).
-        float a = pdp[qt], z = psum[qt];
+        // Delta'_i = sum_j P_ij dP_ij from the float32 P and dP of this pass
+        // (= sum_j dS_ij + Delta_i sum_j P_ij): it is what rowdot(dO, O) equals for
+        // the exact O, free of the rounding of P to bfloat16 in the forward's PV
+        // product.  The dK/dV pass and both sums of dS use it; rowsum(dS) is then
+        // Delta' (1 - sum_j P_ij).
+        float a = sds[qt], z = psum[qt];
         a += __shfl_xor(a, 16);
         a += __shfl_xor(a, 32);
         z += __shfl_xor(z, 16);
         z += __shfl_xor(z, 32);
         if (g == 0) {
-            dsum[head + query] = a;
-            rowsum[head + query] = a - a * z;
+            const float dp2 = __builtin_fmaf(dl[qt], z, a);
+            dsum[head + query] = dp2;
+            rowsum[head + query] = dp2 - dp2 * z;
         }
     }
 }
@@ -221,8 +232,8 @@ template <int D>
 struct alignas(1024) DkvSmem {
     unsigned char q[2][128 * D];   // 64 x D bf16 tiles (see tile_off)
     unsigned char o[2][128 * D];   // dO
-    float la[2][64];               // a_i = (c_i - r) log2(e) - L_i
-    float dl[2][64];               // Delta'_i
+    float la[2][64];               // a_i / k',  a_i = (c_i - r) log2(e) - L_i
+    float dl[2][64];               // -Delta'_i
 };
 
 template <int D>
@@ -285,8 +296,8 @@ __global__ __launch_bounds__(kBwdThreads) void dkdv_bf16_kernel(
     };
     auto put_rows = [&](float3 r, int buf) __attribute__((always_inline)) {
         if (tid < 64) {
-            sm.la[buf][tid] = (r.x - cref) * kLog2e - r.y;
-            sm.dl[buf][tid] = r.z;
+            sm.la[buf][tid] = ((r.x - cref) * kLog2e - r.y) / kscale;
+            sm.dl[buf][tid] = -r.z;
         }
     };
     int roff[NDS], coff[NDT];
@@ -304,7 +315,6 @@ __global__ __launch_bounds__(kBwdThreads) void dkdv_bf16_kernel(
             dv[kt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
         }
     float csum[2] = {0.f, 0.f};
-    const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
 
     auto tile = [&](auto diag_tag, int buf) __attribute__((always_inline)) {
         constexpr bool kDiag = decltype(diag_tag)::value;
@@ -315,7 +325,11 @@ __global__ __launch_bounds__(kBwdThreads) void dkdv_bf16_kernel(
             f32x4 s[2][2], dp[2][2];
 #pragma unroll
             for (int t = 0; t < 2; ++t) {
-                // row 32 h + 4 t + (row of roff)
+                // rows 32 h + 4 t + (row of roff); the lane's accumulator rows are the
+                // queries 32 h + 8 g + 4 t + u, whose a_i / k' and -Delta'_i start S
+                // and dP, so the MFMAs leave the exponent's row term and dP - Delta'
+                const f32x4 si = *reinterpret_cast<const f32x4*>(&sm.la[buf][32 * h + 8 * g + 4 * t]);
+                const f32x4 di = *reinterpret_cast<const f32x4*>(&sm.dl[buf][32 * h + 8 * g + 4 * t]);
                 const int rstep = 128 * (32 * h + 4 * t);
 #pragma unroll
                 for (int ds = 0; ds < NDS; ++ds) {
@@ -323,18 +337,12 @@ __global__ __launch_bounds__(kBwdThreads) void dkdv_bf16_kernel(
                     const bf16x8 b = *reinterpret_cast<const bf16x8*>(otile + roff[ds] + rstep);
 #pragma unroll
                     for (int kt = 0; kt < 2; ++kt) {
-                        s[t][kt] = mfma16(a, kf[kt][ds], ds == 0 ? zero : s[t][kt]);
-                        dp[t][kt] = mfma16(b, vf[kt][ds], ds == 0 ? zero : dp[t][kt]);
+                        s[t][kt] = mfma16(a, kf[kt][ds], ds == 0 ? si : s[t][kt]);
+                        dp[t][kt] = mfma16(b, vf[kt][ds], ds == 0 ? di : dp[t][kt]);
                     }
                 }
             }
             // the lane's queries: 32 h + 8 g + j, j = 0..7 (j < 4 from subtile 0)
-            const float4 a0 = *reinterpret_cast<const float4*>(&sm.la[buf][32 * h + 8 * g]);
-            const float4 a1 = *reinterpret_cast<const float4*>(&sm.la[buf][32 * h + 8 * g + 4]);
-            const float4 b0 = *reinterpret_cast<const float4*>(&sm.dl[buf][32 * h + 8 * g]);
-            const float4 b1 = *reinterpret_cast<const float4*>(&sm.dl[buf][32 * h + 8 * g + 4]);
-            const float l8[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
-            const float d8[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
             bf16x8 pb[2], db[2];
 #pragma unroll
             for (int kt = 0; kt < 2; ++kt) {
@@ -343,9 +351,9 @@ __global__ __launch_bounds__(kBwdThreads) void dkdv_bf16_kernel(
 #pragma unroll
                 for (int j = 0; j < 8; ++j) {
                     const int t = j >> 2, u = j & 3;
-                    float p = fast_exp2(__builtin_fmaf(s[t][kt][u], kscale, nk[kt]) + l8[j]);
+                    float p = fast_exp2(__builtin_fmaf(s[t][kt][u], kscale, nk[kt]));
                     if (kDiag && kloc > (32 * h + 8 * g + j)) p = 0.f;
-                    const float dsv = p * (dp[t][kt][u] - d8[j]);
+                    const float dsv = p * dp[t][kt][u];
                     csum[kt] += dsv;
                     pb[kt][j] = (__bf16)p;
                     db[kt][j] = (__bf16)dsv;
