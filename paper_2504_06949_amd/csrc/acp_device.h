@@ -171,6 +171,10 @@ struct TileDma {
 // writes into LDS) have completed.
 __device__ __forceinline__ void wait_vmcnt0() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
+// s_waitcnt vmcnt(0) lgkmcnt(0): additionally, this wave's LDS reads have
+// returned (before a barrier after which other waves overwrite what they read).
+__device__ __forceinline__ void wait_vmcnt0_lgkmcnt0() { __builtin_amdgcn_s_waitcnt(0x0070); }
+
 // ---- workgroup -> (head, block) mapping ------------------------------------
 // Workgroups are dealt round-robin to the 8 XCDs (each with its own L2).  This
 // renumbering gives every XCD a contiguous range of logical ids, so the blocks

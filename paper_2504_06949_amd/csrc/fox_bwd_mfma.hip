@@ -316,79 +316,150 @@ __global__ __launch_bounds__(kBwdThreads) void dkdv_bf16_kernel(
         }
     float csum[2] = {0.f, 0.f};
 
-    auto tile = [&](auto diag_tag, int buf) __attribute__((always_inline)) {
-        constexpr bool kDiag = decltype(diag_tag)::value;
+    // Each query tile is taken in two halves of 32 queries, each in three
+    // phases: A forms S and dP (MFMA; query rows and the accumulator starts from
+    // LDS), B the softmax terms (VALU), C accumulates dV and dK (MFMA; query
+    // columns from LDS).  Every LDS operand is read one phase before it is used,
+    // so its latency passes under other work: the columns of a half during its
+    // phase A, the rows of the second half during the first half's phase C, and
+    // the rows of the next tile's first half during the second half's phase C,
+    // which runs after the barrier that publishes that tile.
+    struct OpA {
+        bf16x8 a[2][NDS], b[2][NDS];
+        f32x4 si[2], di[2];
+    };
+    struct OpC {
+        bf16x8 ao[NDT], aq[NDT];
+    };
+    struct SdP {
+        f32x4 s[2][2], dp[2][2];
+    };
+    struct PdS {
+        bf16x8 pb[2], db[2];
+    };
+    auto load_a = [&](int buf, int h) __attribute__((always_inline)) {
+        OpA r;
         const unsigned char* qtile = sm.q[buf];
         const unsigned char* otile = sm.o[buf];
-#pragma unroll 1
-        for (int h = 0; h < 2; ++h) {          // queries 32 h .. 32 h + 31
-            f32x4 s[2][2], dp[2][2];
 #pragma unroll
-            for (int t = 0; t < 2; ++t) {
-                // rows 32 h + 4 t + (row of roff); the lane's accumulator rows are the
-                // queries 32 h + 8 g + 4 t + u, whose a_i / k' and -Delta'_i start S
-                // and dP, so the MFMAs leave the exponent's row term and dP - Delta'
-                const f32x4 si = *reinterpret_cast<const f32x4*>(&sm.la[buf][32 * h + 8 * g + 4 * t]);
-                const f32x4 di = *reinterpret_cast<const f32x4*>(&sm.dl[buf][32 * h + 8 * g + 4 * t]);
-                const int rstep = 128 * (32 * h + 4 * t);
+        for (int t = 0; t < 2; ++t) {
+            // rows 32 h + 4 t + (row of roff); the lane's accumulator rows are the
+            // queries 32 h + 8 g + 4 t + u, whose a_i / k' and -Delta'_i start S
+            // and dP, so the MFMAs leave the exponent's row term and dP - Delta'
+            r.si[t] = *reinterpret_cast<const f32x4*>(&sm.la[buf][32 * h + 8 * g + 4 * t]);
+            r.di[t] = *reinterpret_cast<const f32x4*>(&sm.dl[buf][32 * h + 8 * g + 4 * t]);
+            const int rstep = 128 * (32 * h + 4 * t);
 #pragma unroll
-                for (int ds = 0; ds < NDS; ++ds) {
-                    const bf16x8 a = *reinterpret_cast<const bf16x8*>(qtile + roff[ds] + rstep);
-                    const bf16x8 b = *reinterpret_cast<const bf16x8*>(otile + roff[ds] + rstep);
-#pragma unroll
-                    for (int kt = 0; kt < 2; ++kt) {
-                        s[t][kt] = mfma16(a, kf[kt][ds], ds == 0 ? si : s[t][kt]);
-                        dp[t][kt] = mfma16(b, vf[kt][ds], ds == 0 ? di : dp[t][kt]);
-                    }
-                }
+            for (int ds = 0; ds < NDS; ++ds) {
+                r.a[t][ds] = *reinterpret_cast<const bf16x8*>(qtile + roff[ds] + rstep);
+                r.b[t][ds] = *reinterpret_cast<const bf16x8*>(otile + roff[ds] + rstep);
             }
-            // the lane's queries: 32 h + 8 g + j, j = 0..7 (j < 4 from subtile 0)
-            bf16x8 pb[2], db[2];
+        }
+        return r;
+    };
+    auto load_c = [&](int buf, int h) __attribute__((always_inline)) {
+        OpC r;
 #pragma unroll
-            for (int kt = 0; kt < 2; ++kt) {
-                int kloc = 32 * (w & 1) + 16 * kt + r16;   // key column within a diagonal tile
-                if constexpr (kDiag) asm volatile("" : "+v"(kloc));
+        for (int dt = 0; dt < NDT; ++dt) {
+            r.ao[dt] = tile_col8_at(sm.o[buf] + coff[dt] + 128 * 32 * h);
+            r.aq[dt] = tile_col8_at(sm.q[buf] + coff[dt] + 128 * 32 * h);
+        }
+        return r;
+    };
+    auto phase_a = [&](const OpA& ra) __attribute__((always_inline)) {
+        SdP x;
 #pragma unroll
-                for (int j = 0; j < 8; ++j) {
-                    const int t = j >> 2, u = j & 3;
-                    float p = fast_exp2(__builtin_fmaf(s[t][kt][u], kscale, nk[kt]));
-                    if (kDiag && kloc > (32 * h + 8 * g + j)) p = 0.f;
-                    const float dsv = p * dp[t][kt][u];
-                    csum[kt] += dsv;
-                    pb[kt][j] = (__bf16)p;
-                    db[kt][j] = (__bf16)dsv;
-                }
-            }
-            // dV^T += dO^T P,  dK^T += Q^T dS over these 32 queries
+        for (int t = 0; t < 2; ++t)
 #pragma unroll
-            for (int dt = 0; dt < NDT; ++dt) {
-                const bf16x8 ao = tile_col8_at(otile + coff[dt] + 128 * 32 * h);
-                const bf16x8 aq = tile_col8_at(qtile + coff[dt] + 128 * 32 * h);
+            for (int ds = 0; ds < NDS; ++ds)
 #pragma unroll
                 for (int kt = 0; kt < 2; ++kt) {
-                    dv[kt][dt] = mfma16(ao, pb[kt], dv[kt][dt]);
-                    dk[kt][dt] = mfma16(aq, db[kt], dk[kt][dt]);
+                    x.s[t][kt] = mfma16(ra.a[t][ds], kf[kt][ds], ds == 0 ? ra.si[t] : x.s[t][kt]);
+                    x.dp[t][kt] = mfma16(ra.b[t][ds], vf[kt][ds], ds == 0 ? ra.di[t] : x.dp[t][kt]);
                 }
+        return x;
+    };
+    // The lane's queries are 32 h + 8 g + j, j = 0..7 (j < 4 from subtile 0).
+    // kMask: the tile may be this wave's diagonal one, where key kloc is dropped
+    // for the queries before it.  The test is kq > 32 h + j with the lane's
+    // kq = kloc - 8 g, lowered out of reach on tiles that are not diagonal, so
+    // that the comparisons take immediate operands.
+    auto phase_b = [&](auto mask_tag, const SdP& x, int h, int kq0) __attribute__((always_inline)) {
+        constexpr bool kMask = decltype(mask_tag)::value;
+        PdS y;
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt) {
+            int kq = kq0 + 16 * kt;
+            if constexpr (kMask) asm volatile("" : "+v"(kq));
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const int t = j >> 2, u = j & 3;
+                float p = fast_exp2(__builtin_fmaf(x.s[t][kt][u], kscale, nk[kt]));
+                if (kMask && kq > 32 * h + j) p = 0.f;
+                const float dsv = p * x.dp[t][kt][u];
+                csum[kt] += dsv;
+                y.pb[kt][j] = (__bf16)p;
+                y.db[kt][j] = (__bf16)dsv;
             }
         }
+        return y;
+    };
+    // dV^T += dO^T P,  dK^T += Q^T dS over the half's 32 queries
+    auto phase_c = [&](const OpC& rc, const PdS& y) __attribute__((always_inline)) {
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+            for (int kt = 0; kt < 2; ++kt) {
+                dv[kt][dt] = mfma16(rc.ao[dt], y.pb[kt], dv[kt][dt]);
+                dk[kt][dt] = mfma16(rc.aq[dt], y.db[kt], dk[kt][dt]);
+            }
     };
 
+    // tile m_lo in LDS and published; tile m_lo + 1 on its way
     put_rows(issue(m_lo, 0), 0);
     wait_vmcnt0();
+    __syncthreads();
+    float3 rnext = make_float3(0.f, 0.f, 0.f);
+    if (m_lo < m_hi) rnext = issue(m_lo + 1, 1);
+    // (the rows are read whether or not this wave takes the tile, so that no
+    // path keeps an older set of them live through the loop)
+    OpA ra = load_a(0, 0);
     int buf = 0;
-    for (int m = m_lo; m <= m_hi; ++m) {
-        __syncthreads();   // tile m is in LDS; every wave is done with tile m - 1
-        const bool more = m < m_hi;
-        float3 rnext = make_float3(0.f, 0.f, 0.f);
-        if (more) rnext = issue(m + 1, buf ^ 1);
-        if (m >= nw && m <= w_hi) {
-            if (m == nw) tile(std::true_type{}, buf);
-            else tile(std::false_type{}, buf);
+    // One query tile.  Waves 0-1 meet their diagonal tile at m_lo, waves 2-3 at
+    // m_lo + 1; those two tiles go through the masking variant.
+    auto step = [&](auto mask_tag, int m) __attribute__((always_inline)) {
+        const bool act = m >= nw && m <= w_hi;
+        const int kq0 = 32 * (w & 1) + r16 - 8 * g - (m == nw ? 0 : 4096);
+        OpC rc;
+        PdS y;
+        if (act) {
+            // first half
+            rc = load_c(buf, 0);
+            SdP x = phase_a(ra);
+            y = phase_b(mask_tag, x, 0, kq0);
+            ra = load_a(buf, 1);
+            phase_c(rc, y);
+            // (not merged with the second half's phase A: both hold four operand
+            // sets and would not fit the registers of two waves per SIMD)
+            __builtin_amdgcn_sched_barrier(0);
+            // second half up to its softmax terms
+            rc = load_c(buf, 1);
+            x = phase_a(ra);
+            y = phase_b(mask_tag, x, 1, kq0);
         }
-        if (more) put_rows(rnext, buf ^ 1);
-        wait_vmcnt0();
+        if (m < m_hi) put_rows(rnext, buf ^ 1);
+        // tile m + 1 has landed and every wave's reads of tile m are complete
+        wait_vmcnt0_lgkmcnt0();
+        __syncthreads();
+        if (m + 1 < m_hi) rnext = issue(m + 2, buf);
+        if (m < m_hi) ra = load_a(buf ^ 1, 0);
+        if (act) phase_c(rc, y);
         buf ^= 1;
-    }
+    };
+    const int m_diag = min(m_lo + 1, m_hi);
+    int m = m_lo;
+    for (; m <= m_diag; ++m) step(std::true_type{}, m);
+    for (; m <= m_hi; ++m) step(std::false_type{}, m);
 
     if (!wave_on) return;
 #pragma unroll
