@@ -123,74 +123,137 @@ __global__ __launch_bounds__(kBwdThreads) void dq_bf16_kernel(
     float sds[2] = {0.f, 0.f};   // sum_j dS_ij (lane partial)
     float psum[2] = {0.f, 0.f};  // sum_j P_ij (lane partial)
 
-    auto tile = [&](auto diag_tag, int buf) __attribute__((always_inline)) {
-        constexpr bool kDiag = decltype(diag_tag)::value;
+    // Each key tile is taken in two halves of 32 keys, each in three phases: A
+    // forms S^T and dP^T (MFMA; key rows from LDS), B the softmax terms (VALU),
+    // C accumulates dQ (MFMA; key columns from LDS).  As in the dK/dV pass, each
+    // LDS operand is read one phase before it is used, and the barrier that
+    // publishes the next tile sits before the second half's phase C.
+    struct OpA {
+        bf16x8 a[2][NDS], b[2][NDS];
+        float4 lo, hi;                 // key biases of the lane's 8 keys
+    };
+    struct OpC {
+        bf16x8 ak[NDT];
+    };
+    struct SdP {
+        f32x4 s[2][2], dp[2][2];
+    };
+    struct DsH {   // dS of the half in the B-operand layout of the dQ product
+        bf16x8 d[2];
+    };
+    auto load_a = [&](int buf, int h) __attribute__((always_inline)) {
+        OpA r;
         const unsigned char* ktile = sm.k[buf];
         const unsigned char* vtile = sm.v[buf];
-        const float* nc = sm.kb[buf];
-#pragma unroll 1
-        for (int h = 0; h < 2; ++h) {          // keys 32 h .. 32 h + 31
-            f32x4 s[2][2], dp[2][2];
 #pragma unroll
-            for (int t = 0; t < 2; ++t) {
-                // row 32 h + 4 t + (row of roff)
-                const int rstep = 128 * (32 * h + 4 * t);
+        for (int t = 0; t < 2; ++t) {
+            // row 32 h + 4 t + (row of roff)
+            const int rstep = 128 * (32 * h + 4 * t);
 #pragma unroll
-                for (int ds = 0; ds < NDS; ++ds) {
-                    const bf16x8 a = *reinterpret_cast<const bf16x8*>(ktile + roff[ds] + rstep);
-                    const bf16x8 b = *reinterpret_cast<const bf16x8*>(vtile + roff[ds] + rstep);
+            for (int ds = 0; ds < NDS; ++ds) {
+                r.a[t][ds] = *reinterpret_cast<const bf16x8*>(ktile + roff[ds] + rstep);
+                r.b[t][ds] = *reinterpret_cast<const bf16x8*>(vtile + roff[ds] + rstep);
+            }
+        }
+        r.lo = *reinterpret_cast<const float4*>(&sm.kb[buf][32 * h + 8 * g]);
+        r.hi = *reinterpret_cast<const float4*>(&sm.kb[buf][32 * h + 8 * g + 4]);
+        return r;
+    };
+    auto load_c = [&](int buf, int h) __attribute__((always_inline)) {
+        OpC r;
 #pragma unroll
-                    for (int qt = 0; qt < 2; ++qt) {
-                        s[t][qt] = mfma16(a, qf[qt][ds], ds == 0 ? sinit[qt] : s[t][qt]);
-                        dp[t][qt] = mfma16(b, dof[qt][ds], ds == 0 ? dinit[qt] : dp[t][qt]);
-                    }
+        for (int dt = 0; dt < NDT; ++dt) r.ak[dt] = tile_col8_at(sm.k[buf] + coff[dt] + 128 * 32 * h);
+        return r;
+    };
+    auto phase_a = [&](const OpA& ra) __attribute__((always_inline)) {
+        SdP x;
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+            for (int ds = 0; ds < NDS; ++ds)
+#pragma unroll
+                for (int qt = 0; qt < 2; ++qt) {
+                    x.s[t][qt] = mfma16(ra.a[t][ds], qf[qt][ds], ds == 0 ? sinit[qt] : x.s[t][qt]);
+                    x.dp[t][qt] = mfma16(ra.b[t][ds], dof[qt][ds], ds == 0 ? dinit[qt] : x.dp[t][qt]);
                 }
-            }
-            const float4 lo = *reinterpret_cast<const float4*>(nc + 32 * h + 8 * g);
-            const float4 hi = *reinterpret_cast<const float4*>(nc + 32 * h + 8 * g + 4);
-            const float nk[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
-            bf16x8 dsf[2];
+        return x;
+    };
+    // The lane's keys are 32 h + 8 g + j, j = 0..7 (j < 4 from subtile 0), its
+    // query qloc = 32 (w % 2) + 16 qt + r16 within the tile.  kMask: the tile may
+    // be this wave's diagonal one, where keys after the query are dropped.  The
+    // test is 32 h + j > qk with the lane's qk = qloc - 8 g, raised out of reach
+    // on tiles that are not diagonal, so that the comparisons take immediates.
+    auto phase_b = [&](auto mask_tag, const SdP& x, const OpA& ra, int h, int qk0) __attribute__((always_inline)) {
+        constexpr bool kMask = decltype(mask_tag)::value;
+        const float nk[8] = {ra.lo.x, ra.lo.y, ra.lo.z, ra.lo.w, ra.hi.x, ra.hi.y, ra.hi.z, ra.hi.w};
+        bf16x8 dsf[2];
 #pragma unroll
-            for (int qt = 0; qt < 2; ++qt) {
-                int qloc = 32 * (w & 1) + 16 * qt + r16;   // query row within a diagonal tile
-                if constexpr (kDiag) asm volatile("" : "+v"(qloc));
+        for (int qt = 0; qt < 2; ++qt) {
+            int qk = qk0 + 16 * qt;
+            if constexpr (kMask) asm volatile("" : "+v"(qk));
 #pragma unroll
-                for (int j = 0; j < 8; ++j) {
-                    const int t = j >> 2, u = j & 3;
-                    float p = fast_exp2(__builtin_fmaf(s[t][qt][u], kscale, nk[j]));
-                    if (kDiag && (32 * h + 8 * g + j) > qloc) p = 0.f;
-                    const float dsv = p * dp[t][qt][u];
-                    sds[qt] += dsv;
-                    psum[qt] += p;
-                    dsf[qt][j] = (__bf16)dsv;
-                }
+            for (int j = 0; j < 8; ++j) {
+                const int t = j >> 2, u = j & 3;
+                float p = fast_exp2(__builtin_fmaf(x.s[t][qt][u], kscale, nk[j]));
+                if (kMask && 32 * h + j > qk) p = 0.f;
+                const float dsv = p * x.dp[t][qt][u];
+                sds[qt] += dsv;
+                psum[qt] += p;
+                dsf[qt][j] = (__bf16)dsv;
             }
-            // dQ^T += K^T dS^T over these 32 keys
+        }
+        return DsH{{dsf[0], dsf[1]}};
+    };
+    // dQ^T += K^T dS^T over the half's 32 keys
+    auto phase_c = [&](const OpC& rc, const DsH& y) __attribute__((always_inline)) {
 #pragma unroll
-            for (int dt = 0; dt < NDT; ++dt) {
-                const bf16x8 a = tile_col8_at(ktile + coff[dt] + 128 * 32 * h);
-                acc[0][dt] = mfma16(a, dsf[0], acc[0][dt]);
-                acc[1][dt] = mfma16(a, dsf[1], acc[1][dt]);
-            }
+        for (int dt = 0; dt < NDT; ++dt) {
+            acc[0][dt] = mfma16(rc.ak[dt], y.d[0], acc[0][dt]);
+            acc[1][dt] = mfma16(rc.ak[dt], y.d[1], acc[1][dt]);
         }
     };
 
+    // tile n_lo in LDS and published; tile n_lo + 1 on its way
     put_kb(issue(n_lo, 0), 0);
     wait_vmcnt0();
+    __syncthreads();
+    float4 cnext = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (n_lo < n_hi) cnext = issue(n_lo + 1, 1);
+    // (read whether or not this wave takes the tile: no path keeps an older set
+    // of them live through the loop)
+    OpA ra = load_a(0, 0);
     int buf = 0;
-    for (int n = n_lo; n <= n_hi; ++n) {
-        __syncthreads();   // tile n is in LDS; every wave is done with tile n - 1
-        const bool more = n < n_hi;
-        float4 cnext = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (more) cnext = issue(n + 1, buf ^ 1);
-        if (n >= w_lo && n <= mw) {
-            if (n == mw) tile(std::true_type{}, buf);
-            else tile(std::false_type{}, buf);
+    auto step = [&](auto mask_tag, int n) __attribute__((always_inline)) {
+        const bool act = n >= w_lo && n <= mw;
+        const int qk0 = 32 * (w & 1) + r16 - 8 * g + (n == mw ? 0 : 4096);
+        OpC rc;
+        DsH y;
+        if (act) {
+            rc = load_c(buf, 0);
+            SdP x = phase_a(ra);
+            y = phase_b(mask_tag, x, ra, 0, qk0);
+            ra = load_a(buf, 1);
+            phase_c(rc, y);
+            __builtin_amdgcn_sched_barrier(0);
+            rc = load_c(buf, 1);
+            x = phase_a(ra);
+            y = phase_b(mask_tag, x, ra, 1, qk0);
         }
-        if (more) put_kb(cnext, buf ^ 1);
-        wait_vmcnt0();
+        if (n < n_hi) put_kb(cnext, buf ^ 1);
+        // tile n + 1 has landed and every wave's reads of tile n are complete
+        wait_vmcnt0_lgkmcnt0();
+        __syncthreads();
+        if (n + 1 < n_hi) cnext = issue(n + 2, buf);
+        if (n < n_hi) ra = load_a(buf ^ 1, 0);
+        if (act) phase_c(rc, y);
         buf ^= 1;
-    }
+    };
+    // The diagonal tiles (m0 for waves 0-1, m0 + 1 = n_hi for waves 2-3) are the
+    // last two and go through the masking variant.
+    const int n_mask = max(n_lo, n_hi - 1);
+    int n = n_lo;
+    for (; n < n_mask; ++n) step(std::false_type{}, n);
+    for (; n <= n_hi; ++n) step(std::true_type{}, n);
 
     if (!wave_on) return;
 #pragma unroll
