@@ -145,40 +145,78 @@ __global__ __launch_bounds__(kFwdThreads) void fwd_bf16_kernel(
 #pragma unroll
     for (int dt = 0; dt < NDT; ++dt) voff[dt] = tile_off(8 * g + (r16 >> 2), 16 * dt + 4 * (r16 & 3));
 
-    // One 64-key tile for this wave; kDiag masks keys after the query.
-    auto tile = [&](auto diag_tag, int n, int buf) __attribute__((always_inline)) {
-        constexpr bool kDiag = decltype(diag_tag)::value;
-        const unsigned char* ktile = sm.k[buf];
-        const unsigned char* vtile = sm.v[buf];
-        const float* nc = sm.kb[buf];
+    // Each key tile is taken in three phases: A forms S^T (MFMA; key rows and
+    // key biases from LDS), B the weights P (VALU), C accumulates O^T (MFMA; V^T
+    // columns from LDS).  Every LDS operand is read one phase before it is used:
+    // the V^T columns during phase A, the next tile's key rows during phase C,
+    // which runs after the barrier that publishes that tile.
+    struct OpA {
+        bf16x8 a[4][NDS];
+        float4 nk[4];   // key biases of the lane's keys 32 ks + 8 g + (0..3 | 4..7)
+    };
+    struct OpC {
+        bf16x8 v[NDT][2];
+    };
+    struct STile {
         f32x4 s[4][2];
+    };
+    struct PTile {
+        bf16x8 p[2][2];
+    };
+    auto load_a = [&](int buf) __attribute__((always_inline)) {
+        OpA r;
+        const unsigned char* ktile = sm.k[buf];
 #pragma unroll
-        for (int kt = 0; kt < 4; ++kt) {
+        for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+            for (int ds = 0; ds < NDS; ++ds)
+                // row krow = 32 (kt / 2) + 4 (kt % 2) + (row of koff)
+                r.a[kt][ds] = *reinterpret_cast<const bf16x8*>(
+                    ktile + koff[ds] + 128 * (32 * (kt >> 1) + 4 * (kt & 1)));
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            r.nk[i] = *reinterpret_cast<const float4*>(&sm.kb[buf][32 * (i >> 1) + 8 * g + 4 * (i & 1)]);
+        return r;
+    };
+    auto load_c = [&](int buf) __attribute__((always_inline)) {
+        OpC r;
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+            for (int ks = 0; ks < 2; ++ks) r.v[dt][ks] = tile_col8_at(sm.v[buf] + voff[dt] + 128 * 32 * ks);
+        return r;
+    };
+    auto phase_a = [&](const OpA& ra) __attribute__((always_inline)) {
+        STile x;
+#pragma unroll
+        for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
             for (int ds = 0; ds < NDS; ++ds) {
-                // row krow = 32 (kt / 2) + 4 (kt % 2) + (row of koff)
-                const bf16x8 a = *reinterpret_cast<const bf16x8*>(
-                    ktile + koff[ds] + 128 * (32 * (kt >> 1) + 4 * (kt & 1)));
-                s[kt][0] = mfma16(a, qf[0][ds], ds == 0 ? sinit[0] : s[kt][0]);
-                s[kt][1] = mfma16(a, qf[1][ds], ds == 0 ? sinit[1] : s[kt][1]);
+                x.s[kt][0] = mfma16(ra.a[kt][ds], qf[0][ds], ds == 0 ? sinit[0] : x.s[kt][0]);
+                x.s[kt][1] = mfma16(ra.a[kt][ds], qf[1][ds], ds == 0 ? sinit[1] : x.s[kt][1]);
             }
-        }
-        // the lane's keys are 32 ks + 8 g + j, j = 0..7 (j < 4 from tile 2ks)
+        return x;
+    };
+    // The lane's keys are 32 ks + 8 g + j, j = 0..7 (j < 4 from subtile 2 ks),
+    // its query qloc = 32 (w % 2) + 16 qt + r16 within the tile.  kMask: the tile
+    // may be this wave's diagonal one, where keys after the query are dropped.
+    // The test is 32 ks + j > qk with the lane's qk = qloc - 8 g, raised out of
+    // reach on tiles that are not diagonal, so that the comparisons take
+    // immediate operands.
+    auto phase_b = [&](auto mask_tag, const STile& x, const OpA& ra, int qk0) __attribute__((always_inline)) {
+        constexpr bool kMask = decltype(mask_tag)::value;
         float nk[2][8];
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) {
-            const float4 lo = *reinterpret_cast<const float4*>(nc + 32 * ks + 8 * g);
-            const float4 hi = *reinterpret_cast<const float4*>(nc + 32 * ks + 8 * g + 4);
+            const float4 lo = ra.nk[2 * ks], hi = ra.nk[2 * ks + 1];
             nk[ks][0] = lo.x; nk[ks][1] = lo.y; nk[ks][2] = lo.z; nk[ks][3] = lo.w;
             nk[ks][4] = hi.x; nk[ks][5] = hi.y; nk[ks][6] = hi.z; nk[ks][7] = hi.w;
         }
-        bf16x8 pf[2][2];
+        PTile pt;
 #pragma unroll
         for (int qt = 0; qt < 2; ++qt) {
-            // query row within a diagonal tile; the empty asm keeps the mask
-            // comparisons inside this (rare) tile instead of hoisted into SGPRs
-            int qloc = 32 * (w & 1) + 16 * qt + r16;
-            if constexpr (kDiag) asm volatile("" : "+v"(qloc));
+            int qk = qk0 + 16 * qt;
+            if constexpr (kMask) asm volatile("" : "+v"(qk));
             if constexpr (kFixed) {
                 float l = lrun[qt], lb = lbf[qt];
 #pragma unroll
@@ -186,12 +224,12 @@ __global__ __launch_bounds__(kFwdThreads) void fwd_bf16_kernel(
 #pragma unroll
                     for (int j = 0; j < 8; ++j) {
                         float p = fast_exp2(
-                            __builtin_fmaf(s[2 * ks + (j >> 2)][qt][j & 3], kscale, nk[ks][j]));
-                        if (kDiag && (32 * ks + 8 * g + j) > qloc) p = 0.f;
+                            __builtin_fmaf(x.s[2 * ks + (j >> 2)][qt][j & 3], kscale, nk[ks][j]));
+                        if (kMask && 32 * ks + j > qk) p = 0.f;
                         l += p;
-                        pf[qt][ks][j] = (__bf16)p;
+                        pt.p[qt][ks][j] = (__bf16)p;
                     }
-                    lb = sum_bf16x8(pf[qt][ks], lb);
+                    lb = sum_bf16x8(pt.p[qt][ks], lb);
                 }
                 lrun[qt] = l;
                 lbf[qt] = lb;
@@ -202,8 +240,8 @@ __global__ __launch_bounds__(kFwdThreads) void fwd_bf16_kernel(
                 for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
                     for (int j = 0; j < 8; ++j) {
-                        float v = __builtin_fmaf(s[2 * ks + (j >> 2)][qt][j & 3], kscale, nk[ks][j]);
-                        if (kDiag && (32 * ks + 8 * g + j) > qloc) v = -INFINITY;
+                        float v = __builtin_fmaf(x.s[2 * ks + (j >> 2)][qt][j & 3], kscale, nk[ks][j]);
+                        if (kMask && 32 * ks + j > qk) v = -INFINITY;
                         y[ks][j] = v;
                         mx = fmaxf(mx, v);
                     }
@@ -221,38 +259,59 @@ __global__ __launch_bounds__(kFwdThreads) void fwd_bf16_kernel(
                     for (int j = 0; j < 8; ++j) {
                         const float p = fast_exp2(y[ks][j] - mnew);
                         l += p;
-                        pf[qt][ks][j] = (__bf16)p;
+                        pt.p[qt][ks][j] = (__bf16)p;
                     }
                 lrun[qt] = l;
             }
         }
-        // O^T += V^T P^T
+        return pt;
+    };
+    // O^T += V^T P^T
+    auto phase_c = [&](const OpC& rc, const PTile& pt) __attribute__((always_inline)) {
 #pragma unroll
         for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
             for (int ks = 0; ks < 2; ++ks) {
-                const bf16x8 a = tile_col8_at(vtile + voff[dt] + 128 * 32 * ks);
-                acc[0][dt] = mfma16(a, pf[0][ks], acc[0][dt]);
-                acc[1][dt] = mfma16(a, pf[1][ks], acc[1][dt]);
+                acc[0][dt] = mfma16(rc.v[dt][ks], pt.p[0][ks], acc[0][dt]);
+                acc[1][dt] = mfma16(rc.v[dt][ks], pt.p[1][ks], acc[1][dt]);
             }
     };
 
+    // tile n_lo in LDS and published; tile n_lo + 1 on its way
     put_kb(issue(n_lo, 0), 0);
     wait_vmcnt0();
+    __syncthreads();
+    float4 cnext = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (n_lo < n_hi) cnext = issue(n_lo + 1, 1);
+    // (read whether or not this wave takes the tile: no path keeps an older set
+    // of them live through the loop)
+    OpA ra = load_a(0);
     int buf = 0;
-    for (int n = n_lo; n <= n_hi; ++n) {
-        __syncthreads();   // tile n is in LDS; every wave is done with tile n - 1
-        const bool more = n < n_hi;
-        float4 cnext = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (more) cnext = issue(n + 1, buf ^ 1);
-        if (n >= w_lo && n <= mw) {
-            if (n == mw) tile(std::true_type{}, n, buf);
-            else tile(std::false_type{}, n, buf);
+    auto step = [&](auto mask_tag, int n) __attribute__((always_inline)) {
+        const bool act = n >= w_lo && n <= mw;
+        const int qk0 = 32 * (w & 1) + r16 - 8 * g + (n == mw ? 0 : 4096);
+        OpC rc;
+        PTile pt;
+        if (act) {
+            rc = load_c(buf);
+            const STile x = phase_a(ra);
+            pt = phase_b(mask_tag, x, ra, qk0);
         }
-        if (more) put_kb(cnext, buf ^ 1);
-        wait_vmcnt0();
+        if (n < n_hi) put_kb(cnext, buf ^ 1);
+        // tile n + 1 has landed and every wave's reads of tile n are complete
+        wait_vmcnt0_lgkmcnt0();
+        __syncthreads();
+        if (n + 1 < n_hi) cnext = issue(n + 2, buf);
+        if (n < n_hi) ra = load_a(buf ^ 1);
+        if (act) phase_c(rc, pt);
         buf ^= 1;
-    }
+    };
+    // The diagonal tiles (m0 for waves 0-1, m0 + 1 for waves 2-3) are the last
+    // two and go through the masking variant.
+    const int n_mask = max(n_lo, n_hi - 1);
+    int n = n_lo;
+    for (; n < n_mask; ++n) step(std::false_type{}, n);
+    for (; n <= n_hi; ++n) step(std::true_type{}, n);
 
     if (!wave_on) return;
 #pragma unroll
