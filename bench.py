@@ -73,7 +73,7 @@ def run_workload(name: str, steps: int, warmup: int, eps_override=None, unpruned
 
     def step(e):
         acp.forward(g["q"], g["k"], g["v"], g["log_f"], e, ws=ws, out=(o, lse))
-        acp.backward(g["q"], g["k"], g["v"], g["do"], ws, out=grads)
+        acp.backward(g["q"], g["k"], g["v"], o, g["do"], ws, out=grads)
 
     def timed(e):
         for _ in range(warmup):

@@ -83,8 +83,8 @@ typedef struct {
 
 /* Size in bytes of the workspace that acp_boundary, fox_attn_fwd and fox_attn_bwd
  * need for these shapes (the same figure for all three).  Holds the plan above,
- * the float64 norm partials, the float32 copy of O and the reduced log-sum-exp
- * that the backward pass reads, and the backward's per-row sums. */
+ * the float64 norm partials, the reduced log-sum-exp that the backward pass reads,
+ * and the backward's per-row sums. */
 acp_status acp_workspace_size(int B, int H, int L, int d, acp_dtype dt, size_t* bytes);
 
 /* Where the plan lives inside a workspace of these shapes. */
@@ -111,8 +111,8 @@ acp_status acp_boundary(const void* Q, const void* K, const float* log_f, acp_dt
  *   in : Q, K, V [B,H,L,d] dt; log_f [B,H,L] float; eps.
  *   out: O [B,H,L,d] dt; lse [B,H,L] float, the natural-log row log-sum-exp of the
  *        masked logits q.k/sqrt(d) + c_i - c_j.
- *   ws : workspace of acp_workspace_size() bytes; keeps the plan, a float32 copy of
- *        O and the reduced log-sum-exp for fox_attn_bwd. */
+ *   ws : workspace of acp_workspace_size() bytes; keeps the plan and the reduced
+ *        log-sum-exp for fox_attn_bwd. */
 acp_status fox_attn_fwd(const void* Q, const void* K, const void* V, const float* log_f,
                         acp_dtype dt, int B, int H, int L, int d, double eps,
                         void* O, float* lse, void* ws, size_t ws_bytes, void* stream);
@@ -123,12 +123,13 @@ acp_status fox_attn_fwd(const void* Q, const void* K, const void* V, const float
  * dS = P o (dO V^T - rowdot(dO, O)):
  *   dQ = dS K / sqrt(d), dK = dS^T Q / sqrt(d), dV = P^T dO,
  *   dlog_f_l = sum_{i >= l} (rowsum(dS)_i - colsum(dS)_i).
- *   in : Q, K, V, dO [B,H,L,d] dt; ws exactly as the matching fox_attn_fwd left it
- *        (same shapes, dtype and eps; its plan, float32 O and log-sum-exp are read).
+ *   in : Q, K, V, O, dO [B,H,L,d] dt, O being the output of the matching
+ *        fox_attn_fwd; ws exactly as that call left it (same shapes, dtype and
+ *        eps; its plan and log-sum-exp are read).
  *   out: dQ, dK, dV [B,H,L,d] dt; dlog_f [B,H,L] float.  Outputs are overwritten,
  *        not accumulated into.  ws: the backward's row sums are written there. */
-acp_status fox_attn_bwd(const void* Q, const void* K, const void* V, const void* dO,
-                        acp_dtype dt, int B, int H, int L, int d,
+acp_status fox_attn_bwd(const void* Q, const void* K, const void* V, const void* O,
+                        const void* dO, acp_dtype dt, int B, int H, int L, int d,
                         void* dQ, void* dK, void* dV, float* dlog_f,
                         void* ws, size_t ws_bytes, void* stream);
 
@@ -142,7 +143,8 @@ enum {
     ACP_K_ROWNORM = 0,  /* Q/K squared row-norm maxima          */
     ACP_K_PLAN = 1,     /* cumsum, threshold, boundary search   */
     ACP_K_FWD = 2,      /* attention forward                    */
-    ACP_K_DSUM = 3,     /* rowdot(dO, O)                        */
+    ACP_K_DSUM = 3,     /* rowdot(dO, O) (float32 path; the bf16
+                           dQ pass forms it itself)              */
     ACP_K_DQ = 4,       /* dQ and row sums of dS                */
     ACP_K_DKDV = 5,     /* dK, dV and column sums of dS         */
     ACP_K_DLOGF = 6,    /* reverse cumulative sum -> dlog f     */

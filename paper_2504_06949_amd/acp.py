@@ -54,7 +54,7 @@ _SIGS = {
     "acp_plan_offsets": [_i, _i, _i, _i, _i, ctypes.POINTER(PlanLayout)],
     "acp_boundary": [_p, _p, _p, _i, _i, _i, _i, _i, _d, _p, _p, _p, _p, _p, _p, _p, _p, _sz, _p],
     "fox_attn_fwd": [_p, _p, _p, _p, _i, _i, _i, _i, _i, _d, _p, _p, _p, _sz, _p],
-    "fox_attn_bwd": [_p, _p, _p, _p, _i, _i, _i, _i, _i, _p, _p, _p, _p, _p, _sz, _p],
+    "fox_attn_bwd": [_p, _p, _p, _p, _p, _i, _i, _i, _i, _i, _p, _p, _p, _p, _p, _sz, _p],
     "acp_timing_enable": [_i],
     "acp_timing_reset": [],
     "acp_timing_read": [ctypes.POINTER(KernelTimes)],
@@ -123,9 +123,10 @@ def fox_attn_fwd(Q, K, V, log_f, dt, B, H, L, d, eps, O, lse, ws, ws_bytes, stre
     return lib().fox_attn_fwd(Q, K, V, log_f, dt, B, H, L, d, eps, O, lse, ws, ws_bytes, stream)
 
 
-def fox_attn_bwd(Q, K, V, dO, dt, B, H, L, d, dQ, dK, dV, dlog_f, ws, ws_bytes, stream) -> int:
-    return lib().fox_attn_bwd(Q, K, V, dO, dt, B, H, L, d, dQ, dK, dV, dlog_f, ws, ws_bytes,
-                              stream)
+def fox_attn_bwd(Q, K, V, O, dO, dt, B, H, L, d, dQ, dK, dV, dlog_f, ws, ws_bytes,
+                 stream) -> int:
+    return lib().fox_attn_bwd(Q, K, V, O, dO, dt, B, H, L, d, dQ, dK, dV, dlog_f, ws,
+                              ws_bytes, stream)
 
 
 def acp_timing_enable(on: bool):
@@ -224,18 +225,19 @@ def forward(q, k, v, log_f, eps: float, ws: torch.Tensor | None = None, out=None
     return o, lse, ws
 
 
-def backward(q, k, v, do, ws: torch.Tensor, out=None):
-    """Returns (dQ, dK, dV, dlog_f) for the forward that filled `ws`."""
-    dev = _dev(q, k, v, do)
+def backward(q, k, v, o, do, ws: torch.Tensor, out=None):
+    """Returns (dQ, dK, dV, dlog_f) for the forward that produced `o` and filled `ws`."""
+    dev = _dev(q, k, v, o, do)
     B, H, L, d = _shape(q)
-    if do.shape != q.shape or do.dtype != q.dtype:
-        raise ValueError("dO must match Q")
+    for name, t in (("O", o), ("dO", do)):
+        if t.shape != q.shape or t.dtype != q.dtype:
+            raise ValueError(name + " must match Q")
     if out is None:
         dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
         dlf = torch.empty((B, H, L), dtype=torch.float32, device=dev)
     else:
         dq, dk, dv, dlf = out
-    _check(fox_attn_bwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), do.data_ptr(), _dt(q),
+    _check(fox_attn_bwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), do.data_ptr(), _dt(q),
                         B, H, L, d, dq.data_ptr(), dk.data_ptr(), dv.data_ptr(), dlf.data_ptr(),
                         ws.data_ptr(), ws.numel(), _stream(dev)))
     return dq, dk, dv, dlf

@@ -31,7 +31,7 @@ acp_status ok() {
 }
 
 struct Layout {
-    size_t c, u, delta, rs, ce, kept, flags, part, lse2, o32, dsum, rowsum, colsum, total;
+    size_t c, u, delta, rs, ce, kept, flags, part, lse2, dsum, rowsum, colsum, total;
     int nchunk;
 };
 
@@ -54,7 +54,6 @@ Layout layout(int B, int H, int L, int d) {
     y.flags = take(BH * 4);
     y.part = take(BH * 2 * (size_t)y.nchunk * 8);
     y.lse2 = take(BHL * 4);
-    y.o32 = take(BHL * (size_t)d * 4);
     y.dsum = take(BHL * 4);
     y.rowsum = take(BHL * 4);
     y.colsum = take(BHL * 4);
@@ -281,19 +280,20 @@ acp_status fox_attn_fwd(const void* Q, const void* K, const void* V, const float
     f.row_start = (const int*)(w + y.rs);
     f.u = (const double*)(w + y.u);
     f.O = O;
-    f.O32 = (float*)(w + y.o32);
     f.lse = lse;
     f.lse2 = (float*)(w + y.lse2);
     return hip_status(acp::launch_fwd(f, (hipStream_t)stream), "fox_attn_fwd launch");
 }
 
-acp_status fox_attn_bwd(const void* Q, const void* K, const void* V, const void* dO,
-                        acp_dtype dt, int B, int H, int L, int d, void* dQ, void* dK, void* dV,
-                        float* dlog_f, void* ws, size_t ws_bytes, void* stream) {
+acp_status fox_attn_bwd(const void* Q, const void* K, const void* V, const void* O,
+                        const void* dO, acp_dtype dt, int B, int H, int L, int d, void* dQ,
+                        void* dK, void* dV, float* dlog_f, void* ws, size_t ws_bytes,
+                        void* stream) {
     ACP_TRY(check_shape(B, H, L, d, dt));
     ACP_TRY(check_ptr(Q, "Q"));
     ACP_TRY(check_ptr(K, "K"));
     ACP_TRY(check_ptr(V, "V"));
+    ACP_TRY(check_ptr(O, "O"));
     ACP_TRY(check_ptr(dO, "dO"));
     ACP_TRY(check_ptr(dQ, "dQ"));
     ACP_TRY(check_ptr(dK, "dK"));
@@ -303,13 +303,12 @@ acp_status fox_attn_bwd(const void* Q, const void* K, const void* V, const void*
     ACP_TRY(check_ws(ws, ws_bytes, y));
     char* w = (char*)ws;
     acp::BwdArgs b{};
-    b.Q = Q; b.K = K; b.V = V; b.dO = dO; b.bf16 = dt == ACP_BF16;
+    b.Q = Q; b.K = K; b.V = V; b.O = O; b.dO = dO; b.bf16 = dt == ACP_BF16;
     b.B = B; b.H = H; b.L = L; b.d = d;
     b.c = (const float*)(w + y.c);
     b.row_start = (const int*)(w + y.rs);
     b.col_end = (const int*)(w + y.ce);
     b.lse2 = (const float*)(w + y.lse2);
-    b.O32 = (const float*)(w + y.o32);
     b.dsum = (float*)(w + y.dsum);
     b.rowsum = (float*)(w + y.rowsum);
     b.colsum = (float*)(w + y.colsum);

@@ -37,7 +37,6 @@ struct FwdArgs {
     const int* row_start;
     const double* u;          // [B*H] logit bound U
     void* O;
-    float* O32;
     float* lse;
     float* lse2;
 };
@@ -46,6 +45,7 @@ struct BwdArgs {
     const void* Q;
     const void* K;
     const void* V;
+    const void* O;            // the forward's output
     const void* dO;
     bool bf16;
     int B, H, L, d;
@@ -53,8 +53,7 @@ struct BwdArgs {
     const int* row_start;
     const int* col_end;
     const float* lse2;
-    const float* O32;
-    float* dsum;
+    float* dsum;              // Delta (float32 path), then Delta' from the dQ pass
     float* rowsum;
     float* colsum;
     void* dQ;

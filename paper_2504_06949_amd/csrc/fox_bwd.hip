@@ -9,7 +9,8 @@
 //   dc_i = sum_j dS_ij - sum_j dS_ji,  dlog f_l = sum_{i >= l} dc_i.
 //
 // Four launches:
-//   dsum_kernel   Delta from dO and the float32 copy of O kept by the forward
+//   dsum_kernel   Delta = rowdot(dO, O) (float32 path; the bf16 dQ pass forms
+//                 Delta itself from the rows of O and dO it holds)
 //   dq kernel     per query block, loops over kept key blocks: dQ, then
 //                 Delta'_i = sum_j P_ij dP_ij (replacing Delta) and the row sums
 //                 of dS (bf16: fox_bwd_mfma.hip; fp32: below)
@@ -26,9 +27,9 @@ namespace acp {
 // ---------------------------------------------------------------------------
 // Delta_i = sum_d dO_id O_id: 16 lanes per row.
 // ---------------------------------------------------------------------------
-template <typename T, int D>
-__global__ __launch_bounds__(256) void dsum_kernel(const T* __restrict__ dO,
-                                                   const float* __restrict__ O32,
+template <int D>
+__global__ __launch_bounds__(256) void dsum_kernel(const float* __restrict__ dO,
+                                                   const float* __restrict__ O,
                                                    float* __restrict__ dsum, size_t rows) {
     constexpr int E = D / 16;
     const size_t gt = (size_t)blockIdx.x * 256 + threadIdx.x;
@@ -39,7 +40,7 @@ __global__ __launch_bounds__(256) void dsum_kernel(const T* __restrict__ dO,
 #pragma unroll
         for (int e = 0; e < E; ++e) {
             const size_t off = row * D + sub * E + e;
-            acc = __builtin_fmaf(to_f32(dO[off]), O32[off], acc);
+            acc = __builtin_fmaf(dO[off], O[off], acc);
         }
     }
     acc += __shfl_xor(acc, 8);
@@ -218,24 +219,17 @@ hipError_t launch_bwd(const BwdArgs& a, hipStream_t s) {
     const size_t rows = (size_t)BH * a.L;
     const unsigned dgrid = (unsigned)((rows * 16 + 255) / 256);
     hipError_t e;
-    trace_begin(ACP_K_DSUM, s);
-    if (a.bf16) {
+    if (!a.bf16) {
+        trace_begin(ACP_K_DSUM, s);
         if (a.d == 64)
-            hipLaunchKernelGGL((dsum_kernel<__bf16, 64>), dim3(dgrid), dim3(256), 0, s,
-                               (const __bf16*)a.dO, a.O32, a.dsum, rows);
+            hipLaunchKernelGGL(dsum_kernel<64>, dim3(dgrid), dim3(256), 0, s,
+                               (const float*)a.dO, (const float*)a.O, a.dsum, rows);
         else
-            hipLaunchKernelGGL((dsum_kernel<__bf16, 128>), dim3(dgrid), dim3(256), 0, s,
-                               (const __bf16*)a.dO, a.O32, a.dsum, rows);
-    } else {
-        if (a.d == 64)
-            hipLaunchKernelGGL((dsum_kernel<float, 64>), dim3(dgrid), dim3(256), 0, s,
-                               (const float*)a.dO, a.O32, a.dsum, rows);
-        else
-            hipLaunchKernelGGL((dsum_kernel<float, 128>), dim3(dgrid), dim3(256), 0, s,
-                               (const float*)a.dO, a.O32, a.dsum, rows);
+            hipLaunchKernelGGL(dsum_kernel<128>, dim3(dgrid), dim3(256), 0, s,
+                               (const float*)a.dO, (const float*)a.O, a.dsum, rows);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        trace_end(ACP_K_DSUM, s);
     }
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    trace_end(ACP_K_DSUM, s);
 
     trace_begin(ACP_K_DQ, s);
     if (a.bf16) {

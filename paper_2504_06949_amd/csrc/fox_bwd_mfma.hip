@@ -39,7 +39,7 @@ struct alignas(1024) DqSmem {
 template <int D>
 __global__ __launch_bounds__(kBwdThreads) void dq_bf16_kernel(
     const __bf16* __restrict__ Q, const __bf16* __restrict__ K, const __bf16* __restrict__ V,
-    const __bf16* __restrict__ dO, const float* __restrict__ cg,
+    const __bf16* __restrict__ O, const __bf16* __restrict__ dO, const float* __restrict__ cg,
     const int* __restrict__ row_start, const float* __restrict__ lse2,
     float* __restrict__ dsum, __bf16* __restrict__ dQ, float* __restrict__ rowsum,
     int L, int M, int nqb, int nblocks, float kscale, float qscale) {
@@ -76,7 +76,18 @@ __global__ __launch_bounds__(kBwdThreads) void dq_bf16_kernel(
                 dof[qt][ds] = *reinterpret_cast<const bf16x8*>(dO + row * D + 32 * ds + 8 * g);
             }
             aq[qt] = (cg[row] - cref) * kLog2e - lse2[row];
-            dl[qt] = dsum[row];
+            // Delta_i = rowdot(dO, O) over the lane's columns, then across the four
+            // lanes that hold row i
+            float dd = 0.f;
+#pragma unroll
+            for (int ds = 0; ds < NDS; ++ds) {
+                const bf16x8 o8 = *reinterpret_cast<const bf16x8*>(O + row * D + 32 * ds + 8 * g);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) dd = __builtin_fmaf((float)dof[qt][ds][e], (float)o8[e], dd);
+            }
+            dd += __shfl_xor(dd, 16);
+            dd += __shfl_xor(dd, 32);
+            dl[qt] = dd;
         }
     }
 
@@ -556,13 +567,13 @@ hipError_t launch_dq_bf16(const BwdArgs& a, hipStream_t s) {
     if (a.d == 64)
         hipLaunchKernelGGL(dq_bf16_kernel<64>, dim3(nblocks), dim3(kBwdThreads), 0, s,
                            (const __bf16*)a.Q, (const __bf16*)a.K, (const __bf16*)a.V,
-                           (const __bf16*)a.dO, a.c, a.row_start, a.lse2, a.dsum,
-                           (__bf16*)a.dQ, a.rowsum, a.L, M, nqb, nblocks, kscale, qscale);
+                           (const __bf16*)a.O, (const __bf16*)a.dO, a.c, a.row_start, a.lse2,
+                           a.dsum, (__bf16*)a.dQ, a.rowsum, a.L, M, nqb, nblocks, kscale, qscale);
     else
         hipLaunchKernelGGL(dq_bf16_kernel<128>, dim3(nblocks), dim3(kBwdThreads), 0, s,
                            (const __bf16*)a.Q, (const __bf16*)a.K, (const __bf16*)a.V,
-                           (const __bf16*)a.dO, a.c, a.row_start, a.lse2, a.dsum,
-                           (__bf16*)a.dQ, a.rowsum, a.L, M, nqb, nblocks, kscale, qscale);
+                           (const __bf16*)a.O, (const __bf16*)a.dO, a.c, a.row_start, a.lse2,
+                           a.dsum, (__bf16*)a.dQ, a.rowsum, a.L, M, nqb, nblocks, kscale, qscale);
     return hipGetLastError();
 }
 

@@ -61,9 +61,8 @@ template <int D, bool kFixed>
 __global__ __launch_bounds__(kFwdThreads) void fwd_bf16_kernel(
     const __bf16* __restrict__ Q, const __bf16* __restrict__ K, const __bf16* __restrict__ V,
     const float* __restrict__ cg, const int* __restrict__ row_start,
-    const double* __restrict__ bound_u, __bf16* __restrict__ O, float* __restrict__ O32,
-    float* __restrict__ lse, float* __restrict__ lse2, int L, int M, int nqb, int nblocks,
-    float kscale) {
+    const double* __restrict__ bound_u, __bf16* __restrict__ O, float* __restrict__ lse,
+    float* __restrict__ lse2, int L, int M, int nqb, int nblocks, float kscale) {
     constexpr int NDS = D / 32;                     // k-steps over the head dim
     constexpr int NDT = D / 16;                     // output tiles over the head dim
     __shared__ FwdSmem<D> sm;
@@ -333,7 +332,6 @@ __global__ __launch_bounds__(kFwdThreads) void fwd_bf16_kernel(
         for (int dt = 0; dt < NDT; ++dt) {
             const f32x4 o = acc[qt][dt] * inv;
             const size_t off = (head + query) * D + 16 * dt + 4 * g;
-            *reinterpret_cast<f32x4*>(O32 + off) = o;
             bf16x4 ob;
             ob[0] = (__bf16)o[0]; ob[1] = (__bf16)o[1]; ob[2] = (__bf16)o[2]; ob[3] = (__bf16)o[3];
             *reinterpret_cast<bf16x4*>(O + off) = ob;
@@ -357,7 +355,7 @@ template <int D>
 __global__ __launch_bounds__(64) void fwd_f32_kernel(
     const float* __restrict__ Q, const float* __restrict__ K, const float* __restrict__ V,
     const float* __restrict__ cg, const int* __restrict__ row_start,
-    float* __restrict__ O, float* __restrict__ O32, float* __restrict__ lse,
+    float* __restrict__ O, float* __restrict__ lse,
     float* __restrict__ lse2, int L, int M, float kscale) {
     __shared__ float ks[64 * D];
     __shared__ float vs[64 * D];
@@ -403,7 +401,6 @@ __global__ __launch_bounds__(64) void fwd_f32_kernel(
     for (int k = 0; k < D; ++k) {
         const float o = acc[k] * inv;
         O[(head + query) * D + k] = o;
-        O32[(head + query) * D + k] = o;
     }
     const float l2 = mrun + fast_log2(lrun) + (cg[head + query] - cref) * kLog2e;
     lse2[head + query] = l2;
@@ -418,11 +415,11 @@ static void launch_fwd_bf16(const FwdArgs& a, int M, float kscale, hipStream_t s
     const int nblocks = BH * nqb;
     hipLaunchKernelGGL((fwd_bf16_kernel<D, true>), dim3(nblocks), dim3(kFwdThreads), 0, s,
                        (const __bf16*)a.Q, (const __bf16*)a.K, (const __bf16*)a.V, a.c,
-                       a.row_start, a.u, (__bf16*)a.O, a.O32, a.lse, a.lse2, a.L, M, nqb,
+                       a.row_start, a.u, (__bf16*)a.O, a.lse, a.lse2, a.L, M, nqb,
                        nblocks, kscale);
     hipLaunchKernelGGL((fwd_bf16_kernel<D, false>), dim3(nblocks), dim3(kFwdThreads), 0, s,
                        (const __bf16*)a.Q, (const __bf16*)a.K, (const __bf16*)a.V, a.c,
-                       a.row_start, a.u, (__bf16*)a.O, a.O32, a.lse, a.lse2, a.L, M, nqb,
+                       a.row_start, a.u, (__bf16*)a.O, a.lse, a.lse2, a.L, M, nqb,
                        nblocks, kscale);
 }
 
@@ -437,11 +434,11 @@ hipError_t launch_fwd(const FwdArgs& a, hipStream_t s) {
         if (a.d == 64)
             hipLaunchKernelGGL(fwd_f32_kernel<64>, dim3(BH * M), dim3(64), 0, s,
                                (const float*)a.Q, (const float*)a.K, (const float*)a.V, a.c,
-                               a.row_start, (float*)a.O, a.O32, a.lse, a.lse2, a.L, M, kscale);
+                               a.row_start, (float*)a.O, a.lse, a.lse2, a.L, M, kscale);
         else
             hipLaunchKernelGGL(fwd_f32_kernel<128>, dim3(BH * M), dim3(64), 0, s,
                                (const float*)a.Q, (const float*)a.K, (const float*)a.V, a.c,
-                               a.row_start, (float*)a.O, a.O32, a.lse, a.lse2, a.L, M, kscale);
+                               a.row_start, (float*)a.O, a.lse, a.lse2, a.L, M, kscale);
     }
     const hipError_t e = hipGetLastError();
     trace_end(ACP_K_FWD, s);

@@ -42,9 +42,10 @@ def test_workspace_size_and_layout():
     assert offs == sorted(offs) and len(set(offs)) == len(offs)
     BHL = 8 * 12 * 4096
     assert lay.bound_u - lay.c >= 4 * BHL
-    # the float32 copy of O dominates: at least B*H*L*d*4 bytes
-    assert n >= BHL * 64 * 4
-    assert acp.acp_workspace_size(8, 12, 4096, 128, acp.ACP_BF16) > n
+    # five float32 rows per position (c, L_i, Delta', row and column sums of dS)
+    # dominate, and nothing scales with the head dim
+    assert n >= 5 * 4 * BHL
+    assert acp.acp_workspace_size(8, 12, 4096, 128, acp.ACP_BF16) == n
 
 
 @pytest.mark.parametrize("args,status", [
@@ -88,10 +89,13 @@ def test_forward_rejects_before_launch(kw, status):
 
 
 def test_backward_and_boundary_reject_before_launch():
-    st = acp.fox_attn_bwd(16, 16, 16, 0, acp.ACP_BF16, 1, 1, 64, 64, 16, 16, 16, 16, 16,
+    st = acp.fox_attn_bwd(16, 16, 16, 16, 0, acp.ACP_BF16, 1, 1, 64, 64, 16, 16, 16, 16, 16,
                           1 << 40, None)
     assert st == acp.ACP_EINVAL and "dO" in acp.acp_last_error()
-    st = acp.fox_attn_bwd(16, 16, 16, 16, acp.ACP_BF16, 1, 1, 64, 64, 16, 16, 16, 16, 16, 8,
+    st = acp.fox_attn_bwd(16, 16, 16, 0, 16, acp.ACP_BF16, 1, 1, 64, 64, 16, 16, 16, 16, 16,
+                          1 << 40, None)
+    assert st == acp.ACP_EINVAL and "O" in acp.acp_last_error()
+    st = acp.fox_attn_bwd(16, 16, 16, 16, 16, acp.ACP_BF16, 1, 1, 64, 64, 16, 16, 16, 16, 16, 8,
                           None)
     assert st == acp.ACP_EWORKSPACE
     st = acp.acp_boundary(16, 16, 16, acp.ACP_F32, 1, 1, 64, 64, 0.5, 16, 16, 16, 16, 16, 0, 16,

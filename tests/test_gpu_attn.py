@@ -30,7 +30,7 @@ def _run_gpu(x, eps, grads=True):
     o, lse, ws = acp.forward(g["q"], g["k"], g["v"], g["log_f"], eps)
     out = {"o": o, "lse": lse, "ws": ws}
     if grads:
-        dq, dk, dv, dlf = acp.backward(g["q"], g["k"], g["v"], g["do"], ws)
+        dq, dk, dv, dlf = acp.backward(g["q"], g["k"], g["v"], o, g["do"], ws)
         out.update({"dq": dq, "dk": dk, "dv": dv, "dlog_f": dlf})
     torch.cuda.synchronize()
     return out
