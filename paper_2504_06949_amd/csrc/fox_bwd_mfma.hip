@@ -132,7 +132,6 @@ __global__ __launch_bounds__(kBwdThreads) void dq_bf16_kernel(
         dinit[qt] = f32x4{b, b, b, b};
     }
     float sds[2] = {0.f, 0.f};   // sum_j dS_ij (lane partial)
-    float psum[2] = {0.f, 0.f};  // sum_j P_ij (lane partial)
 
     // Each key tile is taken in two halves of 32 keys, each in three phases: A
     // forms S^T and dP^T (MFMA; key rows from LDS), B the softmax terms (VALU),
@@ -209,7 +208,6 @@ __global__ __launch_bounds__(kBwdThreads) void dq_bf16_kernel(
                 if (kMask && 32 * h + j > qk) p = 0.f;
                 const float dsv = p * x.dp[t][qt][u];
                 sds[qt] += dsv;
-                psum[qt] += p;
                 dsf[qt][j] = (__bf16)dsv;
             }
         }
@@ -280,17 +278,17 @@ __global__ __launch_bounds__(kBwdThreads) void dq_bf16_kernel(
         // Delta'_i = sum_j P_ij dP_ij from the float32 P and dP of this pass
         // (= sum_j dS_ij + Delta_i sum_j P_ij): it is what rowdot(dO, O) equals for
         // the exact O, free of the rounding of P to bfloat16 in the forward's PV
-        // product.  The dK/dV pass and both sums of dS use it; rowsum(dS) is then
-        // Delta' (1 - sum_j P_ij).
-        float a = sds[qt], z = psum[qt];
+        // product.  The dK/dV pass uses it for dS.  sum_j P_ij is 1 here up to
+        // float32 rounding, since L_i is the log of the forward's float32 weight
+        // sum; the row sums of dS, Delta'_i (1 - sum_j P_ij), are therefore zero
+        // to that rounding, as they are exactly for any softmax (its value does not
+        // change when a whole row of logits is shifted).
+        float a = sds[qt];
         a += __shfl_xor(a, 16);
         a += __shfl_xor(a, 32);
-        z += __shfl_xor(z, 16);
-        z += __shfl_xor(z, 32);
         if (g == 0) {
-            const float dp2 = __builtin_fmaf(dl[qt], z, a);
-            dsum[head + query] = dp2;
-            rowsum[head + query] = dp2 - dp2 * z;
+            dsum[head + query] = a + dl[qt];
+            rowsum[head + query] = 0.f;
         }
     }
 }
