@@ -213,6 +213,13 @@ __global__ __launch_bounds__(kBwdThreads) void dq_bf16_kernel(
         }
         return DsH{{dsf[0], dsf[1]}};
     };
+    auto phase_c_part = [&](const OpC& rc, const DsH& y, int part) __attribute__((always_inline)) {
+#pragma unroll
+        for (int dt = part * NDT / 2; dt < (part + 1) * NDT / 2; ++dt) {
+            acc[0][dt] = mfma16(rc.ak[dt], y.d[0], acc[0][dt]);
+            acc[1][dt] = mfma16(rc.ak[dt], y.d[1], acc[1][dt]);
+        }
+    };
     // dQ^T += K^T dS^T over the half's 32 keys
     auto phase_c = [&](const OpC& rc, const DsH& y) __attribute__((always_inline)) {
 #pragma unroll
@@ -252,9 +259,15 @@ __global__ __launch_bounds__(kBwdThreads) void dq_bf16_kernel(
         // tile n + 1 has landed and every wave's reads of tile n are complete
         wait_vmcnt0_lgkmcnt0();
         __syncthreads();
-        if (n + 1 < n_hi) cnext = issue(n + 2, buf);
+        // the next tile's loads, spread over this tile's last MFMAs (see the dK/dV
+        // pass)
+        const bool more = n + 1 < n_hi;
+        if (more && tid < 16) cnext = *reinterpret_cast<const float4*>(cg + head + 64 * (n + 2) + 4 * tid);
         if (n < n_hi) ra = load_a(buf ^ 1, 0);
-        if (act) phase_c(rc, y);
+        if (act) phase_c_part(rc, y, 0);
+        if (more) dma.issue(sm.k[buf], K + (head + (size_t)64 * (n + 2)) * D, w);
+        if (act) phase_c_part(rc, y, 1);
+        if (more) dma.issue(sm.v[buf], V + (head + (size_t)64 * (n + 2)) * D, w);
         buf ^= 1;
     };
     // The diagonal tiles (m0 for waves 0-1, m0 + 1 = n_hi for waves 2-3) are the
@@ -335,6 +348,7 @@ __global__ __launch_bounds__(kBwdThreads) void dkdv_bf16_kernel(
     const int m_lo = n0;
     const int m_hi = col_end[(size_t)bh * M + min(n0 + 1, M - 1)];
     const int w_hi = wave_on ? col_end[(size_t)bh * M + nw] : -1;
+    const float kinv = 1.0f / kscale;
     const float cref = cg[head + k0];
 
     bf16x8 kf[2][NDS], vf[2][NDS];
@@ -368,7 +382,7 @@ __global__ __launch_bounds__(kBwdThreads) void dkdv_bf16_kernel(
     };
     auto put_rows = [&](float3 r, int buf) __attribute__((always_inline)) {
         if (tid < 64) {
-            sm.la[buf][tid] = ((r.x - cref) * kLog2e - r.y) / kscale;
+            sm.la[buf][tid] = ((r.x - cref) * kLog2e - r.y) * kinv;
             sm.dl[buf][tid] = -r.z;
         }
     };
@@ -476,6 +490,15 @@ __global__ __launch_bounds__(kBwdThreads) void dkdv_bf16_kernel(
         }
         return y;
     };
+    auto phase_c_part = [&](const OpC& rc, const PdS& y, int part) __attribute__((always_inline)) {
+#pragma unroll
+        for (int dt = part * NDT / 2; dt < (part + 1) * NDT / 2; ++dt)
+#pragma unroll
+            for (int kt = 0; kt < 2; ++kt) {
+                dv[kt][dt] = mfma16(rc.ao[dt], y.pb[kt], dv[kt][dt]);
+                dk[kt][dt] = mfma16(rc.aq[dt], y.db[kt], dk[kt][dt]);
+            }
+    };
     // dV^T += dO^T P,  dK^T += Q^T dS over the half's 32 queries
     auto phase_c = [&](const OpC& rc, const PdS& y) __attribute__((always_inline)) {
 #pragma unroll
@@ -523,9 +546,19 @@ __global__ __launch_bounds__(kBwdThreads) void dkdv_bf16_kernel(
         // tile m + 1 has landed and every wave's reads of tile m are complete
         wait_vmcnt0_lgkmcnt0();
         __syncthreads();
-        if (m + 1 < m_hi) rnext = issue(m + 2, buf);
+        // The next tile's loads are spread over this tile's last MFMAs: issued in
+        // one clump right after the barrier, the four waves' DMA instructions
+        // queue for the CU's address unit and stall the waves' issue.
+        const bool more = m + 1 < m_hi;
+        if (more && tid < 64) {
+            const size_t row = head + 64 * (m + 2) + tid;
+            rnext = make_float3(cg[row], lse2[row], dsum[row]);
+        }
         if (m < m_hi) ra = load_a(buf ^ 1, 0);
-        if (act) phase_c(rc, y);
+        if (act) phase_c_part(rc, y, 0);
+        if (more) dma.issue(sm.q[buf], Q + (head + (size_t)64 * (m + 2)) * D, w);
+        if (act) phase_c_part(rc, y, 1);
+        if (more) dma.issue(sm.o[buf], dO + (head + (size_t)64 * (m + 2)) * D, w);
         buf ^= 1;
     };
     const int m_diag = min(m_lo + 1, m_hi);

@@ -265,10 +265,10 @@ __global__ __launch_bounds__(kFwdThreads) void fwd_bf16_kernel(
         }
         return pt;
     };
-    // O^T += V^T P^T
-    auto phase_c = [&](const OpC& rc, const PTile& pt) __attribute__((always_inline)) {
+    // O^T += V^T P^T, head-dim tiles [part NDT/2, (part + 1) NDT/2)
+    auto phase_c_part = [&](const OpC& rc, const PTile& pt, int part) __attribute__((always_inline)) {
 #pragma unroll
-        for (int dt = 0; dt < NDT; ++dt)
+        for (int dt = part * NDT / 2; dt < (part + 1) * NDT / 2; ++dt)
 #pragma unroll
             for (int ks = 0; ks < 2; ++ks) {
                 acc[0][dt] = mfma16(rc.v[dt][ks], pt.p[0][ks], acc[0][dt]);
@@ -300,9 +300,16 @@ __global__ __launch_bounds__(kFwdThreads) void fwd_bf16_kernel(
         // tile n + 1 has landed and every wave's reads of tile n are complete
         wait_vmcnt0_lgkmcnt0();
         __syncthreads();
-        if (n + 1 < n_hi) cnext = issue(n + 2, buf);
+        // The next tile's loads are spread over this tile's last MFMAs: issued in
+        // one clump right after the barrier, the four waves' DMA instructions
+        // queue for the CU's address unit and stall the waves' issue.
+        const bool more = n + 1 < n_hi;
+        if (more && tid < 16) cnext = *reinterpret_cast<const float4*>(cg + head + 64 * (n + 2) + 4 * tid);
         if (n < n_hi) ra = load_a(buf ^ 1);
-        if (act) phase_c(rc, pt);
+        if (act) phase_c_part(rc, pt, 0);
+        if (more) dma.issue(sm.k[buf], K + (head + (size_t)64 * (n + 2)) * D, w);
+        if (act) phase_c_part(rc, pt, 1);
+        if (more) dma.issue(sm.v[buf], V + (head + (size_t)64 * (n + 2)) * D, w);
         buf ^= 1;
     };
     // The diagonal tiles (m0 for waves 0-1, m0 + 1 for waves 2-3) are the last
