@@ -56,6 +56,16 @@ def measured_traffic(kernel: str, workload: str):
     return None
 
 
+def _hbm_gbps(w, pk: dict) -> dict:
+    """Achieved HBM rates of the memory-bound kernels from their compulsory bytes:
+    row norms read Q and K; the plan reads log f and writes c (plus L/64-sized
+    tables); the dlog f scan reads the row and column sums and writes dlog f."""
+    bhl = w.B * w.H * w.L
+    s = 2 if w.dtype == "bf16" else 4
+    nbytes = {"rownorm": 2 * bhl * w.d * s, "plan": 8 * bhl, "dlogf": 12 * bhl}
+    return {k: round(v / (pk[k] * 1e-3) / 1e9, 1) for k, v in nbytes.items() if pk.get(k)}
+
+
 def run_workload(name: str, steps: int, warmup: int, eps_override=None, unpruned=True):
     import torch
     from paper_2504_06949_amd import acp, workloads
@@ -200,6 +210,7 @@ def main():
         "speedup_vs_unpruned": None if args.skip_unpruned else round(res["ms_dense"] / res["ms"], 3),
         "per_kernel_ms": {k: round(v, 4) for k, v in pk.items()},
         "boundary_share": round((pk["rownorm"] + pk["plan"]) / res["ms"], 4),
+        "hbm_gbps": _hbm_gbps(w, pk),
         "roofline": {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 2),
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
