@@ -66,11 +66,13 @@ def _hbm_gbps(w, pk: dict) -> dict:
     return {k: round(v / (pk[k] * 1e-3) / 1e9, 1) for k, v in nbytes.items() if pk.get(k)}
 
 
-def run_workload(name: str, steps: int, warmup: int, eps_override=None, unpruned=True):
+def run_workload(name, steps: int, warmup: int, eps_override=None, unpruned=True):
+    """Time fwd+bwd steps of a named workload (or a Workload); QK-norm workloads
+    take their bound from the norm scales (fox_attn_fwd_qknorm)."""
     import torch
     from paper_2504_06949_amd import acp, workloads
 
-    w = workloads.WORKLOADS[name]
+    w = workloads.WORKLOADS[name] if isinstance(name, str) else name
     x = workloads.generate(w)
     dev = torch.device("cuda:0")
     g = {k: (v.to(dev) if torch.is_tensor(v) else v) for k, v in x.items()}
@@ -82,7 +84,11 @@ def run_workload(name: str, steps: int, warmup: int, eps_override=None, unpruned
              torch.empty(g["log_f"].shape, dtype=torch.float32, device=dev))
 
     def step(e):
-        acp.forward(g["q"], g["k"], g["v"], g["log_f"], e, ws=ws, out=(o, lse))
+        if w.qk_norm:
+            acp.forward_qknorm(g["q"], g["k"], g["v"], g["log_f"], g["gamma_q"], g["gamma_k"], e,
+                               ws=ws, out=(o, lse))
+        else:
+            acp.forward(g["q"], g["k"], g["v"], g["log_f"], e, ws=ws, out=(o, lse))
         acp.backward(g["q"], g["k"], g["v"], o, g["do"], ws, out=grads)
 
     def timed(e):
@@ -226,6 +232,19 @@ def main():
                            "executed_tflops": round(f["executed"] / (r["ms"] * 1e-3) / 1e12, 1),
                            "pruned_fraction": round(1 - r["kept"] / r["causal"], 4),
                            "per_kernel_ms": {k: round(v, 4) for k, v in r["per_kernel_ms"].items()}}
+        # the 125m layer again with QK-normed queries and keys: the bound comes from
+        # the norm scales and stage 1 makes no pass over Q and K
+        from paper_2504_06949_amd import workloads as wl
+        w125 = wl.WORKLOADS["125m"]
+        wq = wl.custom("125m_qknorm", w125.B, w125.H, w125.L, w125.d, "bf16", w125.seed, qk_norm=True)
+        r = run_workload(wq, max(3, args.steps // 4), 2)
+        f = _flops(r["w"], r["kept"])
+        rpk = r["per_kernel_ms"]
+        extra["125m_qknorm"] = {"ms": round(r["ms"], 3), "ms_unpruned": round(r["ms_dense"], 3),
+                                "effective_tflops": round(f["effective"] / (r["ms"] * 1e-3) / 1e12, 1),
+                                "pruned_fraction": round(1 - r["kept"] / r["causal"], 4),
+                                "boundary_share": round((rpk["rownorm"] + rpk["plan"]) / r["ms"], 4),
+                                "per_kernel_ms": {k: round(v, 4) for k, v in rpk.items()}}
         out["other_workloads"] = extra
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(res)

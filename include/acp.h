@@ -36,7 +36,8 @@
  *       bit 1  some log f is NaN or infinite
  *       bit 2  the partial sums of log f span more than 53 bits, so c may differ in
  *              its last bit from the sequential float64 definition
- *       bit 3  rho_q^2 or rho_k^2 is not finite (Q or K holds NaN/Inf or overflows)
+ *       bit 3  rho_q^2 or rho_k^2 is not finite (Q or K holds NaN/Inf or overflows),
+ *              or, in the QK-norm variants, a scale bound is negative or not finite
  *     With bit 0, 1 or 3 set the boundary and the attention outputs are unspecified.
  *
  * Numerics of the pruning decision (identical on every device and on the host):
@@ -105,6 +106,23 @@ acp_status acp_boundary(const void* Q, const void* K, const float* log_f, acp_dt
                         int32_t* row_start, int32_t* col_end, int64_t* kept,
                         int32_t* flags, void* ws, size_t ws_bytes, void* stream);
 
+/* Stage 1 with the logit bound taken from QK-norm scales instead of the row
+ * norms (App. E; Sec. 3 notes that U may come from the normalisation layers).
+ * When q and k are RMS-normalised (mean square 1 over the d features) and then
+ * scaled elementwise by weights of magnitude at most gamma_q[h], gamma_k[h],
+ * |q.k| / sqrt(d) <= U = gamma_q[h] gamma_k[h] sqrt(d), so the pruning stays safe
+ * without reading Q and K.  The caller vouches for that premise.
+ *   in : log_f [B,H,L] float; gamma_q, gamma_k [H] float (>= 0, finite; shared over
+ *        the batch); dt and d fix the workspace shape only.
+ *   out: as acp_boundary; U = (gamma_q gamma_k) sqrt(d) in float64.  Flag bit 3
+ *        reports a negative or non-finite gamma.
+ *   ws : scratch of acp_workspace_size() bytes (nothing of it is read). */
+acp_status acp_boundary_qknorm(const float* log_f, const float* gamma_q, const float* gamma_k,
+                               acp_dtype dt, int B, int H, int L, int d, double eps,
+                               float* c, double* bound_u, double* delta,
+                               int32_t* row_start, int32_t* col_end, int64_t* kept,
+                               int32_t* flags, void* ws, size_t ws_bytes, void* stream);
+
 /* Forgetting Attention forward with ACP (Sec. 2 eq. 1-2 with the block-level
  * mask of Sec. 3): runs stage 1 into the workspace, then attention over the kept
  * blocks only (pruned blocks' K and V are never read).
@@ -116,6 +134,14 @@ acp_status acp_boundary(const void* Q, const void* K, const float* log_f, acp_dt
 acp_status fox_attn_fwd(const void* Q, const void* K, const void* V, const float* log_f,
                         acp_dtype dt, int B, int H, int L, int d, double eps,
                         void* O, float* lse, void* ws, size_t ws_bytes, void* stream);
+
+/* fox_attn_fwd with stage 1 as in acp_boundary_qknorm: the bound comes from the
+ * QK-norm scales gamma_q, gamma_k [H] and Q, K are read only by the attention
+ * pass.  fox_attn_bwd takes the workspace it leaves like that of fox_attn_fwd. */
+acp_status fox_attn_fwd_qknorm(const void* Q, const void* K, const void* V, const float* log_f,
+                               const float* gamma_q, const float* gamma_k, acp_dtype dt,
+                               int B, int H, int L, int d, double eps, void* O, float* lse,
+                               void* ws, size_t ws_bytes, void* stream);
 
 /* Backward of fox_attn_fwd (the paper states only that it mirrors the forward,
  * Sec. 2; the gradients follow from eq. 2 by the chain rule, with the pruning

@@ -43,7 +43,7 @@ BLOCK = 64
 
 __all__ = [
     "BLOCK", "cumsum_log_gates", "cumsum_exact_fraction", "cumsum_span_bits",
-    "row_norm_sq_max", "logit_bound", "log_len_over_eps", "threshold",
+    "row_norm_sq_max", "logit_bound", "logit_bound_qknorm", "log_len_over_eps", "threshold",
     "entry_keep", "block_keep_bruteforce", "block_keep_topright", "boundary_from_block_keep",
     "boundary_alg1", "col_end_from_row_start", "kept_tiles", "causal_tiles",
     "block_mask", "entry_mask", "causal_mask", "forward", "backward", "pruned_mass",
@@ -134,6 +134,17 @@ def row_norm_sq_max(x) -> float:
 def logit_bound(rho2_q: float, rho2_k: float, d: int) -> float:
     """U = rho_q rho_k / sqrt(d), evaluated as sqrt(rho_q^2 rho_k^2 / d) (Sec. 3)."""
     return math.sqrt((float(rho2_q) * float(rho2_k)) / float(d))
+
+
+def logit_bound_qknorm(gamma_q: float, gamma_k: float, d: int) -> float:
+    """U from QK-norm scales (App. E; Sec. 3 allows any valid bound on the logits):
+    an RMS-normalised row has norm sqrt(d), an elementwise scale of magnitude at
+    most gamma multiplies that by at most gamma, so |q.k| / sqrt(d) is at most
+    gamma_q sqrt(d) gamma_k sqrt(d) / sqrt(d) = gamma_q gamma_k sqrt(d).  The scales
+    are float32; their product is exact in float64; one rounding per operation."""
+    gq = float(np.float32(gamma_q))
+    gk = float(np.float32(gamma_k))
+    return (gq * gk) * math.sqrt(d)
 
 
 def log_len_over_eps(L: int, eps: float) -> float:
@@ -324,13 +335,18 @@ def pruned_mass(q, k, c, kept_mask):
 # One head end to end
 # --------------------------------------------------------------------------
 
-def plan_head(q, k, log_f, eps: float, block: int = BLOCK, method: str = "bruteforce"):
-    """Stage 1 for one (batch, head): c, U, delta and the boundary (Sec. 3)."""
+def plan_head(q, k, log_f, eps: float, block: int = BLOCK, method: str = "bruteforce",
+              U: float | None = None):
+    """Stage 1 for one (batch, head): c, U, delta and the boundary (Sec. 3).  A given
+    U (e.g. logit_bound_qknorm) replaces the bound from the row norms."""
     L, d = np.asarray(q).shape
     c = cumsum_log_gates(log_f)
-    rq = row_norm_sq_max(q)
-    rk = row_norm_sq_max(k)
-    U = logit_bound(rq, rk, d)
+    if U is None:
+        rq = row_norm_sq_max(q)
+        rk = row_norm_sq_max(k)
+        U = logit_bound(rq, rk, d)
+    else:
+        rq = rk = float("nan")
     delta = threshold(U, L, eps)
     if method == "bruteforce":
         kb = block_keep_bruteforce(c, delta, block)
@@ -347,9 +363,11 @@ def plan_head(q, k, log_f, eps: float, block: int = BLOCK, method: str = "brutef
             "row_start": row_start, "col_end": col_end, "kept": kept_tiles(row_start)}
 
 
-def run_head(q, k, v, log_f, eps: float, do=None, block: int = BLOCK, method: str = "topright"):
-    """Plan, pruned forward and (if do is given) backward for one head."""
-    plan = plan_head(q, k, log_f, eps, block, method)
+def run_head(q, k, v, log_f, eps: float, do=None, block: int = BLOCK, method: str = "topright",
+             U: float | None = None):
+    """Plan, pruned forward and (if do is given) backward for one head (U: as in
+    plan_head)."""
+    plan = plan_head(q, k, log_f, eps, block, method, U)
     L = np.asarray(q).shape[0]
     mask = block_mask(plan["row_start"], L, block)
     o, lse = forward(q, k, v, plan["c"], mask)

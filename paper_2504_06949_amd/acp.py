@@ -53,7 +53,11 @@ _SIGS = {
     "acp_workspace_size": [_i, _i, _i, _i, _i, ctypes.POINTER(_sz)],
     "acp_plan_offsets": [_i, _i, _i, _i, _i, ctypes.POINTER(PlanLayout)],
     "acp_boundary": [_p, _p, _p, _i, _i, _i, _i, _i, _d, _p, _p, _p, _p, _p, _p, _p, _p, _sz, _p],
+    "acp_boundary_qknorm": [_p, _p, _p, _i, _i, _i, _i, _i, _d, _p, _p, _p, _p, _p, _p, _p,
+                            _p, _sz, _p],
     "fox_attn_fwd": [_p, _p, _p, _p, _i, _i, _i, _i, _i, _d, _p, _p, _p, _sz, _p],
+    "fox_attn_fwd_qknorm": [_p, _p, _p, _p, _p, _p, _i, _i, _i, _i, _i, _d, _p, _p, _p, _sz,
+                            _p],
     "fox_attn_bwd": [_p, _p, _p, _p, _p, _i, _i, _i, _i, _i, _p, _p, _p, _p, _p, _sz, _p],
     "acp_timing_enable": [_i],
     "acp_timing_reset": [],
@@ -119,8 +123,21 @@ def acp_boundary(Q, K, log_f, dt, B, H, L, d, eps, c, bound_u, delta, row_start,
                               col_end, kept, flags, ws, ws_bytes, stream)
 
 
+def acp_boundary_qknorm(log_f, gamma_q, gamma_k, dt, B, H, L, d, eps, c, bound_u, delta,
+                        row_start, col_end, kept, flags, ws, ws_bytes, stream) -> int:
+    return lib().acp_boundary_qknorm(log_f, gamma_q, gamma_k, dt, B, H, L, d, eps, c, bound_u,
+                                     delta, row_start, col_end, kept, flags, ws, ws_bytes,
+                                     stream)
+
+
 def fox_attn_fwd(Q, K, V, log_f, dt, B, H, L, d, eps, O, lse, ws, ws_bytes, stream) -> int:
     return lib().fox_attn_fwd(Q, K, V, log_f, dt, B, H, L, d, eps, O, lse, ws, ws_bytes, stream)
+
+
+def fox_attn_fwd_qknorm(Q, K, V, log_f, gamma_q, gamma_k, dt, B, H, L, d, eps, O, lse, ws,
+                        ws_bytes, stream) -> int:
+    return lib().fox_attn_fwd_qknorm(Q, K, V, log_f, gamma_q, gamma_k, dt, B, H, L, d, eps, O,
+                                     lse, ws, ws_bytes, stream)
 
 
 def fox_attn_bwd(Q, K, V, O, dO, dt, B, H, L, d, dQ, dK, dV, dlog_f, ws, ws_bytes,
@@ -179,16 +196,9 @@ def workspace(q: torch.Tensor) -> torch.Tensor:
     return torch.empty(n, dtype=torch.uint8, device=q.device)
 
 
-def boundary(q, k, log_f, eps: float, ws: torch.Tensor | None = None) -> dict:
-    """Stage 1 of ACP; returns c, bound_u, delta, row_start, col_end, kept, flags."""
-    dev = _dev(q, k, log_f)
-    B, H, L, d = _shape(q)
-    if k.shape != q.shape or k.dtype != q.dtype or tuple(log_f.shape) != (B, H, L) \
-            or log_f.dtype != torch.float32:
-        raise ValueError("shape/dtype mismatch")
-    ws = workspace(q) if ws is None else ws
+def _plan_outputs(B, H, L, dev) -> dict:
     M = L // 64
-    out = {
+    return {
         "c": torch.empty((B, H, L), dtype=torch.float32, device=dev),
         "bound_u": torch.empty((B, H), dtype=torch.float64, device=dev),
         "delta": torch.empty((B, H), dtype=torch.float64, device=dev),
@@ -197,12 +207,72 @@ def boundary(q, k, log_f, eps: float, ws: torch.Tensor | None = None) -> dict:
         "kept": torch.empty((B, H), dtype=torch.int64, device=dev),
         "flags": torch.empty((B, H), dtype=torch.int32, device=dev),
     }
+
+
+def boundary(q, k, log_f, eps: float, ws: torch.Tensor | None = None) -> dict:
+    """Stage 1 of ACP; returns c, bound_u, delta, row_start, col_end, kept, flags."""
+    dev = _dev(q, k, log_f)
+    B, H, L, d = _shape(q)
+    if k.shape != q.shape or k.dtype != q.dtype or tuple(log_f.shape) != (B, H, L) \
+            or log_f.dtype != torch.float32:
+        raise ValueError("shape/dtype mismatch")
+    ws = workspace(q) if ws is None else ws
+    out = _plan_outputs(B, H, L, dev)
     _check(acp_boundary(q.data_ptr(), k.data_ptr(), log_f.data_ptr(), _dt(q), B, H, L, d, eps,
                         out["c"].data_ptr(), out["bound_u"].data_ptr(), out["delta"].data_ptr(),
                         out["row_start"].data_ptr(), out["col_end"].data_ptr(),
                         out["kept"].data_ptr(), out["flags"].data_ptr(), ws.data_ptr(),
                         ws.numel(), _stream(dev)))
     return out
+
+
+def _check_gammas(gamma_q, gamma_k, H: int):
+    for name, t in (("gamma_q", gamma_q), ("gamma_k", gamma_k)):
+        if tuple(t.shape) != (H,) or t.dtype != torch.float32:
+            raise ValueError(name + " must be float32 [H]")
+
+
+def boundary_qknorm(log_f, gamma_q, gamma_k, d: int, eps: float, dtype=torch.bfloat16,
+                    ws: torch.Tensor | None = None) -> dict:
+    """Stage 1 with U = gamma_q gamma_k sqrt(d) from QK-norm scales (no pass over Q, K)."""
+    dev = _dev(log_f, gamma_q, gamma_k)
+    if log_f.dim() != 3 or log_f.dtype != torch.float32:
+        raise ValueError("log_f must be float32 [B, H, L]")
+    B, H, L = (int(s) for s in log_f.shape)
+    _check_gammas(gamma_q, gamma_k, H)
+    dt = ACP_F32 if dtype == torch.float32 else ACP_BF16
+    if ws is None:
+        ws = torch.empty(acp_workspace_size(B, H, L, d, dt), dtype=torch.uint8, device=dev)
+    out = _plan_outputs(B, H, L, dev)
+    _check(acp_boundary_qknorm(log_f.data_ptr(), gamma_q.data_ptr(), gamma_k.data_ptr(), dt, B, H,
+                               L, d, eps, out["c"].data_ptr(), out["bound_u"].data_ptr(),
+                               out["delta"].data_ptr(), out["row_start"].data_ptr(),
+                               out["col_end"].data_ptr(), out["kept"].data_ptr(),
+                               out["flags"].data_ptr(), ws.data_ptr(), ws.numel(), _stream(dev)))
+    return out
+
+
+def forward_qknorm(q, k, v, log_f, gamma_q, gamma_k, eps: float,
+                   ws: torch.Tensor | None = None, out=None):
+    """forward() with stage 1 bounded by QK-norm scales; returns (O, lse, ws)."""
+    dev = _dev(q, k, v, log_f, gamma_q, gamma_k)
+    B, H, L, d = _shape(q)
+    if k.shape != q.shape or v.shape != q.shape or k.dtype != q.dtype or v.dtype != q.dtype:
+        raise ValueError("Q, K, V must share shape and dtype")
+    if tuple(log_f.shape) != (B, H, L) or log_f.dtype != torch.float32:
+        raise ValueError("log_f must be float32 [B, H, L]")
+    _check_gammas(gamma_q, gamma_k, H)
+    ws = workspace(q) if ws is None else ws
+    if out is None:
+        o = torch.empty_like(q)
+        lse = torch.empty((B, H, L), dtype=torch.float32, device=dev)
+    else:
+        o, lse = out
+    _check(fox_attn_fwd_qknorm(q.data_ptr(), k.data_ptr(), v.data_ptr(), log_f.data_ptr(),
+                               gamma_q.data_ptr(), gamma_k.data_ptr(), _dt(q), B, H, L, d, eps,
+                               o.data_ptr(), lse.data_ptr(), ws.data_ptr(), ws.numel(),
+                               _stream(dev)))
+    return o, lse, ws
 
 
 def forward(q, k, v, log_f, eps: float, ws: torch.Tensor | None = None, out=None):

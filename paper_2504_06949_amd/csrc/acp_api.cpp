@@ -256,9 +256,44 @@ acp_status acp_boundary(const void* Q, const void* K, const float* log_f, acp_dt
     return hip_status(acp::launch_plan(a, (hipStream_t)stream), "acp_boundary launch");
 }
 
-acp_status fox_attn_fwd(const void* Q, const void* K, const void* V, const float* log_f,
-                        acp_dtype dt, int B, int H, int L, int d, double eps, void* O,
-                        float* lse, void* ws, size_t ws_bytes, void* stream) {
+acp_status acp_boundary_qknorm(const float* log_f, const float* gamma_q, const float* gamma_k,
+                               acp_dtype dt, int B, int H, int L, int d, double eps, float* c,
+                               double* bound_u, double* delta, int32_t* row_start,
+                               int32_t* col_end, int64_t* kept, int32_t* flags, void* ws,
+                               size_t ws_bytes, void* stream) {
+    ACP_TRY(check_shape(B, H, L, d, dt));
+    ACP_TRY(check_eps(eps));
+    ACP_TRY(check_ptr(log_f, "log_f"));
+    ACP_TRY(check_ptr(gamma_q, "gamma_q"));
+    ACP_TRY(check_ptr(gamma_k, "gamma_k"));
+    ACP_TRY(check_ptr(c, "c"));
+    ACP_TRY(check_ptr(bound_u, "bound_u"));
+    ACP_TRY(check_ptr(delta, "delta"));
+    ACP_TRY(check_ptr(row_start, "row_start"));
+    ACP_TRY(check_ptr(col_end, "col_end"));
+    ACP_TRY(check_ptr(kept, "kept"));
+    ACP_TRY(check_ptr(flags, "flags"));
+    const Layout y = layout(B, H, L, d);
+    ACP_TRY(check_ws(ws, ws_bytes, y));
+    acp::PlanArgs a = plan_args(nullptr, nullptr, log_f, dt, B, H, L, d, eps, y, (char*)ws);
+    a.gamma_q = gamma_q;
+    a.gamma_k = gamma_k;
+    a.c = c;
+    a.u = bound_u;
+    a.delta = delta;
+    a.row_start = row_start;
+    a.col_end = col_end;
+    a.kept = (long long*)kept;
+    a.flags = flags;
+    return hip_status(acp::launch_plan(a, (hipStream_t)stream), "acp_boundary_qknorm launch");
+}
+
+// Forward after a stage 1 whose bound comes from the row norms (gamma_q null)
+// or from QK-norm scales.
+static acp_status fwd_common(const void* Q, const void* K, const void* V, const float* log_f,
+                             const float* gamma_q, const float* gamma_k, acp_dtype dt, int B,
+                             int H, int L, int d, double eps, void* O, float* lse, void* ws,
+                             size_t ws_bytes, void* stream) {
     ACP_TRY(check_shape(B, H, L, d, dt));
     ACP_TRY(check_eps(eps));
     ACP_TRY(check_ptr(Q, "Q"));
@@ -270,7 +305,9 @@ acp_status fox_attn_fwd(const void* Q, const void* K, const void* V, const float
     const Layout y = layout(B, H, L, d);
     ACP_TRY(check_ws(ws, ws_bytes, y));
     char* w = (char*)ws;
-    const acp::PlanArgs p = plan_args(Q, K, log_f, dt, B, H, L, d, eps, y, w);
+    acp::PlanArgs p = plan_args(Q, K, log_f, dt, B, H, L, d, eps, y, w);
+    p.gamma_q = gamma_q;
+    p.gamma_k = gamma_k;
     hipError_t e = acp::launch_plan(p, (hipStream_t)stream);
     if (e != hipSuccess) return hip_status(e, "fox_attn_fwd boundary launch");
     acp::FwdArgs f{};
@@ -283,6 +320,23 @@ acp_status fox_attn_fwd(const void* Q, const void* K, const void* V, const float
     f.lse = lse;
     f.lse2 = (float*)(w + y.lse2);
     return hip_status(acp::launch_fwd(f, (hipStream_t)stream), "fox_attn_fwd launch");
+}
+
+acp_status fox_attn_fwd(const void* Q, const void* K, const void* V, const float* log_f,
+                        acp_dtype dt, int B, int H, int L, int d, double eps, void* O,
+                        float* lse, void* ws, size_t ws_bytes, void* stream) {
+    return fwd_common(Q, K, V, log_f, nullptr, nullptr, dt, B, H, L, d, eps, O, lse, ws,
+                      ws_bytes, stream);
+}
+
+acp_status fox_attn_fwd_qknorm(const void* Q, const void* K, const void* V, const float* log_f,
+                               const float* gamma_q, const float* gamma_k, acp_dtype dt, int B,
+                               int H, int L, int d, double eps, void* O, float* lse, void* ws,
+                               size_t ws_bytes, void* stream) {
+    ACP_TRY(check_ptr(gamma_q, "gamma_q"));
+    ACP_TRY(check_ptr(gamma_k, "gamma_k"));
+    return fwd_common(Q, K, V, log_f, gamma_q, gamma_k, dt, B, H, L, d, eps, O, lse, ws,
+                      ws_bytes, stream);
 }
 
 acp_status fox_attn_bwd(const void* Q, const void* K, const void* V, const void* O,

@@ -17,6 +17,8 @@ struct PlanArgs {
     int B, H, L, d;
     int nchunk;               // norm partials per (head, tensor)
     double log_l_over_eps;    // log L - log eps, +inf for eps = 0
+    const float* gamma_q;     // [H] QK-norm scale bounds, or null: U from the row norms
+    const float* gamma_k;     // [H]
     double* part;             // [B*H, 2, nchunk]
     float* c;                 // [B*H, L]
     double* u;                // [B*H]

@@ -9,6 +9,8 @@
 //                         maxima to rho_q^2, rho_k^2, form U and delta, scan
 //                         log f into c, then find every row's first kept block
 //                         and every column's last kept block.
+// With QK-norm scale bounds (App. E: U = gamma_q gamma_k sqrt(d)) the first
+// launch is skipped and the plan kernel takes U from the scales.
 #include "acp_device.h"
 #include "acp_internal.h"
 
@@ -121,6 +123,7 @@ __device__ __forceinline__ int lsb_exp(float x) {
 
 __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
     const float* __restrict__ log_f, const double* __restrict__ part, int nchunk,
+    const float* __restrict__ gamma_q, const float* __restrict__ gamma_k, int H,
     int L, int d, double log_l_over_eps,
     float* __restrict__ c_out,
     double* __restrict__ u_out, double* __restrict__ delta_out,
@@ -139,24 +142,40 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
     const int M = L / kBlock;
 
     // ---- rho_q^2, rho_k^2 (maxima are order-free) -------------------------
-    double mq = 0.0, mk = 0.0;
-    for (int i = t; i < nchunk; i += kPlanThreads) {
-        mq = nan_max(mq, part[((size_t)bh * 2 + 0) * nchunk + i]);
-        mk = nan_max(mk, part[((size_t)bh * 2 + 1) * nchunk + i]);
-    }
-    auto nmax = [](double a, double b) { return nan_max(a, b); };
-    mq = block_reduce(mq, s_dbl, nmax);
-    mk = block_reduce(mk, s_dbl, nmax);
     int flags = 0;
-    if (t == 0) {
-        // U = rho_q rho_k / sqrt(d) evaluated as sqrt(rho_q^2 rho_k^2 / d);
-        // delta = -2U - log L + log eps, every step rounded to nearest.
-        const double u = __builtin_sqrt((mq * mk) / (double)d);
+    if (gamma_q == nullptr) {
+        double mq = 0.0, mk = 0.0;
+        for (int i = t; i < nchunk; i += kPlanThreads) {
+            mq = nan_max(mq, part[((size_t)bh * 2 + 0) * nchunk + i]);
+            mk = nan_max(mk, part[((size_t)bh * 2 + 1) * nchunk + i]);
+        }
+        auto nmax = [](double a, double b) { return nan_max(a, b); };
+        mq = block_reduce(mq, s_dbl, nmax);
+        mk = block_reduce(mk, s_dbl, nmax);
+        if (t == 0) {
+            // U = rho_q rho_k / sqrt(d) evaluated as sqrt(rho_q^2 rho_k^2 / d);
+            // delta = -2U - log L + log eps, every step rounded to nearest.
+            const double u = __builtin_sqrt((mq * mk) / (double)d);
+            const double delta = -(2.0 * u + log_l_over_eps);
+            s_delta = delta;
+            u_out[bh] = u;
+            delta_out[bh] = delta;
+            if (!(mq <= 1.7976931348623157e308) || !(mk <= 1.7976931348623157e308)) flags |= 8;
+        }
+    } else if (t == 0) {
+        // QK-norm (App. E): an RMS-normalised row has norm sqrt(d) and a scale of
+        // magnitude at most gamma stretches it by at most gamma, so
+        // U = gamma_q gamma_k sqrt(d), evaluated as (gamma_q gamma_k) sqrt(d)
+        // (the product of two floats is exact in float64).
+        const int h = bh % H;
+        const double gq = (double)gamma_q[h], gk = (double)gamma_k[h];
+        const double u = (gq * gk) * __builtin_sqrt((double)d);
         const double delta = -(2.0 * u + log_l_over_eps);
         s_delta = delta;
         u_out[bh] = u;
         delta_out[bh] = delta;
-        if (!(mq <= 1.7976931348623157e308) || !(mk <= 1.7976931348623157e308)) flags |= 8;
+        if (!(gq >= 0.0 && gq <= 3.4028234663852886e38) || !(gk >= 0.0 && gk <= 3.4028234663852886e38))
+            flags |= 8;
     }
 
     // ---- c = cumsum(log f): each thread owns a contiguous run -------------
@@ -249,19 +268,22 @@ int norm_chunks(int L) { return (L + kNormRows - 1) / kNormRows; }
 hipError_t launch_plan(const PlanArgs& a, hipStream_t s) {
     hipError_t e;
     const int BH = a.B * a.H;
-    trace_begin(ACP_K_ROWNORM, s);
-    if (a.bf16) {
-        e = a.d == 64 ? launch_norm_t<__bf16, 64>(a.Q, a.K, BH, a.L, a.nchunk, a.part, s)
-                      : launch_norm_t<__bf16, 128>(a.Q, a.K, BH, a.L, a.nchunk, a.part, s);
-    } else {
-        e = a.d == 64 ? launch_norm_t<float, 64>(a.Q, a.K, BH, a.L, a.nchunk, a.part, s)
-                      : launch_norm_t<float, 128>(a.Q, a.K, BH, a.L, a.nchunk, a.part, s);
+    if (a.gamma_q == nullptr) {
+        trace_begin(ACP_K_ROWNORM, s);
+        if (a.bf16) {
+            e = a.d == 64 ? launch_norm_t<__bf16, 64>(a.Q, a.K, BH, a.L, a.nchunk, a.part, s)
+                          : launch_norm_t<__bf16, 128>(a.Q, a.K, BH, a.L, a.nchunk, a.part, s);
+        } else {
+            e = a.d == 64 ? launch_norm_t<float, 64>(a.Q, a.K, BH, a.L, a.nchunk, a.part, s)
+                          : launch_norm_t<float, 128>(a.Q, a.K, BH, a.L, a.nchunk, a.part, s);
+        }
+        if (e != hipSuccess) return e;
+        trace_end(ACP_K_ROWNORM, s);
     }
-    if (e != hipSuccess) return e;
-    trace_end(ACP_K_ROWNORM, s);
     trace_begin(ACP_K_PLAN, s);
     hipLaunchKernelGGL(plan_kernel, dim3(BH), dim3(kPlanThreads), 0, s,
-                       a.log_f, a.part, a.nchunk, a.L, a.d, a.log_l_over_eps,
+                       a.log_f, a.part, a.nchunk, a.gamma_q, a.gamma_k, a.H, a.L, a.d,
+                       a.log_l_over_eps,
                        a.c, a.u, a.delta, a.row_start, a.col_end, a.kept, a.flags);
     e = hipGetLastError();
     trace_end(ACP_K_PLAN, s);

@@ -14,9 +14,16 @@ The forget gate is f = sigmoid(a) (Sec. 2, eq. 1); log f = -softplus(-a) is
 evaluated in float64 and rounded once to float32, so that strongly remembering
 gates (mu = 20) do not round to log f = 0.
 
-Draw order (torch.Generator on the CPU): per-head mu, Q, K, V, gate noise, dO.
-Floating draws are float32 N(0,1) (rounded to nearest-even bfloat16 for the
-bf16 workloads).
+Draw order (torch.Generator on the CPU): per-head mu, Q, K, V, gate noise, dO,
+then (QK-norm workloads only) the per-head norm weights.  Floating draws are
+float32 N(0,1) (rounded to nearest-even bfloat16 for the bf16 workloads).
+
+QK-norm workloads stand in for a model with normalised queries and keys (the
+setting of the paper's App. E): every q and k row is RMS-normalised and scaled
+elementwise by a per-head weight vector drawn from U[0.5, 1.5]^d; gamma_q[h] and
+gamma_k[h] are the largest weight magnitudes.  The normalised row is shrunk by
+1 - 2^-7 first, so that rounding to bfloat16 (at most 2^-9 per element) keeps
+|q| <= gamma_q sqrt(d).
 """
 from __future__ import annotations
 
@@ -41,6 +48,7 @@ class Workload:
     gate_sigma: float = 0.5
     row_norms: Optional[Sequence[float]] = None  # per-head q/k row L2 norm (cycled)
     eps: float = math.exp(-10.0)
+    qk_norm: bool = False  # RMS-normalised, weight-scaled q/k rows (see the module note)
 
     @property
     def M(self) -> int:
@@ -66,10 +74,10 @@ WORKLOADS = {
 
 
 def custom(name: str, B: int, H: int, L: int, d: int, dtype: str, seed: int,
-           mu=None, row_norms=None, gate_sigma: float = 0.5) -> Workload:
+           mu=None, row_norms=None, gate_sigma: float = 0.5, qk_norm: bool = False) -> Workload:
     return Workload(name, B, H, L, d, dtype, seed, mu=None if mu is None else tuple(mu),
                     gate_sigma=gate_sigma,
-                    row_norms=None if row_norms is None else tuple(row_norms))
+                    row_norms=None if row_norms is None else tuple(row_norms), qk_norm=qk_norm)
 
 
 def _torch_dtype(dt: str):
@@ -116,6 +124,13 @@ def generate(w: Workload, with_grad: bool = True) -> dict:
     out = {"q": q, "k": k, "v": v, "log_f": log_f, "mu": mu}
     if with_grad:
         out["do"] = torch.randn(shape, generator=g, dtype=torch.float32)
+    if w.qk_norm:
+        for name in ("q", "k"):
+            wt = torch.rand((H, d), generator=g, dtype=torch.float32) + 0.5
+            x = out[name].double()
+            xn = x / torch.sqrt((x * x).mean(dim=-1, keepdim=True)) * (1.0 - 2.0 ** -7)
+            out[name] = (xn * wt.double().view(1, H, 1, d)).float()
+            out["gamma_" + name] = wt.abs().amax(dim=-1).contiguous()
     td = _torch_dtype(w.dtype)
     for name in ("q", "k", "v", "do"):
         if name in out:

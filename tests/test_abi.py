@@ -17,9 +17,9 @@ def _lib():
 def test_every_declared_symbol_is_exported():
     names = acp.header_functions()
     assert set(names) == {"acp_workspace_size", "acp_plan_offsets", "acp_boundary",
-                          "fox_attn_fwd", "fox_attn_bwd", "acp_timing_enable",
-                          "acp_timing_reset", "acp_timing_read", "acp_status_string",
-                          "acp_last_error"}
+                          "acp_boundary_qknorm", "fox_attn_fwd", "fox_attn_fwd_qknorm",
+                          "fox_attn_bwd", "acp_timing_enable", "acp_timing_reset",
+                          "acp_timing_read", "acp_status_string", "acp_last_error"}
     lib = ctypes.CDLL(acp.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
@@ -86,6 +86,21 @@ def _fwd(**kw):
 def test_forward_rejects_before_launch(kw, status):
     assert _fwd(**kw) == status
     assert acp.acp_last_error() != ""
+
+
+def test_qknorm_entries_reject_before_launch():
+    st = acp.acp_boundary_qknorm(16, 0, 16, acp.ACP_BF16, 1, 1, 64, 64, 0.5, 16, 16, 16, 16, 16,
+                                 16, 16, 16, 1 << 40, None)
+    assert st == acp.ACP_EINVAL and "gamma_q" in acp.acp_last_error()
+    st = acp.acp_boundary_qknorm(16, 16, 16, acp.ACP_BF16, 1, 1, 64, 64, 1.5, 16, 16, 16, 16, 16,
+                                 16, 16, 16, 1 << 40, None)
+    assert st == acp.ACP_EINVAL and "eps" in acp.acp_last_error()
+    st = acp.fox_attn_fwd_qknorm(16, 16, 16, 16, 16, 8, acp.ACP_BF16, 1, 1, 64, 64, 0.5, 16, 16,
+                                 16, 1 << 40, None)
+    assert st == acp.ACP_EINVAL and "gamma_k" in acp.acp_last_error()
+    st = acp.fox_attn_fwd_qknorm(16, 16, 16, 16, 16, 16, acp.ACP_BF16, 1, 1, 64, 64, 0.5, 16, 16,
+                                 16, 8, None)
+    assert st == acp.ACP_EWORKSPACE
 
 
 def test_backward_and_boundary_reject_before_launch():

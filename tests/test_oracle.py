@@ -91,6 +91,51 @@ def test_bound_dominates_every_logit_and_is_attained():
     assert abs(q[iq] @ k2[ik] / math.sqrt(d) - U2) <= 1e-12 * U2
 
 
+def _rms_rows(x):
+    return x / np.sqrt(np.mean(x * x, axis=1, keepdims=True))
+
+
+def test_qknorm_bound_attained_by_constant_rows():
+    # RMSNorm of a constant row is all ones; with every weight at gamma the rows are
+    # gamma_q 1 and gamma_k 1, whose logit gamma_q gamma_k d / sqrt(d) is the bound.
+    d, gq, gk = 64, 1.375, 0.8125            # dyadic: every step below is exact
+    q = _rms_rows(np.full((3, d), -2.5)) * gq
+    k = _rms_rows(np.full((5, d), 7.0)) * gk
+    U = orc.logit_bound_qknorm(gq, gk, d)
+    assert U == gq * gk * 8.0
+    assert np.max(np.abs(q @ k.T)) / math.sqrt(d) == U
+
+
+def test_qknorm_bound_dominates_normalised_scaled_rows():
+    rng = _rng(11)
+    L, d = 300, 64
+    wq = rng.uniform(-1.7, 1.7, d); wk = rng.uniform(0.2, 0.9, d)
+    q = _rms_rows(rng.standard_normal((L, d)) * rng.uniform(0.1, 9.0, (L, 1))) * wq
+    k = _rms_rows(rng.standard_normal((L, d))) * wk
+    U = orc.logit_bound_qknorm(np.max(np.abs(wq)), np.max(np.abs(wk)), d)
+    assert np.max(np.abs(q @ k.T)) / math.sqrt(d) <= U
+    # it is never tighter than the bound from the actual row norms
+    U_rows = orc.logit_bound(orc.row_norm_sq_max(q), orc.row_norm_sq_max(k), d)
+    assert U_rows <= U
+
+
+def test_plan_with_given_bound_prunes_a_subset():
+    # a larger (still valid) U lowers delta, so the pruned blocks shrink
+    w = workloads.custom("qk", 1, 2, 512, 64, "f32", 21, mu=(1.0, 2.0), qk_norm=True)
+    x = workloads.generate(w, with_grad=False)
+    for h in range(2):
+        q = workloads.to_f64(x["q"][0, h]); k = workloads.to_f64(x["k"][0, h])
+        lf = x["log_f"][0, h].numpy()
+        U = orc.logit_bound_qknorm(float(x["gamma_q"][h]), float(x["gamma_k"][h]), 64)
+        pn = orc.plan_head(q, k, lf, EPS)
+        pq = orc.plan_head(q, k, lf, EPS, U=U)
+        assert pq["U"] == U and pn["U"] <= U
+        assert pq["delta"] == orc.threshold(U, 512, EPS)
+        assert np.all(pq["row_start"] <= pn["row_start"])
+        kb = orc.block_keep_bruteforce(pq["c"], pq["delta"])
+        np.testing.assert_array_equal(pq["row_start"], orc.boundary_from_block_keep(kb)[0])
+
+
 def test_threshold_hand_value():
     # U = 2, L = 512, eps = e^-10: delta = -(4 + 9 ln 2 + 10)
     delta = orc.threshold(2.0, 512, EPS)
