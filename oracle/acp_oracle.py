@@ -48,6 +48,7 @@ __all__ = [
     "boundary_alg1", "col_end_from_row_start", "kept_tiles", "causal_tiles",
     "block_mask", "entry_mask", "causal_mask", "forward", "backward", "pruned_mass",
     "plan_head", "run_head", "forward_rows", "backward_rows", "backward_cols",
+    "decode_pointer", "decode_row",
 ]
 
 
@@ -459,3 +460,42 @@ def backward_cols(q, k, v, c, row_start, do, cols, block: int = BLOCK):
             dk[r] += ds_ij * q[i] / math.sqrt(d)
             cs[r] += ds_ij
     return dk, dv, cs
+
+
+# --------------------------------------------------------------------------
+# Decoding (Sec. 5, inference: a per-head boundary pointer that only moves
+# forward, with the cache entries behind it dropped)
+# --------------------------------------------------------------------------
+
+def decode_pointer(c, t: int, delta: float, block: int = BLOCK) -> int:
+    """First kept key block for the single query t: block n < t // block is kept iff
+    some entry of it has D_tj = c_t - c_j >= delta (eq. 3 for one row); c is
+    non-increasing, so that entry is the block's last key, 64 n + 63.  The block
+    holding t is always kept (D_tt = 0).  Compared in float64 on the float32 c.
+
+    Because c_t only falls as t grows, the pointer never moves back, and the keys
+    before 64 * pointer can be dropped for every later query as well."""
+    c64 = np.asarray(c).astype(np.float64)
+    nb = t // block
+    for n in range(nb):
+        if c64[t] - c64[n * block + block - 1] >= delta:
+            return n
+    return nb
+
+
+def decode_row(q_t, k, v, c, t: int, delta: float, block: int = BLOCK):
+    """Output of query t over the keys kept for it alone (eq. 1-2 on the entries
+    j in [64 n_t, t] with n_t = decode_pointer): (o [d], lse, n_t)."""
+    q_t = np.asarray(q_t, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    v = np.asarray(v, dtype=np.float64)
+    c64 = np.asarray(c).astype(np.float64)
+    d = q_t.shape[0]
+    n = decode_pointer(c, t, delta, block)
+    j = np.arange(n * block, t + 1)
+    x = (k[j] @ q_t) / math.sqrt(d) + (c64[t] - c64[j])
+    m = np.max(x)
+    e = np.exp(x - m)
+    z = np.sum(e)
+    return (e / z) @ v[j], m + math.log(z), n
+

@@ -380,3 +380,58 @@ def test_backward_no_forgetting_is_sdpa_autograd():
     (o * torch.from_numpy(do)).sum().backward()
     for name, tt in zip(("dq", "dk", "dv"), t):
         np.testing.assert_allclose(g[name], tt.grad.numpy(), rtol=0, atol=1e-11)
+
+
+# --------------------------------------------------------------------------
+# Decoding with an online boundary pointer (Sec. 5)
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("mu", [1.0, 3.0])
+def test_decode_pointer_is_first_block_with_a_kept_entry_and_monotone(mu):
+    rng = _rng(int(10 * mu))
+    L = 700
+    lf = workloads.log_sigmoid_f32(rng.normal(mu, 0.5, L))
+    c = orc.cumsum_log_gates(lf)
+    delta = -12.0
+    prev = 0
+    for t in range(L):
+        row = orc.entry_keep(c, delta)[t]                 # eq. 3, one row
+        kept_blocks = [n for n in range(t // 64 + 1) if np.any(row[n * 64:(n + 1) * 64])]
+        n = orc.decode_pointer(c, t, delta)
+        assert n == kept_blocks[0], t
+        assert n >= prev                                 # never moves back
+        prev = n
+    assert prev > 0
+
+
+def test_decode_row_without_pruning_is_the_causal_row():
+    rng = _rng(17)
+    L, d = 150, 32
+    q, k, v = rng.standard_normal((3, L, d))
+    lf = workloads.log_sigmoid_f32(rng.normal(2.0, 0.5, L))
+    c = orc.cumsum_log_gates(lf)
+    o_full, lse_full = orc.forward(q, k, v, c, orc.causal_mask(L))
+    for t in (0, 63, 64, 149):
+        o, lse, n = orc.decode_row(q[t], k, v, c, t, -math.inf)
+        assert n == 0
+        np.testing.assert_allclose(o, o_full[t], rtol=0, atol=1e-12)
+        assert abs(lse - lse_full[t]) <= 1e-12
+
+
+def test_decode_prunes_at_least_the_prefill_blocks_and_stays_within_eps():
+    rng = _rng(23)
+    L, d = 512, 64
+    q, k, v = rng.standard_normal((3, L, d))
+    lf = workloads.log_sigmoid_f32(rng.normal(1.0, 0.5, L))
+    p = orc.plan_head(q, k, lf, EPS)
+    c, delta = p["c"], p["delta"]
+    c64 = c.astype(np.float64)
+    full = np.where(orc.causal_mask(L), q @ k.T / math.sqrt(d) + c64[:, None] - c64[None, :], -np.inf)
+    a = np.exp(full - np.max(full, axis=1, keepdims=True))
+    a /= np.sum(a, axis=1, keepdims=True)
+    for t in range(0, L, 37):
+        n = orc.decode_pointer(c, t, delta)
+        assert n >= p["row_start"][t // 64]              # one row prunes at least its block's keys
+        assert np.sum(a[t, :64 * n]) < EPS                # App. A bound, L = context length
+        o, _, _ = orc.decode_row(q[t], k, v, c, t, delta)
+        assert np.max(np.abs(o - a[t] @ v)) <= 2 * EPS * np.max(np.abs(v))
