@@ -26,6 +26,12 @@ is silent or garbled are settled as follows (the same readings bind the HIP path
   first kept block; the reading used here is "first kept block of the row"
   (the boundary block the text defines), so the pointer is tested before it is
   advanced.
+* decoding (Sec. 5): the bound U must be known before the tokens are (QK-norm
+  scales, App. E), and the threshold is sized for the longest sequence L_max,
+  delta = -(2U + log L_max - log eps), so that it stays fixed as t grows (App. A
+  needs only that a row holds at most L_max entries).  A cache of fixed size
+  keeps the last positions; see decode_ring_row for what is attended when it
+  has dropped a kept key.
 * backward: the paper only says it follows the forward.  The mask is a constant
   (the indicator has zero derivative almost everywhere, and delta's dependence on
   Q and K is not differentiated).  With x_ij = q_i.k_j/sqrt(d) + c_i - c_j:
@@ -48,7 +54,7 @@ __all__ = [
     "boundary_alg1", "col_end_from_row_start", "kept_tiles", "causal_tiles",
     "block_mask", "entry_mask", "causal_mask", "forward", "backward", "pruned_mass",
     "plan_head", "run_head", "forward_rows", "backward_rows", "backward_cols",
-    "decode_pointer", "decode_row",
+    "decode_pointer", "decode_row", "decode_ring_row",
 ]
 
 
@@ -483,19 +489,41 @@ def decode_pointer(c, t: int, delta: float, block: int = BLOCK) -> int:
     return nb
 
 
-def decode_row(q_t, k, v, c, t: int, delta: float, block: int = BLOCK):
-    """Output of query t over the keys kept for it alone (eq. 1-2 on the entries
-    j in [64 n_t, t] with n_t = decode_pointer): (o [d], lse, n_t)."""
+def _attend_range(q_t, k, v, c, t: int, lo: int):
+    """Eq. 1-2 for the single query t over the keys j = lo .. t: (o [d], lse)."""
     q_t = np.asarray(q_t, dtype=np.float64)
     k = np.asarray(k, dtype=np.float64)
     v = np.asarray(v, dtype=np.float64)
     c64 = np.asarray(c).astype(np.float64)
     d = q_t.shape[0]
-    n = decode_pointer(c, t, delta, block)
-    j = np.arange(n * block, t + 1)
+    j = np.arange(lo, t + 1)
     x = (k[j] @ q_t) / math.sqrt(d) + (c64[t] - c64[j])
     m = np.max(x)
     e = np.exp(x - m)
     z = np.sum(e)
-    return (e / z) @ v[j], m + math.log(z), n
+    return (e / z) @ v[j], m + math.log(z)
+
+
+def decode_row(q_t, k, v, c, t: int, delta: float, block: int = BLOCK):
+    """Output of query t over the keys kept for it alone (eq. 1-2 on the entries
+    j in [64 n_t, t] with n_t = decode_pointer): (o [d], lse, n_t)."""
+    n = decode_pointer(c, t, delta, block)
+    o, lse = _attend_range(q_t, k, v, c, t, n * block)
+    return o, lse, n
+
+
+def decode_ring_row(q_t, k, v, c, t: int, delta: float, capacity: int, block: int = BLOCK):
+    """Decoding from a cache that holds only the last `capacity` positions,
+    t - capacity + 1 .. t.  Sec. 5 proposes dropping the entries behind the
+    pointer; a cache of fixed size may also have to drop kept ones.  Reading
+    used here: the query then attends to the kept keys still held,
+    j in [max(64 n_t, t - capacity + 1), t], `lost` says whether a kept key was
+    dropped, and the pointer reported is max(n_t, block of position
+    t - capacity + 1), the first block whose test can still be made.
+    Returns (o [d], lse, pointer, lost)."""
+    n = decode_pointer(c, t, delta, block)
+    first = t - capacity + 1
+    lost = first > 0 and n * block < first
+    o, lse = _attend_range(q_t, k, v, c, t, max(n * block, first, 0))
+    return o, lse, max(n, first // block if first > 0 else 0), lost
 

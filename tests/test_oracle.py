@@ -435,3 +435,68 @@ def test_decode_prunes_at_least_the_prefill_blocks_and_stays_within_eps():
         assert np.sum(a[t, :64 * n]) < EPS                # App. A bound, L = context length
         o, _, _ = orc.decode_row(q[t], k, v, c, t, delta)
         assert np.max(np.abs(o - a[t] @ v)) <= 2 * EPS * np.max(np.abs(v))
+
+
+def test_decode_ring_row_matches_brute_force_key_sets():
+    """Ring cache of C positions: the attended keys are the entries j in
+    [t - C + 1, t] whose block holds some entry kept by eq. 3 (or is t's own
+    block), found here entry by entry; `lost` is whether such a block also has
+    keys before t - C + 1."""
+    rng = _rng(29)
+    L, d = 400, 16
+    q, k, v = rng.standard_normal((3, L, d))
+    lf = workloads.log_sigmoid_f32(rng.normal(0.5, 0.5, L))
+    c = orc.cumsum_log_gates(lf)
+    c64 = c.astype(np.float64)
+    delta = -20.0
+    keep = orc.entry_keep(c, delta)
+    for C in (64, 128, 192):
+        prev = 0
+        for t in range(0, L, 7):
+            blocks = {n for n in range(t // 64 + 1)
+                      if n == t // 64 or np.any(keep[t, n * 64:(n + 1) * 64])}
+            held = [j for j in range(max(0, t - C + 1), t + 1) if j // 64 in blocks]
+            lost_ref = any(j // 64 in blocks for j in range(0, max(0, t - C + 1)))
+            x = q[t] @ k[held].T / math.sqrt(d) + c64[t] - c64[held]
+            p = np.exp(x - np.max(x))
+            o_ref = (p / p.sum()) @ v[held]
+            o, lse, ptr, lost = orc.decode_ring_row(q[t], k, v, c, t, delta, C)
+            assert lost == lost_ref, (C, t)
+            np.testing.assert_allclose(o, o_ref, rtol=0, atol=1e-12)
+            assert abs(lse - (np.max(x) + math.log(p.sum()))) <= 1e-12
+            assert ptr >= prev and ptr * 64 <= held[0] < (ptr + 1) * 64 + (0 if not lost else 64)
+            prev = ptr
+        assert prev > 0
+
+
+def test_decode_ring_row_without_pruning_is_sliding_window_attention():
+    """eps = 0 (delta = -inf): the ring reduces to attention over the last C
+    positions, checked against torch's attention with an additive mask."""
+    rng = _rng(31)
+    L, d, C = 300, 32, 128
+    q, k, v = rng.standard_normal((3, L, d))
+    lf = workloads.log_sigmoid_f32(rng.normal(2.0, 0.5, L))
+    c = orc.cumsum_log_gates(lf).astype(np.float64)
+    for t in (0, 127, 128, 200, 299):
+        j = np.arange(L)
+        bias = np.where((j <= t) & (j >= t - C + 1), c[t] - c, -np.inf)
+        ref = torch.nn.functional.scaled_dot_product_attention(
+            torch.from_numpy(q[t][None, None]), torch.from_numpy(k[None]), torch.from_numpy(v[None]),
+            attn_mask=torch.from_numpy(bias[None, None]))[0, 0].numpy()
+        o, _, ptr, lost = orc.decode_ring_row(q[t], k, v, c.astype(np.float32), t, -math.inf, C)
+        np.testing.assert_allclose(o, ref, rtol=0, atol=1e-12)
+        assert lost == (t >= C)
+        assert ptr == max(0, t - C + 1) // 64
+
+
+def test_decode_ring_row_with_room_is_decode_row():
+    rng = _rng(37)
+    L, d = 260, 16
+    q, k, v = rng.standard_normal((3, L, d))
+    lf = workloads.log_sigmoid_f32(rng.normal(1.0, 0.5, L))
+    c = orc.cumsum_log_gates(lf)
+    for t in (5, 100, 259):
+        a = orc.decode_row(q[t], k, v, c, t, -15.0)
+        b = orc.decode_ring_row(q[t], k, v, c, t, -15.0, 320)
+        np.testing.assert_array_equal(a[0], b[0])
+        assert a[1] == b[1] and a[2] == b[2] and b[3] is False
