@@ -38,6 +38,8 @@
  *              its last bit from the sequential float64 definition
  *       bit 3  rho_q^2 or rho_k^2 is not finite (Q or K holds NaN/Inf or overflows),
  *              or, in the QK-norm variants, a scale bound is negative or not finite
+ *       bit 4  (decoding only) a key that ACP keeps had already left the ring cache,
+ *              so the output covers only the kept keys the cache still holds
  *     With bit 0, 1 or 3 set the boundary and the attention outputs are unspecified.
  *
  * Numerics of the pruning decision (identical on every device and on the host):
@@ -159,6 +161,69 @@ acp_status fox_attn_bwd(const void* Q, const void* K, const void* V, const void*
                         void* dQ, void* dK, void* dV, float* dlog_f,
                         void* ws, size_t ws_bytes, void* stream);
 
+/* ---- Decoding with ACP (Sec. 5, inference) -----------------------------------
+ * Token-by-token attention after a prompt, with a logit bound fixed in advance
+ * by QK-norm scales (App. E) and the threshold sized for the longest sequence:
+ *   U = (gamma_q gamma_k) sqrt(d),  delta = -(2U + (log L_max - log eps)).
+ * Since c_t never grows with t, the first key block kept by query t (the block
+ * test of Sec. 3 applied to the single row t: block n < t/64 is kept iff
+ * c_t - c_{64n+63} >= delta, the block holding t always) never moves back as t
+ * grows; each (batch, head) keeps it as a pointer and reads keys from 64 pointer
+ * on.  For t + 1 <= L_max the dropped mass of every row is below eps (App. A).
+ *
+ * State: one caller-owned device buffer of acp_decode_state_size() bytes holds,
+ * per (batch, head), a ring cache of C positions (position j in slot j mod C)
+ * for K, V and c, the float64 running sum of log f, delta, the pointer and the
+ * flag word.  C is a multiple of 64; with ACP it only needs to cover the kept
+ * window (positions from 64 pointer to t), which is how ACP frees the cache
+ * memory behind the pointer.  If a kept key is overwritten, flag bit 4 is set and
+ * the query attends to the kept keys the ring still holds, positions
+ * max(64 pointer, t - C + 1) .. t; the pointer then never lies below the block
+ * of position t - C + 1.  Calls on one state must not overlap.
+ *
+ * Per-token tensors are [B, H, d] (q, k, v, O) and [B, H] (log_f, lse), element
+ * type dt for q, k, v, O.  Supported: d in {64, 128}; C a multiple of 64 with
+ * 64 <= C <= 131072; 1 <= L0 <= 131072; L0 <= L_max <= 2^31; 0 <= eps < 1.
+ * The data-error flags of the prompt's cumulative sum (bits 0-2) carry on into
+ * the steps, and bit 3 reports a negative or non-finite gamma. */
+
+/* Offsets, inside a decoding state, of what it holds (multiples of 256). */
+typedef struct {
+    size_t k_cache;    /* [B,H,C,d] dt     keys, position j in slot j mod C          */
+    size_t v_cache;    /* [B,H,C,d] dt     values                                    */
+    size_t c;          /* [B,H,C]   float  c_j of the cached positions               */
+    size_t cum;        /* [B,H]     double running float64 sum of log f so far       */
+    size_t delta;      /* [B,H]     double delta                                     */
+    size_t pointer;    /* [B,H]     int32  first kept key block of the latest query  */
+    size_t flags;      /* [B,H]     int32  data-error bits                           */
+    size_t total;      /* bytes = acp_decode_state_size()                            */
+} acp_decode_layout;
+
+acp_status acp_decode_state_size(int B, int H, int C, int d, acp_dtype dt, size_t* bytes);
+acp_status acp_decode_offsets(int B, int H, int C, int d, acp_dtype dt, acp_decode_layout* out);
+
+/* Start decoding after a prompt of L0 tokens (prefill is fox_attn_fwd_qknorm on
+ * the prompt; this call only builds the state): delta from gamma_q, gamma_k [H]
+ * float, eps and L_max; c of the prompt from log_f [B,H,L0] float; the pointer
+ * of query L0 - 1; the last min(L0, C) rows of K, V [B,H,L0,d] dt copied into
+ * the ring.  Overwrites the whole state's bookkeeping; the caches' slots that
+ * the prompt does not fill are left as they are and never read. */
+acp_status acp_decode_init(const void* K, const void* V, const float* log_f,
+                           const float* gamma_q, const float* gamma_k, acp_dtype dt,
+                           int B, int H, int L0, int C, int d, double eps, int64_t L_max,
+                           void* state, size_t state_bytes, void* stream);
+
+/* One decoding step for the token at position t (t = L0 for the first step after
+ * acp_decode_init, then t + 1 for each next call; other values give unspecified
+ * results): adds log_f [B,H] to the running sum (c_t), appends k, v [B,H,d] to the
+ * ring, advances the pointer, and writes the attention output of query q [B,H,d]
+ * over its kept keys (eq. 1-2 restricted by the block test above):
+ *   O [B,H,d] dt, lse [B,H] float (natural-log log-sum-exp of the kept logits).
+ * Requires 1 <= t < L_max (checked against the L_max the caller states again). */
+acp_status fox_attn_decode(const void* q, const void* k, const void* v, const float* log_f,
+                           acp_dtype dt, int B, int H, int t, int C, int d, int64_t L_max,
+                           void* O, float* lse, void* state, size_t state_bytes, void* stream);
+
 /* Optional per-kernel timing (tracing).  While enabled, the library brackets
  * each kernel it launches with a pair of HIP events on the launch stream.
  * acp_timing_read() waits for the recorded events and fills, per kernel, the
@@ -174,7 +239,10 @@ enum {
     ACP_K_DQ = 4,       /* dQ and row sums of dS                */
     ACP_K_DKDV = 5,     /* dK, dV and column sums of dS         */
     ACP_K_DLOGF = 6,    /* reverse cumulative sum -> dlog f     */
-    ACP_K_COUNT = 7
+    ACP_K_DECODE_INIT = 7, /* decoding state from a prompt      */
+    ACP_K_DECODE = 8,   /* one decoding step (append, attention
+                           over kept keys, split combine)        */
+    ACP_K_COUNT = 9
 };
 typedef struct {
     int64_t launches[ACP_K_COUNT];

@@ -25,6 +25,7 @@ FLAG_POSITIVE_GATE = 1
 FLAG_NONFINITE_GATE = 2
 FLAG_INEXACT_CUMSUM = 4
 FLAG_NONFINITE_NORM = 8
+FLAG_KEPT_KEY_EVICTED = 16
 
 
 class AcpError(RuntimeError):
@@ -38,7 +39,12 @@ class PlanLayout(ctypes.Structure):
                 ("c", "bound_u", "delta", "row_start", "col_end", "kept", "flags", "total")]
 
 
-K_NAMES = ("rownorm", "plan", "fwd", "dsum", "dq", "dkdv", "dlogf")
+class DecodeLayout(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_size_t) for n in
+                ("k_cache", "v_cache", "c", "cum", "delta", "pointer", "flags", "total")]
+
+
+K_NAMES = ("rownorm", "plan", "fwd", "dsum", "dq", "dkdv", "dlogf", "decode_init", "decode")
 
 
 class KernelTimes(ctypes.Structure):
@@ -48,6 +54,7 @@ class KernelTimes(ctypes.Structure):
 
 _lib = None
 _i, _d, _p, _sz = ctypes.c_int, ctypes.c_double, ctypes.c_void_p, ctypes.c_size_t
+_i64 = ctypes.c_int64
 
 _SIGS = {
     "acp_workspace_size": [_i, _i, _i, _i, _i, ctypes.POINTER(_sz)],
@@ -59,6 +66,10 @@ _SIGS = {
     "fox_attn_fwd_qknorm": [_p, _p, _p, _p, _p, _p, _i, _i, _i, _i, _i, _d, _p, _p, _p, _sz,
                             _p],
     "fox_attn_bwd": [_p, _p, _p, _p, _p, _i, _i, _i, _i, _i, _p, _p, _p, _p, _p, _sz, _p],
+    "acp_decode_state_size": [_i, _i, _i, _i, _i, ctypes.POINTER(_sz)],
+    "acp_decode_offsets": [_i, _i, _i, _i, _i, ctypes.POINTER(DecodeLayout)],
+    "acp_decode_init": [_p, _p, _p, _p, _p, _i, _i, _i, _i, _i, _i, _d, _i64, _p, _sz, _p],
+    "fox_attn_decode": [_p, _p, _p, _p, _i, _i, _i, _i, _i, _i, _i64, _p, _p, _p, _sz, _p],
     "acp_timing_enable": [_i],
     "acp_timing_reset": [],
     "acp_timing_read": [ctypes.POINTER(KernelTimes)],
@@ -144,6 +155,30 @@ def fox_attn_bwd(Q, K, V, O, dO, dt, B, H, L, d, dQ, dK, dV, dlog_f, ws, ws_byte
                  stream) -> int:
     return lib().fox_attn_bwd(Q, K, V, O, dO, dt, B, H, L, d, dQ, dK, dV, dlog_f, ws,
                               ws_bytes, stream)
+
+
+def acp_decode_state_size(B, H, C, d, dt) -> int:
+    out = _sz(0)
+    _check(lib().acp_decode_state_size(B, H, C, d, dt, ctypes.byref(out)))
+    return out.value
+
+
+def acp_decode_offsets(B, H, C, d, dt) -> DecodeLayout:
+    out = DecodeLayout()
+    _check(lib().acp_decode_offsets(B, H, C, d, dt, ctypes.byref(out)))
+    return out
+
+
+def acp_decode_init(K, V, log_f, gamma_q, gamma_k, dt, B, H, L0, C, d, eps, L_max, state,
+                    state_bytes, stream) -> int:
+    return lib().acp_decode_init(K, V, log_f, gamma_q, gamma_k, dt, B, H, L0, C, d, eps, L_max,
+                                 state, state_bytes, stream)
+
+
+def fox_attn_decode(q, k, v, log_f, dt, B, H, t, C, d, L_max, O, lse, state, state_bytes,
+                    stream) -> int:
+    return lib().fox_attn_decode(q, k, v, log_f, dt, B, H, t, C, d, L_max, O, lse, state,
+                                 state_bytes, stream)
 
 
 def acp_timing_enable(on: bool):
@@ -332,3 +367,77 @@ def plan_views(ws: torch.Tensor, B: int, H: int, L: int, d: int, dtype) -> dict:
         "kept": view(lay.kept, B * H, torch.int64).view(B, H),
         "flags": view(lay.flags, B * H, torch.int32).view(B, H),
     }
+
+
+class Decoder:
+    """Decoding state of acp_decode_init / fox_attn_decode for B x H heads: a ring
+    cache of C positions per head plus the per-head pointer, delta and flags, in
+    one device buffer.  Tracks the next position t on the host."""
+
+    def __init__(self, B: int, H: int, C: int, d: int, dtype=torch.bfloat16, device="cuda"):
+        self.B, self.H, self.C, self.d, self.dtype = B, H, C, d, dtype
+        self.dt = ACP_F32 if dtype == torch.float32 else ACP_BF16
+        n = acp_decode_state_size(B, H, C, d, self.dt)
+        self.state = torch.empty(n, dtype=torch.uint8, device=device)
+        self.t = None
+        self.L_max = None
+
+    def init(self, k, v, log_f, gamma_q, gamma_k, eps: float, L_max: int):
+        """Build the state from a prompt: k, v [B, H, L0, d], log_f [B, H, L0]."""
+        dev = _dev(k, v, log_f, gamma_q, gamma_k, self.state)
+        B, H, L0, d = _shape(k)
+        if (B, H, d) != (self.B, self.H, self.d) or v.shape != k.shape:
+            raise ValueError("prompt K/V shape does not match the decoder")
+        if k.dtype != self.dtype or v.dtype != self.dtype:
+            raise ValueError("prompt K/V dtype does not match the decoder")
+        if tuple(log_f.shape) != (B, H, L0) or log_f.dtype != torch.float32:
+            raise ValueError("log_f must be float32 [B, H, L0]")
+        _check_gammas(gamma_q, gamma_k, H)
+        _check(acp_decode_init(k.data_ptr(), v.data_ptr(), log_f.data_ptr(), gamma_q.data_ptr(),
+                               gamma_k.data_ptr(), self.dt, B, H, L0, self.C, d, eps, L_max,
+                               self.state.data_ptr(), self.state.numel(), _stream(dev)))
+        self.t, self.L_max = L0, L_max
+        return self
+
+    def step(self, q, k, v, log_f, out=None):
+        """Append token t (k, v [B, H, d], log_f [B, H]) and attend with q [B, H, d];
+        returns (O [B, H, d], lse [B, H])."""
+        if self.t is None:
+            raise RuntimeError("call init() first")
+        dev = _dev(q, k, v, log_f, self.state)
+        for name, x in (("q", q), ("k", k), ("v", v)):
+            if tuple(x.shape) != (self.B, self.H, self.d) or x.dtype != self.dtype:
+                raise ValueError(name + " must be [B, H, d] of the decoder's dtype")
+        if tuple(log_f.shape) != (self.B, self.H) or log_f.dtype != torch.float32:
+            raise ValueError("log_f must be float32 [B, H]")
+        if out is None:
+            o = torch.empty_like(q)
+            lse = torch.empty((self.B, self.H), dtype=torch.float32, device=dev)
+        else:
+            o, lse = out
+        _check(fox_attn_decode(q.data_ptr(), k.data_ptr(), v.data_ptr(), log_f.data_ptr(),
+                               self.dt, self.B, self.H, self.t, self.C, self.d, self.L_max,
+                               o.data_ptr(), lse.data_ptr(), self.state.data_ptr(),
+                               self.state.numel(), _stream(dev)))
+        self.t += 1
+        return o, lse
+
+    def views(self) -> dict:
+        """Views of the state: k_cache, v_cache [B,H,C,d], c [B,H,C], cum, delta,
+        pointer, flags [B,H]."""
+        lay = acp_decode_offsets(self.B, self.H, self.C, self.d, self.dt)
+        B, H, C, d = self.B, self.H, self.C, self.d
+
+        def view(off, n, t):
+            nbytes = n * torch.empty((), dtype=t).element_size()
+            return self.state[off:off + nbytes].view(t)
+
+        return {
+            "k_cache": view(lay.k_cache, B * H * C * d, self.dtype).view(B, H, C, d),
+            "v_cache": view(lay.v_cache, B * H * C * d, self.dtype).view(B, H, C, d),
+            "c": view(lay.c, B * H * C, torch.float32).view(B, H, C),
+            "cum": view(lay.cum, B * H, torch.float64).view(B, H),
+            "delta": view(lay.delta, B * H, torch.float64).view(B, H),
+            "pointer": view(lay.pointer, B * H, torch.int32).view(B, H),
+            "flags": view(lay.flags, B * H, torch.int32).view(B, H),
+        }

@@ -61,6 +61,10 @@ Layout layout(int B, int H, int L, int d) {
     return y;
 }
 
+struct DecLayout {
+    size_t k, v, c, cum, delta, ptr, flags, part, total;
+};
+
 acp_status check_shape(int B, int H, int L, int d, acp_dtype dt) {
     if (B <= 0 || H <= 0 || L <= 0 || d <= 0)
         return fail(ACP_EINVAL, "sizes must be positive (B=%d H=%d L=%d d=%d)", B, H, L, d);
@@ -368,6 +372,133 @@ acp_status fox_attn_bwd(const void* Q, const void* K, const void* V, const void*
     b.colsum = (float*)(w + y.colsum);
     b.dQ = dQ; b.dK = dK; b.dV = dV; b.dlog_f = dlog_f;
     return hip_status(acp::launch_bwd(b, (hipStream_t)stream), "fox_attn_bwd launch");
+}
+
+// ---- decoding ----------------------------------------------------------------------
+static DecLayout dec_layout(int B, int H, int C, int d, acp_dtype dt) {
+    DecLayout y{};
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        const size_t o = off;
+        off += (bytes + 255) & ~(size_t)255;
+        return o;
+    };
+    const size_t BH = (size_t)B * H, es = dt == ACP_BF16 ? 2 : 4;
+    y.k = take(BH * C * d * es);
+    y.v = take(BH * C * d * es);
+    y.c = take(BH * C * 4);
+    y.cum = take(BH * 8);
+    y.delta = take(BH * 8);
+    y.ptr = take(BH * 4);
+    y.flags = take(BH * 4);
+    y.part = take(acp::decode_partials_floats((int)BH, C, d) * 4);
+    y.total = off;
+    return y;
+}
+
+static acp_status check_dec_shape(int B, int H, int C, int d, acp_dtype dt) {
+    if (B <= 0 || H <= 0 || C <= 0 || d <= 0)
+        return fail(ACP_EINVAL, "sizes must be positive (B=%d H=%d C=%d d=%d)", B, H, C, d);
+    if (dt != ACP_F32 && dt != ACP_BF16) return fail(ACP_EINVAL, "unknown dtype %d", (int)dt);
+    if (d != 64 && d != 128) return fail(ACP_EUNSUPPORTED, "head dim %d not in {64, 128}", d);
+    if (C % 64 != 0 || C > 64 * 2048)
+        return fail(ACP_EUNSUPPORTED, "cache size C=%d is not a multiple of 64 up to 131072", C);
+    if ((long long)B * H > 65535)
+        return fail(ACP_EUNSUPPORTED, "B*H=%lld exceeds 65535", (long long)B * H);
+    return ACP_OK;
+}
+
+static acp_status check_state(void* state, size_t state_bytes, const DecLayout& y) {
+    acp_status s = check_ptr(state, "state");
+    if (s != ACP_OK) return s;
+    if (state_bytes < y.total)
+        return fail(ACP_EWORKSPACE, "decoding state of %zu bytes, %zu needed", state_bytes,
+                    y.total);
+    return ACP_OK;
+}
+
+static acp_status check_lmax(int64_t L_max) {
+    if (L_max < 1 || L_max > ((int64_t)1 << 31))
+        return fail(ACP_EINVAL, "L_max=%lld outside [1, 2^31]", (long long)L_max);
+    return ACP_OK;
+}
+
+acp_status acp_decode_state_size(int B, int H, int C, int d, acp_dtype dt, size_t* bytes) {
+    ACP_TRY(check_dec_shape(B, H, C, d, dt));
+    if (bytes == nullptr) return fail(ACP_EINVAL, "bytes is NULL");
+    *bytes = dec_layout(B, H, C, d, dt).total;
+    return ok();
+}
+
+acp_status acp_decode_offsets(int B, int H, int C, int d, acp_dtype dt, acp_decode_layout* out) {
+    ACP_TRY(check_dec_shape(B, H, C, d, dt));
+    if (out == nullptr) return fail(ACP_EINVAL, "out is NULL");
+    const DecLayout y = dec_layout(B, H, C, d, dt);
+    out->k_cache = y.k;
+    out->v_cache = y.v;
+    out->c = y.c;
+    out->cum = y.cum;
+    out->delta = y.delta;
+    out->pointer = y.ptr;
+    out->flags = y.flags;
+    out->total = y.total;
+    return ok();
+}
+
+acp_status acp_decode_init(const void* K, const void* V, const float* log_f,
+                           const float* gamma_q, const float* gamma_k, acp_dtype dt, int B,
+                           int H, int L0, int C, int d, double eps, int64_t L_max, void* state,
+                           size_t state_bytes, void* stream) {
+    ACP_TRY(check_dec_shape(B, H, C, d, dt));
+    ACP_TRY(check_eps(eps));
+    ACP_TRY(check_lmax(L_max));
+    if (L0 <= 0 || L0 > 64 * 2048)
+        return fail(ACP_EUNSUPPORTED, "prompt length L0=%d outside [1, 131072]", L0);
+    if ((int64_t)L0 > L_max) return fail(ACP_EINVAL, "L0=%d exceeds L_max=%lld", L0, (long long)L_max);
+    ACP_TRY(check_ptr(K, "K"));
+    ACP_TRY(check_ptr(V, "V"));
+    ACP_TRY(check_ptr(log_f, "log_f"));
+    ACP_TRY(check_ptr(gamma_q, "gamma_q"));
+    ACP_TRY(check_ptr(gamma_k, "gamma_k"));
+    const DecLayout y = dec_layout(B, H, C, d, dt);
+    ACP_TRY(check_state(state, state_bytes, y));
+    char* w = (char*)state;
+    acp::DecodeInitArgs a{};
+    a.K = K; a.V = V; a.log_f = log_f; a.gamma_q = gamma_q; a.gamma_k = gamma_k;
+    a.bf16 = dt == ACP_BF16;
+    a.B = B; a.H = H; a.L0 = L0; a.C = C; a.d = d;
+    a.log_lmax_over_eps = eps == 0.0 ? INFINITY : std::log((double)L_max) - std::log(eps);
+    a.Kc = w + y.k; a.Vc = w + y.v; a.cc = (float*)(w + y.c);
+    a.cs = (double*)(w + y.cum); a.ptr = (int*)(w + y.ptr);
+    a.delta = (double*)(w + y.delta); a.flags = (int*)(w + y.flags);
+    return hip_status(acp::launch_decode_init(a, (hipStream_t)stream), "acp_decode_init launch");
+}
+
+acp_status fox_attn_decode(const void* q, const void* k, const void* v, const float* log_f,
+                           acp_dtype dt, int B, int H, int t, int C, int d, int64_t L_max,
+                           void* O, float* lse, void* state, size_t state_bytes, void* stream) {
+    ACP_TRY(check_dec_shape(B, H, C, d, dt));
+    ACP_TRY(check_lmax(L_max));
+    if (t < 1 || (int64_t)t >= L_max)
+        return fail(ACP_EINVAL, "position t=%d outside [1, L_max=%lld)", t, (long long)L_max);
+    ACP_TRY(check_ptr(q, "q"));
+    ACP_TRY(check_ptr(k, "k"));
+    ACP_TRY(check_ptr(v, "v"));
+    ACP_TRY(check_ptr(log_f, "log_f"));
+    ACP_TRY(check_ptr(O, "O"));
+    ACP_TRY(check_ptr(lse, "lse"));
+    const DecLayout y = dec_layout(B, H, C, d, dt);
+    ACP_TRY(check_state(state, state_bytes, y));
+    char* w = (char*)state;
+    acp::DecodeArgs a{};
+    a.q = q; a.k = k; a.v = v; a.log_f = log_f; a.bf16 = dt == ACP_BF16;
+    a.B = B; a.H = H; a.t = t; a.C = C; a.d = d;
+    a.Kc = w + y.k; a.Vc = w + y.v; a.cc = (float*)(w + y.c);
+    a.cs = (double*)(w + y.cum); a.ptr = (int*)(w + y.ptr);
+    a.delta = (const double*)(w + y.delta); a.flags = (int*)(w + y.flags);
+    a.part = (float*)(w + y.part);
+    a.O = O; a.lse = lse;
+    return hip_status(acp::launch_decode(a, (hipStream_t)stream), "fox_attn_decode launch");
 }
 
 const char* acp_status_string(acp_status s) {

@@ -64,6 +64,43 @@ struct BwdArgs {
     float* dlog_f;
 };
 
+struct DecodeInitArgs {
+    const void* K;            // [B*H, L0, d] prompt keys
+    const void* V;
+    const float* log_f;       // [B*H, L0]
+    const float* gamma_q;     // [H]
+    const float* gamma_k;     // [H]
+    bool bf16;
+    int B, H, L0, C, d;
+    double log_lmax_over_eps; // log L_max - log eps, +inf for eps = 0
+    void* Kc;                 // [B*H, C, d] ring caches, position j in slot j mod C
+    void* Vc;
+    float* cc;                // [B*H, C] c of the cached positions
+    double* cs;               // [B*H] float64 running sum of log f
+    int* ptr;                 // [B*H] first kept block of the latest query
+    double* delta;            // [B*H]
+    int* flags;               // [B*H]
+};
+
+struct DecodeArgs {
+    const void* q;            // [B*H, d] the new token
+    const void* k;
+    const void* v;
+    const float* log_f;       // [B*H]
+    bool bf16;
+    int B, H, t, C, d;        // t: position of the new token
+    void* Kc;
+    void* Vc;
+    float* cc;
+    double* cs;
+    int* ptr;
+    const double* delta;
+    int* flags;
+    float* part;              // [B*H, ceil(C / 256), d + 2] split partials
+    void* O;                  // [B*H, d]
+    float* lse;               // [B*H]
+};
+
 // Tracing hooks: no-ops unless acp_timing_enable(1) was called.
 void trace_begin(int kernel, hipStream_t s);
 void trace_end(int kernel, hipStream_t s);
@@ -74,5 +111,8 @@ hipError_t launch_fwd(const FwdArgs& a, hipStream_t s);
 hipError_t launch_bwd(const BwdArgs& a, hipStream_t s);
 hipError_t launch_dq_bf16(const BwdArgs& a, hipStream_t s);
 hipError_t launch_dkdv_bf16(const BwdArgs& a, hipStream_t s);
+size_t decode_partials_floats(int BH, int C, int d);
+hipError_t launch_decode_init(const DecodeInitArgs& a, hipStream_t s);
+hipError_t launch_decode(const DecodeArgs& a, hipStream_t s);
 
 }  // namespace acp

@@ -13,6 +13,7 @@
 // launch is skipped and the plan kernel takes U from the scales.
 #include "acp_device.h"
 #include "acp_internal.h"
+#include "acp_scan.h"
 
 namespace acp {
 
@@ -69,56 +70,6 @@ __global__ __launch_bounds__(kNormRows) void rownorm_max_kernel(
         for (int w = 1; w < kNormRows / 64; ++w) r = nan_max(r, wave_max[w]);
         part[((size_t)bh * 2 + which) * nchunk + chunk] = r;
     }
-}
-
-constexpr int kPlanThreads = 1024;
-constexpr int kPlanWaves = kPlanThreads / 64;
-
-// Inclusive prefix sum over the workgroup of one double per thread (any
-// association: the callers only add values whose float64 sums are exact).
-__device__ double block_inclusive_scan(double v, double* s_wave) {
-    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-        const double o = __shfl_up(v, off);
-        if (lane >= off) v += o;
-    }
-    if (lane == 63) s_wave[wid] = v;
-    __syncthreads();
-    if (wid == 0) {
-        double w = lane < kPlanWaves ? s_wave[lane] : 0.0;
-#pragma unroll
-        for (int off = 1; off < kPlanWaves; off <<= 1) {
-            const double o = __shfl_up(w, off);
-            if (lane >= off) w += o;
-        }
-        if (lane < kPlanWaves) s_wave[lane] = w;   // inclusive wave totals
-    }
-    __syncthreads();
-    const double before = wid > 0 ? s_wave[wid - 1] : 0.0;
-    const double out = v + before;
-    __syncthreads();  // s_wave may be reused by the caller
-    return out;
-}
-
-template <typename V, typename Op>
-__device__ V block_reduce(V v, V* s_wave, Op op) {
-    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) v = op(v, __shfl_xor(v, off));
-    if (lane == 0) s_wave[wid] = v;
-    __syncthreads();
-    V r = s_wave[0];
-    for (int w = 1; w < kPlanWaves; ++w) r = op(r, s_wave[w]);
-    __syncthreads();
-    return r;
-}
-
-// Position of the last bit of a float32 value: it is an integer multiple of
-// 2^lsb_exp(x).  Subnormals share the exponent of the smallest normal.
-__device__ __forceinline__ int lsb_exp(float x) {
-    const int biased = (int)((__float_as_uint(x) >> 23) & 0xff);
-    return (biased > 0 ? biased : 1) - 150;
 }
 
 __global__ __launch_bounds__(kPlanThreads) void plan_kernel(

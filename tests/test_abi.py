@@ -18,7 +18,9 @@ def test_every_declared_symbol_is_exported():
     names = acp.header_functions()
     assert set(names) == {"acp_workspace_size", "acp_plan_offsets", "acp_boundary",
                           "acp_boundary_qknorm", "fox_attn_fwd", "fox_attn_fwd_qknorm",
-                          "fox_attn_bwd", "acp_timing_enable", "acp_timing_reset",
+                          "fox_attn_bwd", "acp_decode_state_size", "acp_decode_offsets",
+                          "acp_decode_init", "fox_attn_decode",
+                          "acp_timing_enable", "acp_timing_reset",
                           "acp_timing_read", "acp_status_string", "acp_last_error"}
     lib = ctypes.CDLL(acp.LIB_PATH)
     for n in names:
@@ -134,3 +136,50 @@ def test_timing_state_without_launches():
     assert set(t) == set(acp.K_NAMES) and all(v == (0, 0.0) for v in t.values())
     acp.acp_timing_enable(True)
     acp.acp_timing_enable(False)
+
+
+def test_decode_state_layout():
+    n = acp.acp_decode_state_size(2, 3, 256, 64, acp.ACP_BF16)
+    lay = acp.acp_decode_offsets(2, 3, 256, 64, acp.ACP_BF16)
+    offs = [getattr(lay, f) for f, _ in acp.DecodeLayout._fields_]
+    assert all(o % 256 == 0 for o in offs) and offs == sorted(offs) and lay.total == n
+    assert lay.v_cache - lay.k_cache >= 2 * 3 * 256 * 64 * 2
+    assert acp.acp_decode_state_size(2, 3, 256, 64, acp.ACP_F32) > n
+    with pytest.raises(acp.AcpError):
+        acp.acp_decode_state_size(2, 3, 100, 64, acp.ACP_BF16)   # C not a multiple of 64
+
+
+def test_decode_entries_reject_before_launch():
+    big = 1 << 40
+    # init: K, V, log_f, gamma_q, gamma_k, dt, B, H, L0, C, d, eps, L_max, state, bytes, stream
+    st = acp.acp_decode_init(16, 16, 16, 16, 16, acp.ACP_BF16, 1, 1, 100, 128, 64, 0.5, 64, 16,
+                             big, None)
+    assert st == acp.ACP_EINVAL and "L_max" in acp.acp_last_error()        # L0 > L_max
+    st = acp.acp_decode_init(16, 16, 16, 0, 16, acp.ACP_BF16, 1, 1, 100, 128, 64, 0.5, 1000, 16,
+                             big, None)
+    assert st == acp.ACP_EINVAL and "gamma_q" in acp.acp_last_error()
+    st = acp.acp_decode_init(16, 16, 16, 16, 16, acp.ACP_BF16, 1, 1, 100, 96, 64, 0.5, 1000, 16,
+                             big, None)
+    assert st == acp.ACP_EUNSUPPORTED
+    st = acp.acp_decode_init(16, 16, 16, 16, 16, acp.ACP_BF16, 1, 1, 100, 128, 64, 1.0, 1000, 16,
+                             big, None)
+    assert st == acp.ACP_EINVAL and "eps" in acp.acp_last_error()
+    st = acp.acp_decode_init(16, 16, 16, 16, 16, acp.ACP_BF16, 1, 1, 100, 128, 64, 0.5, 1000, 16,
+                             8, None)
+    assert st == acp.ACP_EWORKSPACE
+    # step: q, k, v, log_f, dt, B, H, t, C, d, L_max, O, lse, state, bytes, stream
+    st = acp.fox_attn_decode(16, 16, 16, 16, acp.ACP_BF16, 1, 1, 1000, 128, 64, 1000, 16, 16, 16,
+                             big, None)
+    assert st == acp.ACP_EINVAL and "t=1000" in acp.acp_last_error()       # t >= L_max
+    st = acp.fox_attn_decode(16, 16, 16, 16, acp.ACP_BF16, 1, 1, 0, 128, 64, 1000, 16, 16, 16,
+                             big, None)
+    assert st == acp.ACP_EINVAL
+    st = acp.fox_attn_decode(16, 16, 16, 16, acp.ACP_BF16, 1, 1, 10, 128, 64, 1000, 16, 0, 16,
+                             big, None)
+    assert st == acp.ACP_EINVAL and "lse" in acp.acp_last_error()
+    st = acp.fox_attn_decode(16, 16, 24, 16, acp.ACP_BF16, 1, 1, 10, 128, 64, 1000, 16, 16, 16,
+                             big, None)
+    assert st == acp.ACP_EINVAL and "aligned" in acp.acp_last_error()
+    st = acp.fox_attn_decode(16, 16, 16, 16, acp.ACP_BF16, 1, 1, 10, 128, 64, 1000, 16, 16, 16,
+                             8, None)
+    assert st == acp.ACP_EWORKSPACE
