@@ -5,7 +5,10 @@ fox_attn_bwd on the 125M-shaped layer (B=8, H=12, L=4096, d=64, bf16), with
 all inputs already in HBM.  Prints one JSON line.
 
     python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--workload 125m]
-                    [--no-cpu-baseline] [--extra]
+                    [--no-cpu-baseline] [--no-decode] [--extra]
+
+The line also carries a decoding measurement (fox_attn_decode after a 4096-token
+prompt on the same layer shape) unless --no-decode is given.
 """
 from __future__ import annotations
 
@@ -121,6 +124,69 @@ def run_workload(name, steps: int, warmup: int, eps_override=None, unpruned=True
             "per_kernel_ms": per_kernel, "x": x}
 
 
+def run_decode(steps: int = 64, warmup: int = 16, L0: int = 4096, C: int = 8192):
+    """Decoding on the 125M-shaped layer (B=8, H=12, d=64, bf16, QK-normed q/k):
+    a 4096-token prompt, then single-token steps with ACP (eps = e^-10, threshold
+    sized for L_max = C) and with eps = 0.  After `warmup` eager steps, `steps`
+    eager steps give the wall time per call (host side included), then `steps`
+    more are captured in a HIP graph and replayed once: the replay time per step
+    is the GPU time of the step's two kernels without the host's launch latency."""
+    import torch
+    from paper_2504_06949_amd import acp, workloads
+
+    w0 = workloads.WORKLOADS["125m"]
+    n_tok = warmup + 2 * steps
+    L = L0 + 64 * ((n_tok + 63) // 64)
+    w = workloads.custom("125m_decode", w0.B, w0.H, L, w0.d, "bf16", w0.seed, qk_norm=True)
+    x = workloads.generate(w, with_grad=False)
+    dev = torch.device("cuda:0")
+    g = {n: x[n].to(dev) for n in ("q", "k", "v", "log_f", "gamma_q", "gamma_k")}
+    prompt = {n: g[n][:, :, :L0].contiguous() for n in ("k", "v", "log_f")}
+    toks = [{n: g[n][:, :, t].contiguous() for n in ("q", "k", "v", "log_f")}
+            for t in range(L0, L0 + n_tok)]
+    out = {"workload": f"B={w.B} H={w.H} d={w.d} bf16, prompt {L0}, ring C={C}, L_max={C}, "
+                       f"{steps} eager + {steps} graph-replayed steps after {warmup}"}
+    o = torch.empty((w.B, w.H, w.d), dtype=torch.bfloat16, device=dev)
+    lse = torch.empty((w.B, w.H), dtype=torch.float32, device=dev)
+    row_bytes = 2 * w.d * 2 + 4                      # k and v rows plus c, per key
+    for label, eps in (("acp", w.eps), ("unpruned", 0.0)):
+        dec = acp.Decoder(w.B, w.H, C, w.d, dtype=torch.bfloat16, device=dev)
+        dec.init(prompt["k"], prompt["v"], prompt["log_f"], g["gamma_q"], g["gamma_k"], eps, C)
+        for tk in toks[:warmup]:
+            dec.step(tk["q"], tk["k"], tk["v"], tk["log_f"], out=(o, lse))
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for tk in toks[warmup:warmup + steps]:
+            dec.step(tk["q"], tk["k"], tk["v"], tk["log_f"], out=(o, lse))
+        torch.cuda.synchronize()
+        wall = (time.perf_counter() - t0) / steps
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            for tk in toks[warmup + steps:]:
+                dec.step(tk["q"], tk["k"], tk["v"], tk["log_f"], out=(o, lse))
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        graph.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        gpu_us = e0.elapsed_time(e1) * 1e3 / steps
+        t_last = dec.t - 1
+        ptr = dec.current_pointer().long().cpu()
+        lo = torch.clamp(64 * ptr, min=t_last - C + 1)
+        keys = int((t_last - lo + 1).sum())
+        nbytes = keys * row_bytes
+        out[label] = {"step_us": round(gpu_us, 2), "wall_us_per_step": round(wall * 1e6, 1),
+                      "keys_read": keys, "bytes_read": nbytes,
+                      "hbm_gbps": round(nbytes / (gpu_us * 1e-6) / 1e9, 1),
+                      "hbm_frac": round(nbytes / (gpu_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4),
+                      "flags_or": int(dec.views()["flags"].max().item())}
+        del graph, dec
+    out["speedup_vs_unpruned"] = round(out["unpruned"]["step_us"] / out["acp"]["step_us"], 3)
+    out["kv_reads_pruned_fraction"] = round(1 - out["acp"]["keys_read"] / out["unpruned"]["keys_read"], 4)
+    return out
+
+
 def cpu_baseline(res, budget_s: float = 15.0):
     """The oracle, untuned, on whole heads of the same workload until the budget is spent."""
     import numpy as np
@@ -158,6 +224,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="125m")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-decode", action="store_true",
+                    help="skip the decoding measurement (125M-shaped, 4096-token prompt)")
     ap.add_argument("--skip-unpruned", action="store_true",
                     help="do not time the eps = 0 (nothing pruned) reference run")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
@@ -246,6 +314,8 @@ def main():
                                 "boundary_share": round((rpk["rownorm"] + rpk["plan"]) / r["ms"], 4),
                                 "per_kernel_ms": {k: round(v, 4) for k, v in rpk.items()}}
         out["other_workloads"] = extra
+    if not args.no_decode:
+        out["decode"] = run_decode()
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(res)
     print(json.dumps(out), flush=True)

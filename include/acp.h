@@ -192,9 +192,11 @@ typedef struct {
     size_t k_cache;    /* [B,H,C,d] dt     keys, position j in slot j mod C          */
     size_t v_cache;    /* [B,H,C,d] dt     values                                    */
     size_t c;          /* [B,H,C]   float  c_j of the cached positions               */
-    size_t cum;        /* [B,H]     double running float64 sum of log f so far       */
+    size_t cum;        /* [2,B,H]   double running float64 sum of log f; the value
+                                           after position p is in copy p mod 2          */
     size_t delta;      /* [B,H]     double delta                                     */
-    size_t pointer;    /* [B,H]     int32  first kept key block of the latest query  */
+    size_t pointer;    /* [2,B,H]   int32  first kept key block of query p, in copy
+                                           p mod 2                                      */
     size_t flags;      /* [B,H]     int32  data-error bits                           */
     size_t total;      /* bytes = acp_decode_state_size()                            */
 } acp_decode_layout;

@@ -387,9 +387,9 @@ static DecLayout dec_layout(int B, int H, int C, int d, acp_dtype dt) {
     y.k = take(BH * C * d * es);
     y.v = take(BH * C * d * es);
     y.c = take(BH * C * 4);
-    y.cum = take(BH * 8);
+    y.cum = take(2 * BH * 8);
     y.delta = take(BH * 8);
-    y.ptr = take(BH * 4);
+    y.ptr = take(2 * BH * 4);
     y.flags = take(BH * 4);
     y.part = take(acp::decode_partials_floats((int)BH, C, d) * 4);
     y.total = off;

@@ -9,12 +9,22 @@
 // slot j mod C), so its memory is what the kept window needs, not the context.
 //
 // Kernels:
-//   decode_init_kernel    prompt of L0 tokens -> delta, the float64 running
-//                         cumsum, c of the prompt's last C positions, the
-//                         pointer of query L0 - 1, and its K/V rows in the ring
-//   decode_append_kernel  one token: cumsum, c_t, pointer advance, K/V append
-//   decode_attn_kernel    query t over its kept keys, 256 keys per workgroup
-//   decode_combine_kernel the workgroups' partial softmax sums merged
+//   decode_init_kernel  prompt of L0 tokens -> delta, the float64 running cumsum,
+//                       c of the prompt's last C positions, the pointer of query
+//                       L0 - 1, and its K/V rows in the ring
+//   decode_step_kernel  one token: c_t, the pointer advance, query t over its
+//                       kept keys (256 per workgroup, partial softmax sums), and
+//                       the append of k_t, v_t
+//   decode_combine_kernel  the partial sums of each head merged into O and lse
+//                       (a second launch: its start orders every workgroup's
+//                       partials before it without a device-wide fence, which
+//                       would write back a whole L2 per workgroup)
+//
+// The running sum and the pointer are kept twice, the values after position p
+// in copy p mod 2: every workgroup of step t reads copy (t - 1) mod 2 while the
+// first one writes copy t mod 2, so no workgroup sees a half-updated state.
+// The ring slot that token t takes over held position t - C, which no query from
+// t on attends to; the workgroups read k_t and v_t from the inputs, not the ring.
 #include "acp_device.h"
 #include "acp_internal.h"
 #include "acp_scan.h"
@@ -27,6 +37,9 @@ size_t decode_partials_floats(int BH, int C, int d) {
     const int nsplit = (C + kDecChunk - 1) / kDecChunk;
     return (size_t)BH * nsplit * (d + 2);
 }
+
+// ring slot of position j (j >= 0)
+__device__ __forceinline__ int ring(int j, int C) { return j % C; }
 
 // ---------------------------------------------------------------------------
 template <typename T, int D>
@@ -91,7 +104,7 @@ __global__ __launch_bounds__(kPlanThreads) void decode_init_kernel(
         if (i >= L0 - C) cc[(size_t)bh * C + (i % C)] = cf;
         if ((i & (kBlock - 1)) == kBlock - 1) s_last[i / kBlock] = cf;
         if (i == L0 - 1) {
-            cs_out[bh] = run;
+            cs_out[(size_t)((L0 - 1) & 1) * gridDim.x + bh] = run;
             s_ct = cf;
         }
     }
@@ -111,7 +124,7 @@ __global__ __launch_bounds__(kPlanThreads) void decode_init_kernel(
         // and the pointer does not go below the block of the oldest position held.
         const int first = L0 - C;
         if (kBlock * lo < first) flags |= 16;
-        ptr_out[bh] = max(lo, first > 0 ? first / kBlock : 0);
+        ptr_out[(size_t)((L0 - 1) & 1) * gridDim.x + bh] = max(lo, first > 0 ? first / kBlock : 0);
         flags_out[bh] = flags;
     }
 
@@ -130,186 +143,322 @@ __global__ __launch_bounds__(kPlanThreads) void decode_init_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// Token t of every (batch, head): one workgroup of 64 threads.
+// Token t of every (batch, head); grid (nsplit, B*H), nsplit workgroups of 256
+// threads per head, enough to cover min(t + 1, C) keys.
+//   1. The previous pointer p fixes the key range [j_base, t], j_base =
+//      max(64 p, t - C + 1); workgroup s takes keys j_base + 256 s .. + 255,
+//      wave w of it the 64 from 64 w.  Rows are read whole by groups of G lanes
+//      (16 bytes each); the K rows, the V rows (held in registers when they fit)
+//      and the c of the keys are requested together.
+//   2. Meanwhile every wave forms c_t = float32(cum + log f_t) and finds the new
+//      pointer n, the first kept block from max(p, block of position t - C + 1)
+//      on, 64 blocks per ballot; keys below max(64 n, t - C + 1) are masked.
+//   3. Softmax over the workgroup's keys and P V; the workgroup writes (max, sum,
+//      unnormalised O) with logits in log2 units, or max = -inf if it kept none.
+//   4. Workgroup 0 writes the state of position t: cum, pointer, flags, c_t, and
+//      k_t, v_t in slot t mod C.
 template <typename T, int D>
-__global__ __launch_bounds__(64) void decode_append_kernel(
-    const T* __restrict__ k, const T* __restrict__ v, const float* __restrict__ log_f, int t,
-    int C, T* __restrict__ Kc, T* __restrict__ Vc, float* __restrict__ cc,
-    double* __restrict__ cs, int* __restrict__ ptr, const double* __restrict__ delta,
-    int* __restrict__ flags) {
-    const int bh = blockIdx.x, lane = threadIdx.x;
-    const int slot = t % C;
-    if (lane == 0) {
-        int fl = flags[bh];
-        const float lff = log_f[bh];
-        if (!__builtin_isfinite(lff)) fl |= 2;
-        else if (lff > 0.0f) fl |= 1;
-        const double old = cs[bh], lf = (double)lff;
-        const double s2 = old + lf;
-        // the running sum stays the exact prefix sum only while no addition rounds
-        const double bb = s2 - old;
-        if ((old - (s2 - bb)) + (lf - bb) != 0.0) fl |= 4;
-        const float ct = (float)s2;
-        const double dl = delta[bh];
-        const float* crow = cc + (size_t)bh * C;
-        // Before slot t mod C is overwritten the ring holds positions t - C .. t - 1.
-        // A kept key is lost iff the block of position t - C is kept (the blocks
-        // before it are then kept too); its last key is one of those positions.
-        const int nb = t / kBlock, gone = t - C;
-        if (gone >= 0) {
-            const int nx = gone / kBlock;
-            if ((double)ct - (double)crow[(kBlock * nx + kBlock - 1) % C] >= dl) fl |= 16;
-        }
-        // advance from the old pointer, or from the block of the oldest position
-        // still held after the append, to the first kept block
-        int n = max(ptr[bh], gone + 1 > 0 ? (gone + 1) / kBlock : 0);
-        while (n < nb && (double)ct - (double)crow[(kBlock * n + kBlock - 1) % C] < dl) ++n;
-        ptr[bh] = n;
-        cs[bh] = s2;
-        cc[(size_t)bh * C + slot] = ct;
-        flags[bh] = fl;
-    }
-    constexpr int kVec = 16 / (int)sizeof(T);
-    for (int e = lane * kVec; e < D; e += 64 * kVec) {
-        const size_t dst = ((size_t)bh * C + slot) * D + e;
-        *reinterpret_cast<uint4*>(Kc + dst) = *reinterpret_cast<const uint4*>(k + (size_t)bh * D + e);
-        *reinterpret_cast<uint4*>(Vc + dst) = *reinterpret_cast<const uint4*>(v + (size_t)bh * D + e);
-    }
-}
-
-// ---------------------------------------------------------------------------
-// Query t over keys [j_lo, t], j_lo = max(64 ptr, t - C + 1): workgroup s takes
-// keys j_lo + 256 s .. + 255, wave w of it the 64 keys from 64 w.  Rows are read
-// whole by groups of G lanes (16 bytes each), so every load instruction covers
-// 64 / G consecutive cache rows.  Writes the workgroup's (max, sum, unnormalised
-// O) with logits in log2 units.
-template <typename T, int D>
-__global__ __launch_bounds__(kDecChunk) void decode_attn_kernel(
-    const T* __restrict__ q, const T* __restrict__ Kc, const T* __restrict__ Vc,
-    const float* __restrict__ cc, const int* __restrict__ ptr, int t, int C, int nsplit,
-    float kscale, float* __restrict__ part) {
+__global__ __launch_bounds__(kDecChunk) void decode_step_kernel(
+    const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
+    const float* __restrict__ log_f, int t, int C, T* __restrict__ Kc, T* __restrict__ Vc,
+    float* __restrict__ cc, double* __restrict__ cum, int* __restrict__ ptr,
+    const double* __restrict__ delta, int* __restrict__ flags, float* __restrict__ part,
+    float kscale) {
     constexpr int kVec = 16 / (int)sizeof(T);   // elements per 16-byte piece
     constexpr int G = D / kVec;                 // lanes per cache row
     constexpr int kRows = 64 / G;               // rows per wave load
     constexpr int kIter = 64 / kRows;           // loads per wave for its 64 rows
     constexpr int kWaves = kDecChunk / 64;
+    constexpr bool kHoldV = kIter <= 8;         // V rows requested with the K rows
+    constexpr int kHeld = kHoldV ? kIter : 1;
     __shared__ float x_s[kDecChunk];
     __shared__ float red[kWaves][D];
     __shared__ float s_red[kWaves];
 
-    const int bh = blockIdx.y, sp = blockIdx.x, tid = threadIdx.x;
-    const int lane = tid & 63, wid = tid >> 6;
-    const int j_lo = max(kBlock * ptr[bh], t - C + 1);
-    const int j0 = j_lo + sp * kDecChunk;
-    float* out = part + ((size_t)bh * nsplit + sp) * (D + 2);
-    if (j0 > t) {                                // past this query's window
-        if (tid < D) out[2 + tid] = 0.f;
-        if (tid == 0) { out[0] = -INFINITY; out[1] = 0.f; }
+    const int bh = blockIdx.y, sp = blockIdx.x, nsplit = gridDim.x, BH = gridDim.y;
+    const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+    const size_t head = (size_t)bh * C;
+    const float* crow = cc + head;
+    float* pml = part + (size_t)bh * nsplit * 2;                            // [nsplit][2]
+    float* po = part + (size_t)BH * nsplit * 2 + (size_t)bh * nsplit * D;   // [nsplit][D]
+
+    const int rd = (t - 1) & 1;
+    const int nb = t / kBlock, gone = t - C;
+    const int first = gone + 1 > 0 ? gone + 1 : 0;          // oldest position held
+    // (clamped to [0, nb], so that even a corrupted state indexes inside the ring)
+    const int p_old = min(max(ptr[(size_t)rd * BH + bh], 0), nb);
+    const double cs_old = cum[(size_t)rd * BH + bh];
+    const float lff = log_f[bh];
+    const double dl = delta[bh];
+    const int e0 = (lane % G) * kVec;
+    const uint4 qraw = *reinterpret_cast<const uint4*>(q + (size_t)bh * D + e0);
+
+    const int j0 = max(kBlock * p_old, first) + sp * kDecChunk;
+    if (j0 > t) {                             // past the window (never workgroup 0)
+        if (tid == 0) {
+            pml[2 * sp] = -INFINITY;          // weight 0 in the merge
+            pml[2 * sp + 1] = 0.f;
+        }
         return;
     }
-    const int nk = min(kDecChunk, t - j0 + 1);
-    const size_t head = (size_t)bh * C;
-    const int e0 = (lane % G) * kVec;
-    float qv[kVec];
-    {
-        const uint4 raw = *reinterpret_cast<const uint4*>(q + (size_t)bh * D + e0);
-        const T* ev = reinterpret_cast<const T*>(&raw);
-#pragma unroll
-        for (int i = 0; i < kVec; ++i) qv[i] = to_f32(ev[i]);
-    }
+    const int nk = min(kDecChunk, t - j0 + 1);                // keys in this chunk
 
-    // q . k_j for the wave's rows, reduced over the G lanes of each row
+    // c at the last key of blocks n_start .. n_start + 63 for the pointer search,
+    // requested first so that it returns before the rows (loads complete in order)
+    const int n_start = max(p_old, first / kBlock);
+    // (with nb = 0 every lane is kept anyway; slot 63 is read only to stay branch-free)
+    float cb = crow[ring(kBlock * min(n_start + lane, max(nb - 1, 0)) + kBlock - 1, C)];
+
+    // ---- 1. requests for the chunk's rows ----------------------------------------
+    // Slot of key j0 + kk: at most one wrap, since kk < nk <= C.  Lanes past the
+    // chunk load its last row again (branch-free and in bounds) and are masked.
+    const int s0 = ring(j0, C);
+    auto slot = [&](int kk) {
+        const int sl = s0 + kk;
+        return sl >= C ? sl - C : sl;
+    };
+    const int kk_max = nk - 1;
+    uint4 kraw[kIter];
+    uint4 vraw[kHeld];
 #pragma unroll
     for (int it = 0; it < kIter; ++it) {
-        const int kk = 64 * wid + kRows * it + lane / G;
-        float dot = 0.f;
-        if (kk < nk) {
-            const int j = j0 + kk;
-            const uint4 raw = *reinterpret_cast<const uint4*>(Kc + (head + j % C) * D + e0);
-            const T* ev = reinterpret_cast<const T*>(&raw);
+        const int kk = min(64 * wid + kRows * it + lane / G, kk_max);
+        const bool last = j0 + kk == t;      // k_t, v_t come from the inputs
+        const size_t row = (head + slot(kk)) * D + e0;
+        const T* kr = last ? k + (size_t)bh * D + e0 : Kc + row;
+        kraw[it] = *reinterpret_cast<const uint4*>(kr);
+        if constexpr (kHoldV) {
+            const T* vr = last ? v + (size_t)bh * D + e0 : Vc + row;
+            vraw[it] = *reinterpret_cast<const uint4*>(vr);
+        }
+    }
+    float cj = crow[slot(min(tid, kk_max))];
+    // all requests above are issued before anything waits for the first of them
+    asm volatile("" : "+v"(cb) : : "memory");
+
+    // ---- 2. c_t and the new pointer --------------------------------------------------
+    const double s2 = cs_old + (double)lff;
+    const float ct = (float)s2;
+    // blocks n .. n + 63 per ballot; the block holding t (n >= nb) is always kept
+    int n = n_start;
+    unsigned long long bal = __ballot(n + lane >= nb || (double)ct - (double)cb >= dl);
+    while (bal == 0ull) {                     // a jump of more than 64 blocks (rare)
+        n += 64;
+        const float c2 = crow[ring(kBlock * min(n + lane, nb - 1) + kBlock - 1, C)];
+        bal = __ballot(n + lane >= nb || (double)ct - (double)c2 >= dl);
+    }
+    n += __builtin_ctzll(bal);
+    // The rows stay opaque until here, so that the compiler neither waits for them
+    // before the search nor unpacks them early into twice the registers.
+#pragma unroll
+    for (int it = 0; it < kIter; ++it)
+        asm volatile("" : "+v"(kraw[it].x), "+v"(kraw[it].y), "+v"(kraw[it].z), "+v"(kraw[it].w));
+    if constexpr (kHoldV) {
+#pragma unroll
+        for (int it = 0; it < kHeld; ++it)
+            asm volatile("" : "+v"(vraw[it].x), "+v"(vraw[it].y), "+v"(vraw[it].z), "+v"(vraw[it].w));
+    }
+    const int j_lo = max(kBlock * n, first);
+    // this chunk's kept keys: kk in [kk_lo, nk)
+    const int kk_lo = min(max(j_lo - j0, 0), nk);
+
+    // ---- 3. softmax and P V ------------------------------------------------------------
+    if (kk_lo < nk) {
+        float qv[kVec];
+        {
+            const T* ev = reinterpret_cast<const T*>(&qraw);
+#pragma unroll
+            for (int i = 0; i < kVec; ++i) qv[i] = to_f32(ev[i]);
+        }
+#pragma unroll
+        for (int it = 0; it < kIter; ++it) {
+            const int kk = 64 * wid + kRows * it + lane / G;
+            const T* ev = reinterpret_cast<const T*>(&kraw[it]);
+            float dot = 0.f;
 #pragma unroll
             for (int i = 0; i < kVec; ++i) dot = __builtin_fmaf(qv[i], to_f32(ev[i]), dot);
+#pragma unroll
+            for (int off = 1; off < G; off <<= 1) dot += __shfl_xor(dot, off);
+            if (lane % G == 0 && kk < nk) x_s[kk] = dot;
+        }
+        __syncthreads();
+
+        float x = -INFINITY;
+        if (tid >= kk_lo && tid < nk) {
+            if (j0 + tid == t) cj = ct;         // the ring's slot still holds t - C
+            x = __builtin_fmaf(x_s[tid], kscale, (ct - cj) * kLog2e);
+        }
+        float m = x;
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
+        if (lane == 0) s_red[wid] = m;
+        __syncthreads();
+        m = s_red[0];
+#pragma unroll
+        for (int w = 1; w < kWaves; ++w) m = fmaxf(m, s_red[w]);
+        __syncthreads();
+        const float p = (tid >= kk_lo && tid < nk) ? fast_exp2(x - m) : 0.f;
+        float l = p;
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) l += __shfl_xor(l, off);
+        if (lane == 0) s_red[wid] = l;
+        x_s[tid] = p;
+        __syncthreads();
+        l = s_red[0];
+#pragma unroll
+        for (int w = 1; w < kWaves; ++w) l += s_red[w];
+
+        float acc[kVec];
+#pragma unroll
+        for (int i = 0; i < kVec; ++i) acc[i] = 0.f;
+#pragma unroll
+        for (int it = 0; it < kIter; ++it) {
+            const int kk = 64 * wid + kRows * it + lane / G;
+            if (kk >= kk_lo && kk < nk) {
+                const float pj = x_s[kk];
+                uint4 raw;
+                if constexpr (kHoldV) {
+                    raw = vraw[it];
+                } else {
+                    const T* vr = j0 + kk == t ? v + (size_t)bh * D + e0
+                                               : Vc + (head + slot(kk)) * D + e0;
+                    raw = *reinterpret_cast<const uint4*>(vr);
+                }
+                const T* ev = reinterpret_cast<const T*>(&raw);
+#pragma unroll
+                for (int i = 0; i < kVec; ++i) acc[i] = __builtin_fmaf(pj, to_f32(ev[i]), acc[i]);
+            }
         }
 #pragma unroll
-        for (int off = 1; off < G; off <<= 1) dot += __shfl_xor(dot, off);
-        if (lane % G == 0 && kk < nk) x_s[kk] = dot;
+        for (int off = G; off < 64; off <<= 1)
+#pragma unroll
+            for (int i = 0; i < kVec; ++i) acc[i] += __shfl_xor(acc[i], off);
+        if (lane < G)
+#pragma unroll
+            for (int i = 0; i < kVec; ++i) red[wid][e0 + i] = acc[i];
+        __syncthreads();
+        if (tid < D) {
+            float o = red[0][tid];
+#pragma unroll
+            for (int w = 1; w < kWaves; ++w) o += red[w][tid];
+            po[(size_t)sp * D + tid] = o;
+        }
+        if (tid == 0) {
+            pml[2 * sp] = m;
+            pml[2 * sp + 1] = l;
+        }
+    } else if (tid == 0) {
+        pml[2 * sp] = -INFINITY;              // no kept key here: weight 0 in the merge
+        pml[2 * sp + 1] = 0.f;
     }
-    const float ct = cc[head + t % C];
-    __syncthreads();
 
-    float x = -INFINITY;
-    if (tid < nk)
-        x = __builtin_fmaf(x_s[tid], kscale, (ct - cc[head + (j0 + tid) % C]) * kLog2e);
-    float m = x;
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
-    if (lane == 0) s_red[wid] = m;
-    __syncthreads();
-    m = s_red[0];
-#pragma unroll
-    for (int w = 1; w < kWaves; ++w) m = fmaxf(m, s_red[w]);
-    __syncthreads();
-    const float p = tid < nk ? fast_exp2(x - m) : 0.f;
-    float l = p;
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) l += __shfl_xor(l, off);
-    if (lane == 0) s_red[wid] = l;
-    x_s[tid] = p;
-    __syncthreads();
-    l = s_red[0];
-#pragma unroll
-    for (int w = 1; w < kWaves; ++w) l += s_red[w];
-
-    // P V over the same rows, then over the lanes that hold the same columns
-    float acc[kVec];
-#pragma unroll
-    for (int i = 0; i < kVec; ++i) acc[i] = 0.f;
-#pragma unroll
-    for (int it = 0; it < kIter; ++it) {
-        const int kk = 64 * wid + kRows * it + lane / G;
-        if (kk < nk) {
-            const int j = j0 + kk;
-            const float pj = x_s[kk];
-            const uint4 raw = *reinterpret_cast<const uint4*>(Vc + (head + j % C) * D + e0);
-            const T* ev = reinterpret_cast<const T*>(&raw);
-#pragma unroll
-            for (int i = 0; i < kVec; ++i) acc[i] = __builtin_fmaf(pj, to_f32(ev[i]), acc[i]);
+    // ---- 4. the state of position t ---------------------------------------------------
+    if (sp == 0) {
+        if (tid == 0) {
+            int fl = flags[bh];
+            if (!__builtin_isfinite(lff)) fl |= 2;
+            else if (lff > 0.0f) fl |= 1;
+            // the running sum stays the exact prefix sum only while no addition rounds
+            const double bb = s2 - cs_old;
+            if ((cs_old - (s2 - bb)) + ((double)lff - bb) != 0.0) fl |= 4;
+            // A kept key is lost iff the block of position t - C is kept (the blocks
+            // before it are then kept too); its last key is still in the ring.
+            if (gone >= 0) {
+                const int nx = gone / kBlock;
+                if ((double)ct - (double)crow[ring(kBlock * nx + kBlock - 1, C)] >= dl) fl |= 16;
+            }
+            flags[bh] = fl;
+            cum[(size_t)(t & 1) * BH + bh] = s2;
+            ptr[(size_t)(t & 1) * BH + bh] = n;
+            cc[head + ring(t, C)] = ct;
+        }
+        for (int e = tid * kVec; e < D; e += kDecChunk * kVec) {
+            const size_t dst = (head + ring(t, C)) * D + e;
+            *reinterpret_cast<uint4*>(Kc + dst) = *reinterpret_cast<const uint4*>(k + (size_t)bh * D + e);
+            *reinterpret_cast<uint4*>(Vc + dst) = *reinterpret_cast<const uint4*>(v + (size_t)bh * D + e);
         }
     }
-#pragma unroll
-    for (int off = G; off < 64; off <<= 1)
-#pragma unroll
-        for (int i = 0; i < kVec; ++i) acc[i] += __shfl_xor(acc[i], off);
-    if (lane < G)
-#pragma unroll
-        for (int i = 0; i < kVec; ++i) red[wid][e0 + i] = acc[i];
-    __syncthreads();
-    if (tid < D) {
-        float o = red[0][tid];
-#pragma unroll
-        for (int w = 1; w < kWaves; ++w) o += red[w][tid];
-        out[2 + tid] = o;
-    }
-    if (tid == 0) { out[0] = m; out[1] = l; }
 }
 
 // ---------------------------------------------------------------------------
+// The partial sums of one head merged into O and lse: one workgroup of 256
+// threads per head.  Thread i requests dim i mod D of splits i / D, i / D + 256 / D,
+// ... (up to kHeld of them) and the (max, sum) of split i before it waits.
 template <typename T, int D>
-__global__ __launch_bounds__(D) void decode_combine_kernel(
-    const float* __restrict__ part, int nsplit, T* __restrict__ O, float* __restrict__ lse) {
-    const int bh = blockIdx.x, tid = threadIdx.x;
-    const float* P = part + (size_t)bh * nsplit * (D + 2);
-    float M = -INFINITY;
-    for (int s = 0; s < nsplit; ++s) M = fmaxf(M, P[(size_t)s * (D + 2)]);
-    float l = 0.f, o = 0.f;
-    for (int s = 0; s < nsplit; ++s) {
-        const float* ps = P + (size_t)s * (D + 2);
-        const float w = fast_exp2(ps[0] - M);          // 0 for workgroups past the window
-        l = __builtin_fmaf(w, ps[1], l);
-        o = __builtin_fmaf(w, ps[2 + tid], o);
+__global__ __launch_bounds__(kDecChunk) void decode_combine_kernel(
+    int nsplit, const float* __restrict__ part, T* __restrict__ O, float* __restrict__ lse) {
+    constexpr int kWaves = kDecChunk / 64;
+    constexpr int kGroups = kDecChunk / D;
+    constexpr int kMaxSplit = 64 * 2048 / kDecChunk;
+    constexpr int kHeld = 8;
+    __shared__ float w_s[kMaxSplit];
+    __shared__ float o_s[kDecChunk];
+    __shared__ float s_m[kWaves], s_l[kWaves];
+    const int bh = blockIdx.x, BH = gridDim.x, tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+    const float* pml = part + (size_t)bh * nsplit * 2;
+    const float* po = part + (size_t)BH * nsplit * 2 + (size_t)bh * nsplit * D;
+    const int dim = tid % D, grp = tid / D;
+
+    const int sm = min(tid, nsplit - 1);
+    float ms = pml[2 * sm], ls = pml[2 * sm + 1];
+    float ov[kHeld];
+#pragma unroll
+    for (int r = 0; r < kHeld; ++r) ov[r] = po[(size_t)min(grp + kGroups * r, nsplit - 1) * D + dim];
+    if (tid >= nsplit) {
+        ms = -INFINITY;
+        ls = 0.f;
     }
-    O[(size_t)bh * D + tid] = from_f32<T>(o / l);
-    if (tid == 0) lse[bh] = (M + fast_log2(l)) * kLn2;
+    const float m0 = ms;
+    for (int s2 = tid + kDecChunk; s2 < nsplit; s2 += kDecChunk) {   // more than 256 splits
+        const float m2 = pml[2 * s2], l2 = pml[2 * s2 + 1];
+        const float mx = fmaxf(ms, m2);
+        if (mx != -INFINITY) {
+            ls = ls * fast_exp2(ms - mx) + l2 * fast_exp2(m2 - mx);
+            ms = mx;
+        }
+    }
+    float M = ms;
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) M = fmaxf(M, __shfl_xor(M, off));
+    if (lane == 0) s_m[wid] = M;
+    __syncthreads();
+    M = s_m[0];
+#pragma unroll
+    for (int w = 1; w < kWaves; ++w) M = fmaxf(M, s_m[w]);
+    float L = ms != -INFINITY ? ls * fast_exp2(ms - M) : 0.f;
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) L += __shfl_xor(L, off);
+    if (lane == 0) s_l[wid] = L;
+    if (tid < nsplit) w_s[tid] = fast_exp2(m0 - M);
+    for (int s2 = tid + kDecChunk; s2 < nsplit; s2 += kDecChunk) w_s[s2] = fast_exp2(pml[2 * s2] - M);
+    __syncthreads();
+    L = s_l[0];
+#pragma unroll
+    for (int w = 1; w < kWaves; ++w) L += s_l[w];
+    // splits without a kept key (weight 0) hold no O: selected away, not multiplied
+    float o = 0.f;
+#pragma unroll
+    for (int r = 0; r < kHeld; ++r) {
+        const int s2 = grp + kGroups * r;
+        if (s2 < nsplit) {
+            const float w = w_s[s2];
+            o += w != 0.f ? w * ov[r] : 0.f;
+        }
+    }
+    for (int s2 = grp + kGroups * kHeld; s2 < nsplit; s2 += kGroups) {
+        const float w = w_s[s2];
+        const float pv = po[(size_t)s2 * D + dim];
+        o += w != 0.f ? w * pv : 0.f;
+    }
+    o_s[tid] = o;
+    __syncthreads();
+    if (tid < D) {
+        float r = o_s[tid];
+#pragma unroll
+        for (int g2 = 1; g2 < kGroups; ++g2) r += o_s[g2 * D + tid];
+        O[(size_t)bh * D + tid] = from_f32<T>(r / L);
+    }
+    if (tid == 0) lse[bh] = (M + fast_log2(L)) * kLn2;
 }
 
 // ---------------------------------------------------------------------------
@@ -333,19 +482,15 @@ hipError_t launch_decode_init(const DecodeInitArgs& a, hipStream_t s) {
 
 template <typename T, int D>
 static hipError_t step_t(const DecodeArgs& a, hipStream_t s) {
-    const int BH = a.B * a.H;
     const int nsplit = (min(a.t + 1, a.C) + kDecChunk - 1) / kDecChunk;
-    hipLaunchKernelGGL((decode_append_kernel<T, D>), dim3(BH), dim3(64), 0, s,
-                       (const T*)a.k, (const T*)a.v, a.log_f, a.t, a.C, (T*)a.Kc, (T*)a.Vc, a.cc,
-                       a.cs, a.ptr, a.delta, a.flags);
+    hipLaunchKernelGGL((decode_step_kernel<T, D>), dim3(nsplit, a.B * a.H), dim3(kDecChunk), 0, s,
+                       (const T*)a.q, (const T*)a.k, (const T*)a.v, a.log_f, a.t, a.C, (T*)a.Kc,
+                       (T*)a.Vc, a.cc, a.cs, a.ptr, a.delta, a.flags, a.part,
+                       kLog2e / sqrtf((float)D));
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((decode_attn_kernel<T, D>), dim3(nsplit, BH), dim3(kDecChunk), 0, s,
-                       (const T*)a.q, (const T*)a.Kc, (const T*)a.Vc, a.cc, a.ptr, a.t, a.C,
-                       nsplit, kLog2e / sqrtf((float)D), a.part);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL((decode_combine_kernel<T, D>), dim3(BH), dim3(D), 0, s, a.part, nsplit,
-                       (T*)a.O, a.lse);
+    hipLaunchKernelGGL((decode_combine_kernel<T, D>), dim3(a.B * a.H), dim3(kDecChunk), 0, s,
+                       nsplit, a.part, (T*)a.O, a.lse);
     return hipGetLastError();
 }
 

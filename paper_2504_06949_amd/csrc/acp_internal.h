@@ -76,8 +76,9 @@ struct DecodeInitArgs {
     void* Kc;                 // [B*H, C, d] ring caches, position j in slot j mod C
     void* Vc;
     float* cc;                // [B*H, C] c of the cached positions
-    double* cs;               // [B*H] float64 running sum of log f
-    int* ptr;                 // [B*H] first kept block of the latest query
+    double* cs;               // [2][B*H] float64 running sum of log f (copy p mod 2
+                              // holds the value after position p)
+    int* ptr;                 // [2][B*H] first kept block of query p, likewise
     double* delta;            // [B*H]
     int* flags;               // [B*H]
 };
@@ -96,7 +97,8 @@ struct DecodeArgs {
     int* ptr;
     const double* delta;
     int* flags;
-    float* part;              // [B*H, ceil(C / 256), d + 2] split partials
+    float* part;              // split partials: [B*H, nsplit, 2] (max, sum), then
+                              // [B*H, nsplit, d] (unnormalised O)
     void* O;                  // [B*H, d]
     float* lse;               // [B*H]
 };

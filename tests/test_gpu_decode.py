@@ -36,19 +36,22 @@ def _run(w, L0, C, eps, L_max, poke=None):
     dec.init(g["k"][:, :, :L0].contiguous(), g["v"][:, :, :L0].contiguous(),
              g["log_f"][:, :, :L0].contiguous(), g["gamma_q"], g["gamma_k"], eps, L_max)
     vw = dec.views()
-    init = {n: vw[n].clone() for n in ("pointer", "flags", "delta")}
+    init = {n: vw[n].clone() for n in ("flags", "delta")}
+    init["pointer"] = dec.current_pointer().clone()
     steps = []
     for t in range(L0, w.L):
         lf = _token(g, "log_f", t)
         if poke is not None:
             poke(t, lf)
         o, lse = dec.step(_token(g, "q", t), _token(g, "k", t), _token(g, "v", t), lf)
-        steps.append((t, o, lse, vw["pointer"].clone(), vw["flags"].clone()))
+        steps.append((t, o, lse, dec.current_pointer().clone(), vw["flags"].clone()))
     torch.cuda.synchronize()
     steps = [(t, o.double().cpu().numpy(), lse.double().cpu().numpy(), p.cpu(), f.cpu())
              for t, o, lse, p, f in steps]
     init = {n: v.cpu() for n, v in init.items()}
-    return x, init, steps, {n: v.cpu() for n, v in vw.items()}
+    fin = {n: v.cpu() for n, v in vw.items()}
+    fin["cum_now"] = dec.current_cum().cpu()
+    return x, init, steps, fin
 
 
 def _check(w, L0, C, eps, L_max, expect_lost=None):
@@ -83,7 +86,7 @@ def _check(w, L0, C, eps, L_max, expect_lost=None):
             T = w.L
             for pos in range(max(0, T - C), T):
                 assert float(fin["c"][b, h, pos % C]) == float(c_ref[b, h, pos])
-            assert np.float32(float(fin["cum"][b, h])) == c_ref[b, h, T - 1]
+            assert np.float32(float(fin["cum_now"][b, h])) == c_ref[b, h, T - 1]
             kc = fin["k_cache"][b, h]
             pos = T - 1
             assert torch.equal(kc[pos % C], x["k"][b, h, pos])
@@ -128,3 +131,37 @@ def test_decode_flags_a_positive_gate():
     assert int(init["flags"].max()) == 0
     assert int(fin["flags"][0, 1]) & 1 and int(fin["flags"][0, 0]) == 0
     assert all(int(fl[0, 1]) & 1 == (1 if t >= 100 else 0) for t, _, _, _, fl in steps)
+
+
+def test_decode_steps_captured_in_a_graph_match_eager():
+    """Eight steps captured in a HIP graph: each replay (after an eager re-init of
+    the state in between) must give exactly the eager outputs and state."""
+    w = workloads.custom("dec", 2, 3, 320, 64, "bf16", 45, mu=(0.0, 1.0, 6.0), qk_norm=True)
+    x = workloads.generate(w, with_grad=False)
+    g = to_gpu(x)
+    L0, n = 290, 8
+    prompt = [g[n_][:, :, :L0].contiguous() for n_ in ("k", "v", "log_f")]
+    toks = [[_token(g, n_, t) for n_ in ("q", "k", "v", "log_f")] for t in range(L0, L0 + n)]
+    eager = acp.Decoder(w.B, w.H, 256, w.d).init(*prompt, g["gamma_q"], g["gamma_k"], EPS, 4096)
+    ref = [tuple(r.clone() for r in eager.step(*tk)) for tk in toks]
+    ref_ptr = eager.current_pointer().clone()
+
+    dec = acp.Decoder(w.B, w.H, 256, w.d).init(*prompt, g["gamma_q"], g["gamma_k"], EPS, 4096)
+    outs = [(torch.empty_like(o), torch.empty_like(l)) for o, l in ref]
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        for tk, buf in zip(toks, outs):
+            dec.step(*tk, out=buf)
+    for rep in range(3):
+        print(f"case: decode graph replay {rep}", flush=True)
+        dec.init(*prompt, g["gamma_q"], g["gamma_k"], EPS, 4096)   # eager work in between
+        torch.cuda.synchronize()
+        for buf in outs:
+            buf[0].fill_(float("nan"))
+        graph.replay()
+        torch.cuda.synchronize()
+        dec.t = L0 + n
+        for (o, l), (ro, rl) in zip(outs, ref):
+            assert torch.equal(o, ro) and torch.equal(l, rl), rep
+        assert torch.equal(dec.current_pointer(), ref_ptr)
