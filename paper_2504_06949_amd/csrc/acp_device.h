@@ -175,6 +175,13 @@ __device__ __forceinline__ void wait_vmcnt0() { __builtin_amdgcn_s_waitcnt(0x0F7
 // returned (before a barrier after which other waves overwrite what they read).
 __device__ __forceinline__ void wait_vmcnt0_lgkmcnt0() { __builtin_amdgcn_s_waitcnt(0x0070); }
 
+// Workgroup barrier that orders this workgroup's LDS accesses only: unlike
+// __syncthreads() it does not first wait for the wave's global stores to
+// complete (for kernels whose global outputs no other wave reads back).
+__device__ __forceinline__ void lds_barrier() {
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" : : : "memory");
+}
+
 // ---- workgroup -> (head, block) mapping ------------------------------------
 // Workgroups are dealt round-robin to the 8 XCDs (each with its own L2).  This
 // renumbering gives every XCD a contiguous range of logical ids, so the blocks

@@ -72,6 +72,19 @@ __global__ __launch_bounds__(kNormRows) void rownorm_max_kernel(
     }
 }
 
+// One workgroup of 1024 threads per (batch, head); each thread owns a contiguous
+// run of log f, read and written as float4s when the run length is a multiple of
+// 4 (at L = 4096 one float4 per thread, so every access is coalesced), and kept
+// in registers up to kPlanHeld values.  Three barriers in all, none of which
+// waits for global stores: one round through LDS carries the scan's wave totals
+// together with every reduction (|log f| sum, last-bit position, flags, norm
+// maxima), one publishes the block corners of c, one the first kept blocks.
+// U and delta are formed by every thread from the same LDS values, so they are
+// identical everywhere without another round.  Cross-lane traffic is kept low:
+// the gate flags go through wave ballots, and the norm maxima are reduced only
+// by the waves that hold partials.
+constexpr int kPlanHeld = 16;   // log f values a thread keeps in registers (L <= 16384)
+
 __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
     const float* __restrict__ log_f, const double* __restrict__ part, int nchunk,
     const float* __restrict__ gamma_q, const float* __restrict__ gamma_k, int H,
@@ -80,99 +93,182 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
     double* __restrict__ u_out, double* __restrict__ delta_out,
     int* __restrict__ row_start, int* __restrict__ col_end,
     long long* __restrict__ kept_out, int* __restrict__ flags_out) {
-    __shared__ double s_dbl[kPlanWaves];
-    __shared__ double s_dbl2[kPlanWaves];
-    __shared__ int s_int[kPlanWaves];
-    __shared__ long long s_ll[kPlanWaves];
+    __shared__ double s_sum[kPlanWaves], s_abs[kPlanWaves], s_mq[kPlanWaves], s_mk[kPlanWaves];
+    __shared__ int s_lsb[kPlanWaves], s_flg[kPlanWaves];
     __shared__ float s_first[kMaxBlocks];  // c at the first row of each block
     __shared__ float s_last[kMaxBlocks];   // c at the last row of each block
     __shared__ int s_rs[kMaxBlocks];
-    __shared__ double s_delta;
 
-    const int bh = blockIdx.x, t = threadIdx.x;
+    const int bh = blockIdx.x, t = threadIdx.x, lane = t & 63, wid = t >> 6;
     const int M = L / kBlock;
 
-    // ---- rho_q^2, rho_k^2 (maxima are order-free) -------------------------
-    int flags = 0;
-    if (gamma_q == nullptr) {
-        double mq = 0.0, mk = 0.0;
+    // ---- requests: this thread's run of log f and the norm partials -----------
+    const float* x = log_f + (size_t)bh * L;
+    float* cw = c_out + (size_t)bh * L;
+    const int per = (L + kPlanThreads - 1) / kPlanThreads;
+    const int beg = min(t * per, L), n = min(beg + per, L) - beg;
+    const bool held = per <= kPlanHeld;
+    const bool vec = held && (per & 3) == 0;   // then n is per or 0
+    float xv[kPlanHeld];
+    if (vec) {
+#pragma unroll
+        for (int i = 0; i < kPlanHeld; i += 4) {
+            float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (i < n) v = *reinterpret_cast<const float4*>(x + beg + i);
+            xv[i] = v.x; xv[i + 1] = v.y; xv[i + 2] = v.z; xv[i + 3] = v.w;
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < kPlanHeld; ++i) xv[i] = held && i < n ? x[beg + i] : 0.f;
+    }
+    double mq = 0.0, mk = 0.0;   // squared norms are >= 0; a NaN wins nan_max
+    const bool norms = gamma_q == nullptr;
+    if (norms) {
         for (int i = t; i < nchunk; i += kPlanThreads) {
             mq = nan_max(mq, part[((size_t)bh * 2 + 0) * nchunk + i]);
             mk = nan_max(mk, part[((size_t)bh * 2 + 1) * nchunk + i]);
         }
-        auto nmax = [](double a, double b) { return nan_max(a, b); };
-        mq = block_reduce(mq, s_dbl, nmax);
-        mk = block_reduce(mk, s_dbl, nmax);
-        if (t == 0) {
-            // U = rho_q rho_k / sqrt(d) evaluated as sqrt(rho_q^2 rho_k^2 / d);
-            // delta = -2U - log L + log eps, every step rounded to nearest.
-            const double u = __builtin_sqrt((mq * mk) / (double)d);
-            const double delta = -(2.0 * u + log_l_over_eps);
-            s_delta = delta;
-            u_out[bh] = u;
-            delta_out[bh] = delta;
-            if (!(mq <= 1.7976931348623157e308) || !(mk <= 1.7976931348623157e308)) flags |= 8;
+    }
+
+    // ---- this thread's sums and checks --------------------------------------------
+    double local = 0.0, local_abs = 0.0;
+    int min_lsb = 1 << 30;
+    bool positive = false, nonfinite = false;
+    auto take = [&](float v) __attribute__((always_inline)) {
+        if (!__builtin_isfinite(v)) nonfinite = true;
+        else {
+            if (v > 0.0f) positive = true;
+            if (v != 0.0f) min_lsb = min(min_lsb, lsb_exp(v));
         }
-    } else if (t == 0) {
+        local += (double)v;
+        local_abs += __builtin_fabs((double)v);
+    };
+    if (held) {
+#pragma unroll
+        for (int i = 0; i < kPlanHeld; ++i)
+            if (i < n) take(xv[i]);
+    } else {
+        for (int i = 0; i < n; ++i) take(x[beg + i]);
+    }
+
+    // ---- one round through LDS --------------------------------------------------------
+    double incl = local;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const double o = __shfl_up(incl, off);
+        if (lane >= off) incl += o;
+    }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+        local_abs += __shfl_xor(local_abs, off);
+        min_lsb = min(min_lsb, __shfl_xor(min_lsb, off));
+    }
+    const int wflags = (__ballot(positive) != 0ull ? 1 : 0) | (__ballot(nonfinite) != 0ull ? 2 : 0);
+    if (norms && wid * 64 < nchunk) {   // only waves that loaded partials
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) {
+            mq = nan_max(mq, __shfl_xor(mq, off));
+            mk = nan_max(mk, __shfl_xor(mk, off));
+        }
+    }
+    if (lane == 63) s_sum[wid] = incl;
+    if (lane == 0) {
+        s_abs[wid] = local_abs;
+        s_lsb[wid] = min_lsb;
+        s_flg[wid] = wflags;
+        s_mq[wid] = mq;
+        s_mk[wid] = mk;
+    }
+    lds_barrier();
+    double before = 0.0, total_abs = 0.0;
+    int flags = 0;
+    min_lsb = 1 << 30;
+    mq = 0.0;
+    mk = 0.0;
+#pragma unroll 4
+    for (int w2 = 0; w2 < kPlanWaves; ++w2) {
+        if (w2 < wid) before += s_sum[w2];
+        total_abs += s_abs[w2];
+        min_lsb = min(min_lsb, s_lsb[w2]);
+        flags |= s_flg[w2];
+        mq = nan_max(mq, s_mq[w2]);
+        mk = nan_max(mk, s_mk[w2]);
+    }
+    if (total_abs > 0.0) {
+        // every partial sum is a multiple of 2^min_lsb and below 2^(ilogb+2)
+        const int biased = (int)((__double_as_longlong(total_abs) >> 52) & 0x7ff);
+        const int top = (biased > 0 ? biased : 1) - 1023 + 2;
+        if (top - min_lsb > 53) flags |= 4;
+    }
+
+    // ---- U and delta ---------------------------------------------------------------------
+    double u;
+    if (norms) {
+        // U = rho_q rho_k / sqrt(d) evaluated as sqrt(rho_q^2 rho_k^2 / d);
+        // delta = -2U - log L + log eps, every step rounded to nearest.
+        u = __builtin_sqrt((mq * mk) / (double)d);
+        if (!(mq <= 1.7976931348623157e308) || !(mk <= 1.7976931348623157e308)) flags |= 8;
+    } else {
         // QK-norm (App. E): an RMS-normalised row has norm sqrt(d) and a scale of
         // magnitude at most gamma stretches it by at most gamma, so
         // U = gamma_q gamma_k sqrt(d), evaluated as (gamma_q gamma_k) sqrt(d)
         // (the product of two floats is exact in float64).
         const int h = bh % H;
         const double gq = (double)gamma_q[h], gk = (double)gamma_k[h];
-        const double u = (gq * gk) * __builtin_sqrt((double)d);
-        const double delta = -(2.0 * u + log_l_over_eps);
-        s_delta = delta;
-        u_out[bh] = u;
-        delta_out[bh] = delta;
+        u = (gq * gk) * __builtin_sqrt((double)d);
         if (!(gq >= 0.0 && gq <= 3.4028234663852886e38) || !(gk >= 0.0 && gk <= 3.4028234663852886e38))
             flags |= 8;
     }
+    const double delta = -(2.0 * u + log_l_over_eps);
+    if (t == 0) {
+        u_out[bh] = u;
+        delta_out[bh] = delta;
+    }
 
-    // ---- c = cumsum(log f): each thread owns a contiguous run -------------
-    const float* x = log_f + (size_t)bh * L;
-    const int per = (L + kPlanThreads - 1) / kPlanThreads;
-    const int beg = min(t * per, L), end = min(beg + per, L);
-    double local = 0.0, local_abs = 0.0;
-    int min_lsb = 1 << 30;
-    for (int i = beg; i < end; ++i) {
-        const float v = x[i];
-        if (!__builtin_isfinite(v)) flags |= 2;
-        else {
-            if (v > 0.0f) flags |= 1;
-            if (v != 0.0f) min_lsb = min(min_lsb, lsb_exp(v));
+    // ---- c = cumsum(log f) and the block corners ----------------------------------------
+    double run = before + (incl - local);   // exclusive prefix: exact when the span check passes
+    auto corner = [&](int j, float cf) __attribute__((always_inline)) {
+        if ((j & (kBlock - 1)) == 0) s_first[j / kBlock] = cf;
+        if ((j & (kBlock - 1)) == kBlock - 1) s_last[j / kBlock] = cf;
+    };
+    if (vec) {
+#pragma unroll
+        for (int i = 0; i < kPlanHeld; i += 4) {
+            if (i < n) {
+                float4 cv;
+                run += (double)xv[i];     cv.x = (float)run;
+                run += (double)xv[i + 1]; cv.y = (float)run;
+                run += (double)xv[i + 2]; cv.z = (float)run;
+                run += (double)xv[i + 3]; cv.w = (float)run;
+                *reinterpret_cast<float4*>(cw + beg + i) = cv;
+                corner(beg + i, cv.x);            // beg + i is a multiple of 4
+                corner(beg + i + 3, cv.w);
+            }
         }
-        local += (double)v;
-        local_abs += __builtin_fabs((double)v);
+    } else if (held) {
+#pragma unroll
+        for (int i = 0; i < kPlanHeld; ++i) {
+            if (i < n) {
+                run += (double)xv[i];
+                const float cf = (float)run;
+                cw[beg + i] = cf;
+                corner(beg + i, cf);
+            }
+        }
+    } else {
+        for (int i = 0; i < n; ++i) {
+            run += (double)x[beg + i];
+            const float cf = (float)run;
+            cw[beg + i] = cf;
+            corner(beg + i, cf);
+        }
     }
-    const double incl = block_inclusive_scan(local, s_dbl);
-    double run = incl - local;  // exclusive prefix: exact when the span check passes
-    auto sum = [](double a, double b) { return a + b; };
-    auto imin = [](int a, int b) { return min(a, b); };
-    auto ior = [](int a, int b) { return a | b; };
-    const double total_abs = block_reduce(local_abs, s_dbl2, sum);
-    min_lsb = block_reduce(min_lsb, s_int, imin);
-    if (t == 0 && total_abs > 0.0) {
-        // every partial sum is a multiple of 2^min_lsb and below 2^(ilogb+2)
-        const int biased = (int)((__double_as_longlong(total_abs) >> 52) & 0x7ff);
-        const int top = (biased > 0 ? biased : 1) - 1023 + 2;
-        if (top - min_lsb > 53) flags |= 4;
-    }
-    for (int i = beg; i < end; ++i) {
-        run += (double)x[i];
-        const float cf = (float)run;
-        c_out[(size_t)bh * L + i] = cf;
-        if ((i & (kBlock - 1)) == 0) s_first[i / kBlock] = cf;
-        if ((i & (kBlock - 1)) == kBlock - 1) s_last[i / kBlock] = cf;
-    }
-    flags = block_reduce(flags, s_int, ior);   // also orders the LDS writes above
+    lds_barrier();
 
-    // ---- boundary: first kept key block of every query block ---------------
+    // ---- boundary: first kept key block of every query block ---------------------------
     // Block (m, n < m) is kept iff its top-right entry c_{64m} - c_{64n+63} is
     // >= delta.  With non-increasing c that entry grows with n, so the first
     // kept block is found by bisection; the diagonal block is always kept.
-    const double delta = s_delta;
-    long long kept = 0;
     for (int m = t; m < M; m += kPlanThreads) {
         const double f = (double)s_first[m];
         int lo = 0, hi = m;
@@ -183,24 +279,27 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
         }
         s_rs[m] = lo;
         row_start[(size_t)bh * M + m] = lo;
-        kept += (long long)(m - lo + 1);
     }
-    __syncthreads();
+    lds_barrier();
     // last query block that keeps key block n: largest m with row_start[m] <= n
-    for (int n = t; n < M; n += kPlanThreads) {
-        int lo = n, hi = M - 1;
+    for (int nn = t; nn < M; nn += kPlanThreads) {
+        int lo = nn, hi = M - 1;
         while (lo < hi) {
             const int mid = (lo + hi + 1) >> 1;
-            if (s_rs[mid] <= n) lo = mid;
+            if (s_rs[mid] <= nn) lo = mid;
             else hi = mid - 1;
         }
-        col_end[(size_t)bh * M + n] = lo;
+        col_end[(size_t)bh * M + nn] = lo;
     }
-    auto lsum = [](long long a, long long b) { return a + b; };
-    kept = block_reduce(kept, s_ll, lsum);
-    if (t == 0) {
-        kept_out[bh] = kept;
-        flags_out[bh] = flags;
+    if (wid == kPlanWaves - 1) {   // (no col_end work for this wave unless M > 960)
+        long long kept = 0;
+        for (int m = lane; m < M; m += 64) kept += (long long)(m - s_rs[m] + 1);
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) kept += __shfl_xor(kept, off);
+        if (lane == 0) {
+            kept_out[bh] = kept;
+            flags_out[bh] = flags;
+        }
     }
 }
 

@@ -160,54 +160,60 @@ __global__ __launch_bounds__(64) void dkdv_f32_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// dlog f_l = sum_{i >= l} (rowsum_i - colsum_i), accumulated in float64.
+// dlog f_l = sum_{i >= l} (rowsum_i - colsum_i), accumulated in float64.  Each
+// thread owns a contiguous run (held in registers up to kScanHeld values); one
+// round through LDS carries the waves' totals for the suffix sums.
 // ---------------------------------------------------------------------------
 constexpr int kScanThreads = 1024;
+constexpr int kScanHeld = 16;
 
 __global__ __launch_bounds__(kScanThreads) void dlogf_kernel(const float* __restrict__ rowsum,
                                                              const float* __restrict__ colsum,
                                                              float* __restrict__ dlog_f, int L) {
-    __shared__ double s_wave[kScanThreads / 64];
+    constexpr int kWaves = kScanThreads / 64;
+    __shared__ double s_tot[kWaves];
     const int bh = blockIdx.x, t = threadIdx.x, lane = t & 63, wid = t >> 6;
     const size_t head = (size_t)bh * L;
     const int per = (L + kScanThreads - 1) / kScanThreads;
-    const int beg = min(t * per, L), end = min(beg + per, L);
+    const int beg = min(t * per, L), n = min(beg + per, L) - beg;
+    const bool held = per <= kScanHeld;
+    double dv[kScanHeld];
+#pragma unroll
+    for (int i = 0; i < kScanHeld; ++i)
+        dv[i] = held && i < n ? (double)rowsum[head + beg + i] - (double)colsum[head + beg + i] : 0.0;
     double local = 0.0;
-    for (int i = beg; i < end; ++i) local += (double)rowsum[head + i] - (double)colsum[head + i];
-    // exclusive suffix sum over threads: scan with the thread order reversed
-    const int rt = kScanThreads - 1 - t;  // reversed position
-    // place the value of thread t at position rt and scan positions ascending
-    // (done through LDS so that each wave scans contiguous positions)
-    __shared__ double s_val[kScanThreads];
-    s_val[rt] = local;
-    __syncthreads();
-    double v = s_val[t];  // value at position t
+    if (held) {
+#pragma unroll
+        for (int i = 0; i < kScanHeld; ++i) local += dv[i];
+    } else {
+        for (int i = 0; i < n; ++i) local += (double)rowsum[head + beg + i] - (double)colsum[head + beg + i];
+    }
+    // inclusive suffix sums over the lanes of the wave, then over the waves after it
+    double suf = local;
 #pragma unroll
     for (int off = 1; off < 64; off <<= 1) {
-        const double o = __shfl_up(v, off);
-        if (lane >= off) v += o;
+        const double o = __shfl_down(suf, off);
+        if (lane + off < 64) suf += o;
     }
-    if (lane == 63) s_wave[wid] = v;
+    if (lane == 0) s_tot[wid] = suf;
     __syncthreads();
-    if (wid == 0) {
-        double x = lane < kScanThreads / 64 ? s_wave[lane] : 0.0;
+    double after = 0.0;
+#pragma unroll 4
+    for (int w2 = kWaves - 1; w2 > wid; --w2) after += s_tot[w2];
+    double run = after + (suf - local);   // sum over the threads after this one
+    if (held) {
 #pragma unroll
-        for (int off = 1; off < kScanThreads / 64; off <<= 1) {
-            const double o = __shfl_up(x, off);
-            if (lane >= off) x += o;
+        for (int i = kScanHeld - 1; i >= 0; --i) {
+            if (i < n) {
+                run += dv[i];
+                dlog_f[head + beg + i] = (float)run;
+            }
         }
-        if (lane < kScanThreads / 64) s_wave[lane] = x;
-    }
-    __syncthreads();
-    const double incl = v + (wid > 0 ? s_wave[wid - 1] : 0.0);  // inclusive at position t
-    __syncthreads();
-    s_val[t] = incl;
-    __syncthreads();
-    // thread t: sum over positions < rt, i.e. over threads > t
-    double run = rt > 0 ? s_val[rt - 1] : 0.0;
-    for (int i = end - 1; i >= beg; --i) {
-        run += (double)rowsum[head + i] - (double)colsum[head + i];
-        dlog_f[head + i] = (float)run;
+    } else {
+        for (int i = n - 1; i >= 0; --i) {
+            run += (double)rowsum[head + beg + i] - (double)colsum[head + beg + i];
+            dlog_f[head + beg + i] = (float)run;
+        }
     }
 }
 

@@ -63,6 +63,17 @@ def test_boundary_bit_exact(name):
         assert frac.min() == 0.0 and frac.max() > 0.9
 
 
+@pytest.mark.parametrize("L", [4160, 32768])
+def test_boundary_lengths_off_the_vector_path(L):
+    # L = 4160: runs of 5 gates per thread (scalar path); L = 32768: runs longer
+    # than the registers hold (re-read from memory); both bit-exact.
+    w = workloads.custom("len", 1, 3, L, 64, "bf16", 12, mu=(0.5, 3.0, 9.0))
+    print(f"case: boundary {w.describe()}", flush=True)
+    x = workloads.generate(w, with_grad=False)
+    got = _gpu_plan(x, w.eps)
+    _check_plan(x, got, w.eps)
+
+
 def test_boundary_many_heads_exercise_sqrt_and_division():
     # 4096 heads of one block each, Q/K rows scaled per head over six decades:
     # U and delta must match the host's IEEE float64 arithmetic bit for bit.
