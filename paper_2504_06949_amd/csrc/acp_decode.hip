@@ -11,7 +11,8 @@
 // Kernels:
 //   decode_init_kernel  prompt of L0 tokens -> delta, the float64 running cumsum,
 //                       c of the prompt's last C positions, the pointer of query
-//                       L0 - 1, and its K/V rows in the ring
+//                       L0 - 1
+//   decode_copy_kernel  the prompt's last K/V rows into the ring
 //   decode_step_kernel  one token: c_t, the pointer advance, query t over its
 //                       kept keys (256 per workgroup, partial softmax sums), and
 //                       the append of k_t, v_t
@@ -42,11 +43,11 @@ size_t decode_partials_floats(int BH, int C, int d) {
 __device__ __forceinline__ int ring(int j, int C) { return j % C; }
 
 // ---------------------------------------------------------------------------
-template <typename T, int D>
+template <int D>
 __global__ __launch_bounds__(kPlanThreads) void decode_init_kernel(
-    const T* __restrict__ K, const T* __restrict__ V, const float* __restrict__ log_f,
+    const float* __restrict__ log_f,
     const float* __restrict__ gamma_q, const float* __restrict__ gamma_k, int H, int L0, int C,
-    double log_lmax_over_eps, T* __restrict__ Kc, T* __restrict__ Vc, float* __restrict__ cc,
+    double log_lmax_over_eps, float* __restrict__ cc,
     double* __restrict__ cs_out, int* __restrict__ ptr_out, double* __restrict__ delta_out,
     int* __restrict__ flags_out) {
     __shared__ double s_dbl[kPlanWaves];
@@ -127,18 +128,40 @@ __global__ __launch_bounds__(kPlanThreads) void decode_init_kernel(
         ptr_out[(size_t)((L0 - 1) & 1) * gridDim.x + bh] = max(lo, first > 0 ? first / kBlock : 0);
         flags_out[bh] = flags;
     }
+}
 
-    // the prompt's last min(L0, C) K and V rows into their slots
+// The prompt's last min(L0, C) K and V rows into their ring slots: grid
+// (ceil(rows / 64), B*H), each workgroup 64 rows of both tensors, every lane's
+// 16-byte pieces requested before any is stored.
+constexpr int kCopyRows = 64;
+
+template <typename T, int D>
+__global__ __launch_bounds__(256) void decode_copy_kernel(
+    const T* __restrict__ K, const T* __restrict__ V, int L0, int C, T* __restrict__ Kc,
+    T* __restrict__ Vc) {
     constexpr int kVec = 16 / (int)sizeof(T);
-    constexpr int kPerRow = D / kVec;
+    constexpr int kPerRow = D / kVec;                  // 16-byte pieces per row
+    constexpr int kPer = kCopyRows * kPerRow / 256;    // pieces per thread and tensor
+    const int bh = blockIdx.y, t = threadIdx.x;
     const int j0 = max(0, L0 - C);
-    const int nrow = L0 - j0;
-    for (int i = t; i < nrow * kPerRow; i += kPlanThreads) {
-        const int j = j0 + i / kPerRow, e = (i % kPerRow) * kVec;
+    const int r0 = j0 + blockIdx.x * kCopyRows;
+    uint4 kv[kPer], vv[kPer];
+#pragma unroll
+    for (int p = 0; p < kPer; ++p) {
+        // rows past the prompt read its last row again (branch-free)
+        const int i = t + 256 * p, j = min(r0 + i / kPerRow, L0 - 1), e = (i % kPerRow) * kVec;
         const size_t src = ((size_t)bh * L0 + j) * D + e;
+        kv[p] = *reinterpret_cast<const uint4*>(K + src);
+        vv[p] = *reinterpret_cast<const uint4*>(V + src);
+    }
+    __builtin_amdgcn_sched_barrier(0);   // all requests out before the first store
+#pragma unroll
+    for (int p = 0; p < kPer; ++p) {
+        // (a row past the prompt rewrites the last row's slot with the same bytes)
+        const int i = t + 256 * p, j = min(r0 + i / kPerRow, L0 - 1), e = (i % kPerRow) * kVec;
         const size_t dst = ((size_t)bh * C + (j % C)) * D + e;
-        *reinterpret_cast<uint4*>(Kc + dst) = *reinterpret_cast<const uint4*>(K + src);
-        *reinterpret_cast<uint4*>(Vc + dst) = *reinterpret_cast<const uint4*>(V + src);
+        *reinterpret_cast<uint4*>(Kc + dst) = kv[p];
+        *reinterpret_cast<uint4*>(Vc + dst) = vv[p];
     }
 }
 
@@ -464,10 +487,15 @@ __global__ __launch_bounds__(kDecChunk) void decode_combine_kernel(
 // ---------------------------------------------------------------------------
 template <typename T, int D>
 static hipError_t init_t(const DecodeInitArgs& a, hipStream_t s) {
-    hipLaunchKernelGGL((decode_init_kernel<T, D>), dim3(a.B * a.H), dim3(kPlanThreads), 0, s,
-                       (const T*)a.K, (const T*)a.V, a.log_f, a.gamma_q, a.gamma_k, a.H, a.L0,
-                       a.C, a.log_lmax_over_eps, (T*)a.Kc, (T*)a.Vc, a.cc, a.cs, a.ptr, a.delta,
-                       a.flags);
+    hipLaunchKernelGGL((decode_init_kernel<D>), dim3(a.B * a.H), dim3(kPlanThreads), 0, s,
+                       a.log_f, a.gamma_q, a.gamma_k, a.H, a.L0,
+                       a.C, a.log_lmax_over_eps, a.cc, a.cs, a.ptr, a.delta, a.flags);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int rows = min(a.L0, a.C);
+    hipLaunchKernelGGL((decode_copy_kernel<T, D>),
+                       dim3((rows + kCopyRows - 1) / kCopyRows, a.B * a.H), dim3(256), 0, s,
+                       (const T*)a.K, (const T*)a.V, a.L0, a.C, (T*)a.Kc, (T*)a.Vc);
     return hipGetLastError();
 }
 
