@@ -22,7 +22,7 @@
 // running maximum (and its rescaling of the accumulators) is not needed: the
 // constant is folded into the MFMA accumulator initialisation, and each logit
 // costs one FMA and one exp2.  Heads with a larger U take the online-maximum
-// variant.  Both variants are launched; each skips the heads of the other.
+// variant; one launch holds both, and each workgroup takes its head's.
 #include <type_traits>
 
 #include "acp_device.h"
@@ -58,19 +58,14 @@ struct alignas(1024) FwdSmem {
 };
 
 template <int D, bool kFixed>
-__global__ __launch_bounds__(kFwdThreads) void fwd_bf16_kernel(
+__device__ __forceinline__ void fwd_bf16_body(
+    FwdSmem<D>& sm, int lid, int bh, double u_head,
     const __bf16* __restrict__ Q, const __bf16* __restrict__ K, const __bf16* __restrict__ V,
     const float* __restrict__ cg, const int* __restrict__ row_start,
-    const double* __restrict__ bound_u, __bf16* __restrict__ O, float* __restrict__ lse,
-    float* __restrict__ lse2, int L, int M, int nqb, int nblocks, float kscale) {
+    __bf16* __restrict__ O, float* __restrict__ lse,
+    float* __restrict__ lse2, int L, int M, int nqb, float kscale) {
     constexpr int NDS = D / 32;                     // k-steps over the head dim
     constexpr int NDT = D / 16;                     // output tiles over the head dim
-    __shared__ FwdSmem<D> sm;
-
-    const int lid = xcd_logical_id(blockIdx.x, nblocks);
-    const int bh = lid / nqb;
-    const double u_head = bound_u[bh];
-    if ((u_head <= kUFixedMax) != kFixed) return;   // the other variant's head
     const int qb = nqb - 1 - (lid % nqb);           // longest rows first
     const int tid = threadIdx.x, lane = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -354,6 +349,26 @@ __global__ __launch_bounds__(kFwdThreads) void fwd_bf16_kernel(
     }
 }
 
+// One launch for both variants: the head's bound picks the body (uniform over
+// the workgroup), and the two bodies share the workgroup's LDS.
+template <int D>
+__global__ __launch_bounds__(kFwdThreads) void fwd_bf16_kernel(
+    const __bf16* __restrict__ Q, const __bf16* __restrict__ K, const __bf16* __restrict__ V,
+    const float* __restrict__ cg, const int* __restrict__ row_start,
+    const double* __restrict__ bound_u, __bf16* __restrict__ O, float* __restrict__ lse,
+    float* __restrict__ lse2, int L, int M, int nqb, int nblocks, float kscale) {
+    __shared__ FwdSmem<D> sm;
+    const int lid = xcd_logical_id(blockIdx.x, nblocks);
+    const int bh = lid / nqb;
+    const double u_head = bound_u[bh];
+    if (u_head <= kUFixedMax)
+        fwd_bf16_body<D, true>(sm, lid, bh, u_head, Q, K, V, cg, row_start, O, lse, lse2, L, M,
+                               nqb, kscale);
+    else
+        fwd_bf16_body<D, false>(sm, lid, bh, u_head, Q, K, V, cg, row_start, O, lse, lse2, L, M,
+                                nqb, kscale);
+}
+
 // ---------------------------------------------------------------------------
 // fp32 path: plain VALU arithmetic, one thread per query, 64 queries (one
 // pruning row) per workgroup; K/V tiles staged in LDS; online maximum.
@@ -420,11 +435,7 @@ static void launch_fwd_bf16(const FwdArgs& a, int M, float kscale, hipStream_t s
     const int BH = a.B * a.H;
     const int nqb = (a.L + kFwdRows - 1) / kFwdRows;
     const int nblocks = BH * nqb;
-    hipLaunchKernelGGL((fwd_bf16_kernel<D, true>), dim3(nblocks), dim3(kFwdThreads), 0, s,
-                       (const __bf16*)a.Q, (const __bf16*)a.K, (const __bf16*)a.V, a.c,
-                       a.row_start, a.u, (__bf16*)a.O, a.lse, a.lse2, a.L, M, nqb,
-                       nblocks, kscale);
-    hipLaunchKernelGGL((fwd_bf16_kernel<D, false>), dim3(nblocks), dim3(kFwdThreads), 0, s,
+    hipLaunchKernelGGL((fwd_bf16_kernel<D>), dim3(nblocks), dim3(kFwdThreads), 0, s,
                        (const __bf16*)a.Q, (const __bf16*)a.K, (const __bf16*)a.V, a.c,
                        a.row_start, a.u, (__bf16*)a.O, a.lse, a.lse2, a.L, M, nqb,
                        nblocks, kscale);
