@@ -54,7 +54,7 @@ __all__ = [
     "boundary_alg1", "col_end_from_row_start", "kept_tiles", "causal_tiles",
     "block_mask", "entry_mask", "causal_mask", "forward", "backward", "pruned_mass",
     "plan_head", "run_head", "forward_rows", "backward_rows", "backward_cols",
-    "decode_pointer", "decode_row", "decode_ring_row",
+    "decode_pointer", "decode_row", "decode_ring_row", "qk_projection",
 ]
 
 
@@ -527,3 +527,20 @@ def decode_ring_row(q_t, k, v, c, t: int, delta: float, capacity: int, block: in
     o, lse = _attend_range(q_t, k, v, c, t, max(n * block, first, 0))
     return o, lse, max(n, first // block if first > 0 else 0), lost
 
+
+
+# --------------------------------------------------------------------------
+# Projection (Sec. 2: q_i = W_q x_i, k_i = W_k x_i), whose stored output the
+# bound's row norms are taken from (Sec. 3)
+# --------------------------------------------------------------------------
+
+def qk_projection(x, w, B: int, H: int, d: int) -> np.ndarray:
+    """Head-split projection X W in float64: token l of sequence b is row b L + l
+    of X [B L, d_model], feature e of head h is column h d + e of W [d_model, H d];
+    the result is [B, H, L, d] (the layout the attention takes its queries and
+    keys in)."""
+    x = np.asarray(x, dtype=np.float64)
+    w = np.asarray(w, dtype=np.float64)
+    L = x.shape[0] // B
+    y = x @ w
+    return y.reshape(B, L, H, d).transpose(0, 2, 1, 3)

@@ -500,3 +500,35 @@ def test_decode_ring_row_with_room_is_decode_row():
         b = orc.decode_ring_row(q[t], k, v, c, t, -15.0, 320)
         np.testing.assert_array_equal(a[0], b[0])
         assert a[1] == b[1] and a[2] == b[2] and b[3] is False
+
+
+
+def test_qk_projection_matches_the_sum_written_out():
+    """Q[b, h, l, e] = sum_k X[b L + l, k] W[k, h d + e] (Sec. 2), by explicit loops."""
+    rng = _rng(41)
+    B, L, Dm, H, d = 2, 3, 5, 2, 4
+    x = rng.standard_normal((B * L, Dm))
+    w = rng.standard_normal((Dm, H * d))
+    q = orc.qk_projection(x, w, B, H, d)
+    assert q.shape == (B, H, L, d)
+    for b in range(B):
+        for h in range(H):
+            for l in range(L):
+                for e in range(d):
+                    ref = sum(x[b * L + l, k] * w[k, h * d + e] for k in range(Dm))
+                    assert abs(q[b, h, l, e] - ref) <= 1e-12
+
+
+def test_qk_projection_by_a_permutation_moves_columns():
+    """W a permutation matrix: the projection only rearranges X's columns, exactly."""
+    rng = _rng(43)
+    B, L, H, d = 2, 4, 3, 4
+    Dm = H * d
+    x = rng.standard_normal((B * L, Dm))
+    perm = rng.permutation(Dm)
+    w = np.zeros((Dm, Dm))
+    w[perm, np.arange(Dm)] = 1.0                  # column c of X W is column perm[c] of X
+    q = orc.qk_projection(x, w, B, H, d)
+    for b in range(B):
+        for h in range(H):
+            np.testing.assert_array_equal(q[b, h], x[b * L:(b + 1) * L][:, perm[h * d:(h + 1) * d]])
