@@ -187,6 +187,47 @@ def run_decode(steps: int = 64, warmup: int = 16, L0: int = 4096, C: int = 8192)
     return out
 
 
+def run_projection(reps: int = 20, d_model: int = 768):
+    """The Q/K projection with the norm epilogue on the 125M-shaped layer
+    (X [B*L, d_model] bf16, Wq and Wk [d_model, H*d], d_model = 768 as in the
+    paper's 125M model), against torch's bf16 matmul of the same product (no
+    epilogue, row-major output) and the norm pass it makes unnecessary."""
+    import torch
+    from paper_2504_06949_amd import acp, workloads
+
+    w0 = workloads.WORKLOADS["125m"]
+    B, L, H, d = w0.B, w0.L, w0.H, w0.d
+    p = workloads.projection_inputs(B, L, d_model, H, d, seed=7)
+    dev = torch.device("cuda:0")
+    x, wq, wk = (p[n].to(dev) for n in ("x", "wq", "wk"))
+    q = torch.empty((B, H, L, d), dtype=torch.bfloat16, device=dev)
+    k = torch.empty_like(q)
+    ws = torch.empty(acp.acp_workspace_size(B, H, L, d, acp.ACP_BF16), dtype=torch.uint8,
+                     device=dev)
+    wqk = torch.cat([wq, wk], dim=1).contiguous()
+
+    def timed(fn):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / reps
+
+    us = timed(lambda: acp.project_qk(x, wq, wk, B, H, d, ws=ws, out=(q, k)))
+    mm_us = timed(lambda: torch.matmul(x, wqk))
+    flops = 2.0 * 2 * (B * L) * d_model * (H * d)
+    return {"workload": f"X [{B * L}, {d_model}] bf16 -> Q, K [{B}, {H}, {L}, {d}], "
+                        f"norm maxima per 128-row chunk in the epilogue",
+            "us": round(us, 2), "tflops": round(flops / (us * 1e-6) / 1e12, 1),
+            "frac": round(flops / (us * 1e-6) / 1e12 / PEAK_BF16_TFLOPS, 4),
+            "torch_matmul_us": round(mm_us, 2)}
+
+
 def cpu_baseline(res, budget_s: float = 15.0):
     """The oracle, untuned, on whole heads of the same workload until the budget is spent."""
     import numpy as np
@@ -316,6 +357,9 @@ def main():
         out["other_workloads"] = extra
     if not args.no_decode:
         out["decode"] = run_decode()
+        prj = run_projection()
+        prj["norm_pass_us_saved"] = round(pk["rownorm"] * 1e3, 2)
+        out["projection"] = prj
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(res)
     print(json.dumps(out), flush=True)

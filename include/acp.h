@@ -161,6 +161,35 @@ acp_status fox_attn_bwd(const void* Q, const void* K, const void* V, const void*
                         void* dQ, void* dK, void* dV, float* dlog_f,
                         void* ws, size_t ws_bytes, void* stream);
 
+/* ---- Stage 1's norm pass fused into the Q/K projection --------------------------
+ * U needs only the largest row norms of the stored Q and K (Sec. 3), so the
+ * projection that produces them can form those maxima in its epilogue and the
+ * forward can skip its own pass over Q and K.
+ *
+ * acp_qk_project:  Q = X Wq, K = X Wk with X [B*L, d_model] (row b*L + l is token l
+ * of sequence b) and Wq, Wk [d_model, H*d] (column h*d + e is feature e of head h),
+ * all bfloat16 row-major; float32 accumulation, outputs rounded to bfloat16 and
+ * written head-split as Q, K [B, H, L, d].  The epilogue stores, into the
+ * workspace, the largest float64 sum of squares (ascending feature order) of the
+ * stored rows of every 128-row chunk: exactly what the forward's own norm pass
+ * computes for these Q and K.
+ *   Supported: dt = ACP_BF16 only; d in {64, 128}; L a multiple of 128, L <= 131072;
+ *   d_model a positive multiple of 64; H*d a multiple of 128.
+ *   ws: a workspace of acp_workspace_size(B, H, L, d, dt) bytes; only the norm
+ *   partials are written.
+ *
+ * fox_attn_fwd_projected:  fox_attn_fwd for Q and K that acp_qk_project produced
+ * into this workspace (the caller vouches for that): stage 1 takes the norm
+ * partials from ws instead of reading Q and K again.  Same outputs, same
+ * workspace for fox_attn_bwd. */
+acp_status acp_qk_project(const void* X, const void* Wq, const void* Wk, acp_dtype dt, int B,
+                          int L, int d_model, int H, int d, void* Q, void* K, void* ws,
+                          size_t ws_bytes, void* stream);
+
+acp_status fox_attn_fwd_projected(const void* Q, const void* K, const void* V, const float* log_f,
+                                  acp_dtype dt, int B, int H, int L, int d, double eps, void* O,
+                                  float* lse, void* ws, size_t ws_bytes, void* stream);
+
 /* ---- Decoding with ACP (Sec. 5, inference) -----------------------------------
  * Token-by-token attention after a prompt, with a logit bound fixed in advance
  * by QK-norm scales (App. E) and the threshold sized for the longest sequence:
@@ -244,7 +273,8 @@ enum {
     ACP_K_DECODE_INIT = 7, /* decoding state from a prompt      */
     ACP_K_DECODE = 8,   /* one decoding step (append, attention
                            over kept keys, split combine)        */
-    ACP_K_COUNT = 9
+    ACP_K_PROJECT = 9,  /* Q/K projection with norm epilogue    */
+    ACP_K_COUNT = 10
 };
 typedef struct {
     int64_t launches[ACP_K_COUNT];

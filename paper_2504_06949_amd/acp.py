@@ -44,7 +44,8 @@ class DecodeLayout(ctypes.Structure):
                 ("k_cache", "v_cache", "c", "cum", "delta", "pointer", "flags", "total")]
 
 
-K_NAMES = ("rownorm", "plan", "fwd", "dsum", "dq", "dkdv", "dlogf", "decode_init", "decode")
+K_NAMES = ("rownorm", "plan", "fwd", "dsum", "dq", "dkdv", "dlogf", "decode_init", "decode",
+           "project")
 
 
 class KernelTimes(ctypes.Structure):
@@ -66,6 +67,8 @@ _SIGS = {
     "fox_attn_fwd_qknorm": [_p, _p, _p, _p, _p, _p, _i, _i, _i, _i, _i, _d, _p, _p, _p, _sz,
                             _p],
     "fox_attn_bwd": [_p, _p, _p, _p, _p, _i, _i, _i, _i, _i, _p, _p, _p, _p, _p, _sz, _p],
+    "acp_qk_project": [_p, _p, _p, _i, _i, _i, _i, _i, _i, _p, _p, _p, _sz, _p],
+    "fox_attn_fwd_projected": [_p, _p, _p, _p, _i, _i, _i, _i, _i, _d, _p, _p, _p, _sz, _p],
     "acp_decode_state_size": [_i, _i, _i, _i, _i, ctypes.POINTER(_sz)],
     "acp_decode_offsets": [_i, _i, _i, _i, _i, ctypes.POINTER(DecodeLayout)],
     "acp_decode_init": [_p, _p, _p, _p, _p, _i, _i, _i, _i, _i, _i, _d, _i64, _p, _sz, _p],
@@ -155,6 +158,16 @@ def fox_attn_bwd(Q, K, V, O, dO, dt, B, H, L, d, dQ, dK, dV, dlog_f, ws, ws_byte
                  stream) -> int:
     return lib().fox_attn_bwd(Q, K, V, O, dO, dt, B, H, L, d, dQ, dK, dV, dlog_f, ws,
                               ws_bytes, stream)
+
+
+def acp_qk_project(X, Wq, Wk, dt, B, L, d_model, H, d, Q, K, ws, ws_bytes, stream) -> int:
+    return lib().acp_qk_project(X, Wq, Wk, dt, B, L, d_model, H, d, Q, K, ws, ws_bytes, stream)
+
+
+def fox_attn_fwd_projected(Q, K, V, log_f, dt, B, H, L, d, eps, O, lse, ws, ws_bytes,
+                           stream) -> int:
+    return lib().fox_attn_fwd_projected(Q, K, V, log_f, dt, B, H, L, d, eps, O, lse, ws,
+                                        ws_bytes, stream)
 
 
 def acp_decode_state_size(B, H, C, d, dt) -> int:
@@ -307,6 +320,52 @@ def forward_qknorm(q, k, v, log_f, gamma_q, gamma_k, eps: float,
                                gamma_q.data_ptr(), gamma_k.data_ptr(), _dt(q), B, H, L, d, eps,
                                o.data_ptr(), lse.data_ptr(), ws.data_ptr(), ws.numel(),
                                _stream(dev)))
+    return o, lse, ws
+
+
+def project_qk(x, wq, wk, B: int, H: int, d: int, ws: torch.Tensor | None = None, out=None):
+    """Q = X Wq, K = X Wk (X [B*L, d_model], W [d_model, H*d], bf16) written as
+    [B, H, L, d]; the workspace receives the row-norm maxima that
+    forward_projected() then uses.  Returns (Q, K, ws)."""
+    dev = _dev(x, wq, wk)
+    if x.dim() != 2 or wq.dim() != 2 or wq.shape != wk.shape:
+        raise ValueError("X must be [B*L, d_model] and Wq, Wk [d_model, H*d]")
+    for t in (x, wq, wk):
+        if t.dtype != torch.bfloat16:
+            raise TypeError("the projection takes bfloat16 tensors")
+    M, Dm = (int(s) for s in x.shape)
+    if M % B != 0 or tuple(wq.shape) != (Dm, H * d):
+        raise ValueError("shape mismatch")
+    L = M // B
+    if ws is None:
+        ws = torch.empty(acp_workspace_size(B, H, L, d, ACP_BF16), dtype=torch.uint8, device=dev)
+    if out is None:
+        q = torch.empty((B, H, L, d), dtype=torch.bfloat16, device=dev)
+        k = torch.empty_like(q)
+    else:
+        q, k = out
+    _check(acp_qk_project(x.data_ptr(), wq.data_ptr(), wk.data_ptr(), ACP_BF16, B, L, Dm, H, d,
+                          q.data_ptr(), k.data_ptr(), ws.data_ptr(), ws.numel(), _stream(dev)))
+    return q, k, ws
+
+
+def forward_projected(q, k, v, log_f, eps: float, ws: torch.Tensor, out=None):
+    """forward() for Q, K made by project_qk() into `ws`: stage 1 reuses the
+    norm maxima of the projection's epilogue.  Returns (O, lse, ws)."""
+    dev = _dev(q, k, v, log_f)
+    B, H, L, d = _shape(q)
+    if k.shape != q.shape or v.shape != q.shape or k.dtype != q.dtype or v.dtype != q.dtype:
+        raise ValueError("Q, K, V must share shape and dtype")
+    if tuple(log_f.shape) != (B, H, L) or log_f.dtype != torch.float32:
+        raise ValueError("log_f must be float32 [B, H, L]")
+    if out is None:
+        o = torch.empty_like(q)
+        lse = torch.empty((B, H, L), dtype=torch.float32, device=dev)
+    else:
+        o, lse = out
+    _check(fox_attn_fwd_projected(q.data_ptr(), k.data_ptr(), v.data_ptr(), log_f.data_ptr(),
+                                  _dt(q), B, H, L, d, eps, o.data_ptr(), lse.data_ptr(),
+                                  ws.data_ptr(), ws.numel(), _stream(dev)))
     return o, lse, ws
 
 

@@ -292,12 +292,12 @@ acp_status acp_boundary_qknorm(const float* log_f, const float* gamma_q, const f
     return hip_status(acp::launch_plan(a, (hipStream_t)stream), "acp_boundary_qknorm launch");
 }
 
-// Forward after a stage 1 whose bound comes from the row norms (gamma_q null)
-// or from QK-norm scales.
+// Forward after a stage 1 whose bound comes from the row norms (gamma_q null;
+// norms_ready: their chunk maxima are already in ws) or from QK-norm scales.
 static acp_status fwd_common(const void* Q, const void* K, const void* V, const float* log_f,
                              const float* gamma_q, const float* gamma_k, acp_dtype dt, int B,
                              int H, int L, int d, double eps, void* O, float* lse, void* ws,
-                             size_t ws_bytes, void* stream) {
+                             size_t ws_bytes, void* stream, bool norms_ready = false) {
     ACP_TRY(check_shape(B, H, L, d, dt));
     ACP_TRY(check_eps(eps));
     ACP_TRY(check_ptr(Q, "Q"));
@@ -312,6 +312,7 @@ static acp_status fwd_common(const void* Q, const void* K, const void* V, const 
     acp::PlanArgs p = plan_args(Q, K, log_f, dt, B, H, L, d, eps, y, w);
     p.gamma_q = gamma_q;
     p.gamma_k = gamma_k;
+    p.norms_ready = norms_ready;
     hipError_t e = acp::launch_plan(p, (hipStream_t)stream);
     if (e != hipSuccess) return hip_status(e, "fox_attn_fwd boundary launch");
     acp::FwdArgs f{};
@@ -341,6 +342,40 @@ acp_status fox_attn_fwd_qknorm(const void* Q, const void* K, const void* V, cons
     ACP_TRY(check_ptr(gamma_k, "gamma_k"));
     return fwd_common(Q, K, V, log_f, gamma_q, gamma_k, dt, B, H, L, d, eps, O, lse, ws,
                       ws_bytes, stream);
+}
+
+acp_status fox_attn_fwd_projected(const void* Q, const void* K, const void* V, const float* log_f,
+                                  acp_dtype dt, int B, int H, int L, int d, double eps, void* O,
+                                  float* lse, void* ws, size_t ws_bytes, void* stream) {
+    return fwd_common(Q, K, V, log_f, nullptr, nullptr, dt, B, H, L, d, eps, O, lse, ws,
+                      ws_bytes, stream, true);
+}
+
+acp_status acp_qk_project(const void* X, const void* Wq, const void* Wk, acp_dtype dt, int B,
+                          int L, int d_model, int H, int d, void* Q, void* K, void* ws,
+                          size_t ws_bytes, void* stream) {
+    ACP_TRY(check_shape(B, H, L, d, dt));
+    if (dt != ACP_BF16) return fail(ACP_EUNSUPPORTED, "the projection takes bfloat16 only");
+    if (L % 128 != 0) return fail(ACP_EUNSUPPORTED, "L=%d is not a multiple of 128", L);
+    if (d_model <= 0 || d_model % 64 != 0)
+        return fail(ACP_EUNSUPPORTED, "d_model=%d is not a positive multiple of 64", d_model);
+    if ((H * d) % 128 != 0) return fail(ACP_EUNSUPPORTED, "H*d=%d is not a multiple of 128", H * d);
+    if ((long long)B * L / 128 > 65535)
+        return fail(ACP_EUNSUPPORTED, "B*L=%lld exceeds 8388480", (long long)B * L);
+    ACP_TRY(check_ptr(X, "X"));
+    ACP_TRY(check_ptr(Wq, "Wq"));
+    ACP_TRY(check_ptr(Wk, "Wk"));
+    ACP_TRY(check_ptr(Q, "Q"));
+    ACP_TRY(check_ptr(K, "K"));
+    const Layout y = layout(B, H, L, d);
+    ACP_TRY(check_ws(ws, ws_bytes, y));
+    acp::ProjectArgs a{};
+    a.X = X; a.Wq = Wq; a.Wk = Wk;
+    a.B = B; a.L = L; a.Dm = d_model; a.H = H; a.d = d;
+    a.Q = Q; a.K = K;
+    a.part = (double*)((char*)ws + y.part);
+    a.nchunk = y.nchunk;
+    return hip_status(acp::launch_qk_project(a, (hipStream_t)stream), "acp_qk_project launch");
 }
 
 acp_status fox_attn_bwd(const void* Q, const void* K, const void* V, const void* O,

@@ -19,6 +19,7 @@ struct PlanArgs {
     double log_l_over_eps;    // log L - log eps, +inf for eps = 0
     const float* gamma_q;     // [H] QK-norm scale bounds, or null: U from the row norms
     const float* gamma_k;     // [H]
+    bool norms_ready;         // part already holds the chunk maxima (the projection's epilogue)
     double* part;             // [B*H, 2, nchunk]
     float* c;                 // [B*H, L]
     double* u;                // [B*H]
@@ -62,6 +63,17 @@ struct BwdArgs {
     void* dK;
     void* dV;
     float* dlog_f;
+};
+
+struct ProjectArgs {
+    const void* X;            // [B*L, Dm] bf16
+    const void* Wq;           // [Dm, H*d] bf16
+    const void* Wk;
+    int B, L, Dm, H, d;
+    void* Q;                  // [B, H, L, d] bf16
+    void* K;
+    double* part;             // [B*H, 2, nchunk] chunk maxima of the squared row norms
+    int nchunk;
 };
 
 struct DecodeInitArgs {
@@ -113,6 +125,7 @@ hipError_t launch_fwd(const FwdArgs& a, hipStream_t s);
 hipError_t launch_bwd(const BwdArgs& a, hipStream_t s);
 hipError_t launch_dq_bf16(const BwdArgs& a, hipStream_t s);
 hipError_t launch_dkdv_bf16(const BwdArgs& a, hipStream_t s);
+hipError_t launch_qk_project(const ProjectArgs& a, hipStream_t s);
 size_t decode_partials_floats(int BH, int C, int d);
 hipError_t launch_decode_init(const DecodeInitArgs& a, hipStream_t s);
 hipError_t launch_decode(const DecodeArgs& a, hipStream_t s);

@@ -318,7 +318,7 @@ int norm_chunks(int L) { return (L + kNormRows - 1) / kNormRows; }
 hipError_t launch_plan(const PlanArgs& a, hipStream_t s) {
     hipError_t e;
     const int BH = a.B * a.H;
-    if (a.gamma_q == nullptr) {
+    if (a.gamma_q == nullptr && !a.norms_ready) {
         trace_begin(ACP_K_ROWNORM, s);
         if (a.bf16) {
             e = a.d == 64 ? launch_norm_t<__bf16, 64>(a.Q, a.K, BH, a.L, a.nchunk, a.part, s)

@@ -141,3 +141,16 @@ def generate(w: Workload, with_grad: bool = True) -> dict:
 def to_f64(t: torch.Tensor) -> np.ndarray:
     """Exact upcast of a float32/bfloat16 CPU tensor to a float64 numpy array."""
     return t.detach().to(torch.float32).cpu().numpy().astype(np.float64)
+
+
+def projection_inputs(B: int, L: int, d_model: int, H: int, d: int, seed: int) -> dict:
+    """Seeded inputs of the Q/K projection: layer inputs X [B*L, d_model] ~ N(0, 1)
+    and weights Wq, Wk [d_model, H*d] ~ N(0, 0.02^2) (the initialisation the
+    paper's models use, App. B), all rounded to bfloat16 (CPU tensors)."""
+    g = torch.Generator(device="cpu")
+    g.manual_seed(seed)
+    x = torch.randn((B * L, d_model), generator=g, dtype=torch.float32)
+    wq = torch.randn((d_model, H * d), generator=g, dtype=torch.float32) * 0.02
+    wk = torch.randn((d_model, H * d), generator=g, dtype=torch.float32) * 0.02
+    return {"x": x.bfloat16().contiguous(), "wq": wq.bfloat16().contiguous(),
+            "wk": wk.bfloat16().contiguous()}

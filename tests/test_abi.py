@@ -18,7 +18,8 @@ def test_every_declared_symbol_is_exported():
     names = acp.header_functions()
     assert set(names) == {"acp_workspace_size", "acp_plan_offsets", "acp_boundary",
                           "acp_boundary_qknorm", "fox_attn_fwd", "fox_attn_fwd_qknorm",
-                          "fox_attn_bwd", "acp_decode_state_size", "acp_decode_offsets",
+                          "fox_attn_bwd", "acp_qk_project", "fox_attn_fwd_projected",
+                          "acp_decode_state_size", "acp_decode_offsets",
                           "acp_decode_init", "fox_attn_decode",
                           "acp_timing_enable", "acp_timing_reset",
                           "acp_timing_read", "acp_status_string", "acp_last_error"}
@@ -182,4 +183,24 @@ def test_decode_entries_reject_before_launch():
     assert st == acp.ACP_EINVAL and "aligned" in acp.acp_last_error()
     st = acp.fox_attn_decode(16, 16, 16, 16, acp.ACP_BF16, 1, 1, 10, 128, 64, 1000, 16, 16, 16,
                              8, None)
+    assert st == acp.ACP_EWORKSPACE
+
+
+def test_projection_rejects_before_launch():
+    big = 1 << 40
+    # X, Wq, Wk, dt, B, L, d_model, H, d, Q, K, ws, bytes, stream
+    st = acp.acp_qk_project(16, 16, 16, acp.ACP_F32, 1, 128, 64, 2, 64, 16, 16, 16, big, None)
+    assert st == acp.ACP_EUNSUPPORTED and "bfloat16" in acp.acp_last_error()
+    st = acp.acp_qk_project(16, 16, 16, acp.ACP_BF16, 1, 192, 64, 2, 64, 16, 16, 16, big, None)
+    assert st == acp.ACP_EUNSUPPORTED and "128" in acp.acp_last_error()      # L % 128
+    st = acp.acp_qk_project(16, 16, 16, acp.ACP_BF16, 1, 128, 96, 2, 64, 16, 16, 16, big, None)
+    assert st == acp.ACP_EUNSUPPORTED and "d_model" in acp.acp_last_error()
+    st = acp.acp_qk_project(16, 16, 16, acp.ACP_BF16, 1, 128, 64, 1, 64, 16, 16, 16, big, None)
+    assert st == acp.ACP_EUNSUPPORTED and "H*d" in acp.acp_last_error()
+    st = acp.acp_qk_project(16, 0, 16, acp.ACP_BF16, 1, 128, 64, 2, 64, 16, 16, 16, big, None)
+    assert st == acp.ACP_EINVAL and "Wq" in acp.acp_last_error()
+    st = acp.acp_qk_project(16, 16, 16, acp.ACP_BF16, 1, 128, 64, 2, 64, 16, 16, 16, 8, None)
+    assert st == acp.ACP_EWORKSPACE
+    st = acp.fox_attn_fwd_projected(16, 16, 16, 16, acp.ACP_BF16, 1, 1, 64, 64, 0.5, 16, 16, 16,
+                                    8, None)
     assert st == acp.ACP_EWORKSPACE

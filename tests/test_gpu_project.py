@@ -1,0 +1,66 @@
+"""Q/K projection with the bound's norm maxima in its epilogue: the product must
+match the oracle's float64 projection within bfloat16 rounding, and the forward
+that takes the epilogue's maxima must give exactly the plan and outputs of the
+forward that computes the norms itself from the same Q and K."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as orc
+from paper_2504_06949_amd import acp, workloads
+from tests._helpers import EPS, ensure_built, to_gpu
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _lib():
+    ensure_built()
+
+
+@pytest.mark.parametrize("B,L,Dm,H,d", [(2, 256, 192, 2, 64), (1, 384, 128, 3, 128),
+                                        (1, 128, 64, 2, 64)])
+def test_projection_and_projected_forward(B, L, Dm, H, d):
+    print(f"case: projection B={B} L={L} d_model={Dm} H={H} d={d}", flush=True)
+    p = workloads.projection_inputs(B, L, Dm, H, d, seed=50 + d)
+    w = workloads.custom("prj", B, H, L, d, "bf16", 51, mu=(0.5, 2.0, 6.0))
+    x = workloads.generate(w, with_grad=True)
+    g = to_gpu(x)
+    pg = to_gpu(p)
+    acp.acp_timing_enable(True)
+    acp.acp_timing_reset()
+    q, k, ws = acp.project_qk(pg["x"], pg["wq"], pg["wk"], B, H, d)
+    o, lse, ws = acp.forward_projected(q, k, g["v"], g["log_f"], EPS, ws)
+    torch.cuda.synchronize()
+    kt = acp.acp_timing_read()
+    acp.acp_timing_enable(False)
+    assert kt["project"][0] == 1 and kt["rownorm"][0] == 0 and kt["plan"][0] == 1
+
+    # the product: within bfloat16 rounding of the float64 projection
+    xs, wq, wk = (workloads.to_f64(p[n]) for n in ("x", "wq", "wk"))
+    for got, wm in ((q, wq), (k, wk)):
+        ref = orc.qk_projection(xs, wm, B, H, d)
+        bound = orc.qk_projection(np.abs(xs), np.abs(wm), B, H, d)
+        err = np.abs(got.double().cpu().numpy() - ref)
+        assert np.all(err <= 2.0 ** -8 * np.abs(ref) + 1e-5 * bound), float(err.max())
+
+    # the plan and outputs equal those of the forward that reads Q and K itself
+    plan = {n: t.clone() for n, t in acp.plan_views(ws, B, H, L, d, torch.bfloat16).items()}
+    o2, lse2, ws2 = acp.forward(q, k, g["v"], g["log_f"], EPS)
+    plan2 = acp.plan_views(ws2, B, H, L, d, torch.bfloat16)
+    torch.cuda.synchronize()
+    for n in plan:
+        assert torch.equal(plan[n], plan2[n]), n
+    assert torch.equal(o, o2) and torch.equal(lse, lse2)
+    # U from the oracle's norms of the stored Q and K, bit for bit
+    qn, kn = q.float().cpu().numpy(), k.float().cpu().numpy()
+    for b in range(B):
+        for h in range(H):
+            U = orc.logit_bound(orc.row_norm_sq_max(qn[b, h]), orc.row_norm_sq_max(kn[b, h]), d)
+            assert float(plan["bound_u"][b, h]) == U, (b, h)
+    # the backward takes the projected forward's workspace as it takes the other
+    d1 = acp.backward(q, k, g["v"], o, g["do"], ws)
+    d2 = acp.backward(q, k, g["v"], o2, g["do"], ws2)
+    torch.cuda.synchronize()
+    for a1, a2 in zip(d1, d2):
+        assert torch.equal(a1, a2)
