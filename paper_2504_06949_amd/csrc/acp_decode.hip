@@ -32,7 +32,7 @@
 
 namespace acp {
 
-constexpr int kDecChunk = 256;   // keys per attention workgroup (one per thread)
+constexpr int kDecChunk = 256;   // keys per attention workgroup (64 per wave)
 
 size_t decode_partials_floats(int BH, int C, int d) {
     const int nsplit = (C + kDecChunk - 1) / kDecChunk;

@@ -165,3 +165,40 @@ def test_decode_steps_captured_in_a_graph_match_eager():
         for (o, l), (ro, rl) in zip(outs, ref):
             assert torch.equal(o, ro) and torch.equal(l, rl), rep
         assert torch.equal(dec.current_pointer(), ref_ptr)
+
+
+def test_decode_at_the_bench_shape_sampled():
+    """The bench's decoding configuration (B=8, H=12, d=64, prompt 4096, ring and
+    L_max 8192): four steps, every head's pointer and three heads' outputs against
+    the oracle."""
+    w = workloads.custom("dec", 8, 12, 4160, 64, "bf16", 1, qk_norm=True)
+    print(f"case: decode at the bench shape {w.describe()}", flush=True)
+    x = workloads.generate(w, with_grad=False)
+    g = to_gpu(x)
+    L0, C, L_max = 4096, 8192, 8192
+    dec = acp.Decoder(w.B, w.H, C, w.d).init(g["k"][:, :, :L0].contiguous(),
+                                              g["v"][:, :, :L0].contiguous(),
+                                              g["log_f"][:, :, :L0].contiguous(),
+                                              g["gamma_q"], g["gamma_k"], EPS, L_max)
+    steps = []
+    for t in range(L0, L0 + 4):
+        o, lse = dec.step(_token(g, "q", t), _token(g, "k", t), _token(g, "v", t),
+                          _token(g, "log_f", t))
+        steps.append((t, o.double().cpu().numpy(), lse.double().cpu().numpy(),
+                      dec.current_pointer().cpu().numpy()))
+    flags = dec.views()["flags"].cpu().numpy()
+    assert flags.max() == 0
+    c_ref = orc.cumsum_log_gates(x["log_f"].numpy())
+    for b in range(w.B):
+        for h in range(w.H):
+            U = orc.logit_bound_qknorm(float(x["gamma_q"][h]), float(x["gamma_k"][h]), w.d)
+            delta = orc.threshold(U, L_max, EPS)
+            for t, o, lse, ptr in steps:
+                assert int(ptr[b, h]) == orc.decode_pointer(c_ref[b, h], t, delta), (b, h, t)
+    for b, h in ((0, 0), (3, 5), (7, 11)):
+        q, k, v, _, _ = head_inputs(x, b, h)
+        U = orc.logit_bound_qknorm(float(x["gamma_q"][h]), float(x["gamma_k"][h]), w.d)
+        delta = orc.threshold(U, L_max, EPS)
+        for t, o, lse, _ in steps:
+            o_ref, lse_ref, _ = orc.decode_row(q[t], k, v, c_ref[b, h], t, delta)
+            assert float(np.max(np.abs(o[b, h] - o_ref))) <= 2e-2 and abs(lse[b, h] - lse_ref) <= 1e-3

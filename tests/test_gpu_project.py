@@ -64,3 +64,35 @@ def test_projection_and_projected_forward(B, L, Dm, H, d):
     torch.cuda.synchronize()
     for a1, a2 in zip(d1, d2):
         assert torch.equal(a1, a2)
+
+
+def test_projection_at_the_bench_shape_sampled():
+    """X [32768, 768] -> Q, K [8, 12, 4096, 64]: sampled rows against the oracle's
+    projection of those rows, and the plan of the projected forward equal to the
+    plan the forward computes from the same Q and K."""
+    B, L, Dm, H, d = 8, 4096, 768, 12, 64
+    print(f"case: projection at the bench shape B={B} L={L} d_model={Dm}", flush=True)
+    p = workloads.projection_inputs(B, L, Dm, H, d, seed=7)
+    pg = to_gpu(p)
+    q, k, ws = acp.project_qk(pg["x"], pg["wq"], pg["wk"], B, H, d)
+    w = workloads.WORKLOADS["125m"]
+    x = workloads.generate(w, with_grad=False)
+    g = to_gpu({n: x[n] for n in ("v", "log_f")})
+    o, lse, ws = acp.forward_projected(q, k, g["v"], g["log_f"], EPS, ws)
+    plan = {n: t.clone() for n, t in acp.plan_views(ws, B, H, L, d, torch.bfloat16).items()}
+    o2, lse2, ws2 = acp.forward(q, k, g["v"], g["log_f"], EPS)
+    plan2 = acp.plan_views(ws2, B, H, L, d, torch.bfloat16)
+    torch.cuda.synchronize()
+    for n in plan:
+        assert torch.equal(plan[n], plan2[n]), n
+    assert torch.equal(o, o2) and torch.equal(lse, lse2)
+    rng = np.random.default_rng(3)
+    rows = np.sort(rng.choice(B * L, 256, replace=False))
+    xs = workloads.to_f64(p["x"][torch.from_numpy(rows)])
+    for got, name in ((q, "wq"), (k, "wk")):
+        wm = workloads.to_f64(p[name])
+        ref = xs @ wm                                  # rows of the product (Sec. 2)
+        bound = np.abs(xs) @ np.abs(wm)
+        gq = got.permute(0, 2, 1, 3).reshape(B * L, H * d)[torch.from_numpy(rows)]
+        err = np.abs(gq.double().cpu().numpy() - ref)
+        assert np.all(err <= 2.0 ** -8 * np.abs(ref) + 1e-5 * bound), float(err.max())
