@@ -303,6 +303,56 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
     }
 }
 
+// ---- head placement -------------------------------------------------------------
+// The attention kernels give each XCD (one L2 each) a contiguous range of heads,
+// so that a head's K and V stay in one L2.  With few heads per XCD, ACP's uneven
+// work per head would leave some XCDs busy long after the others; this kernel
+// orders the heads so that every XCD's range holds the same number of heads and
+// about the same kept-block count: heads sorted by count (largest first), each
+// placed on the least loaded XCD that still has room, each XCD's heads in
+// decreasing count.  order[x * BH / 8 + i] is the i-th head of XCD x.
+constexpr int kOrderMax = 64;
+
+__global__ __launch_bounds__(kOrderMax) void head_order_kernel(
+    const long long* __restrict__ kept, int BH, int* __restrict__ order) {
+    __shared__ int s_sorted[kOrderMax];
+    const int t = threadIdx.x;
+    if (t < BH) {
+        const long long mine = kept[t];
+        int rank = 0;
+        for (int j = 0; j < BH; ++j) {
+            const long long o = kept[j];
+            rank += (o > mine || (o == mine && j < t)) ? 1 : 0;
+        }
+        s_sorted[rank] = t;
+    }
+    __syncthreads();
+    if (t == 0) {
+        const int per = BH / 8;
+        long long load[8];
+        int count[8];
+#pragma unroll
+        for (int x = 0; x < 8; ++x) { load[x] = 0; count[x] = 0; }
+        for (int i = 0; i < BH; ++i) {
+            const int hd = s_sorted[i];
+            int best = -1;
+#pragma unroll
+            for (int x = 0; x < 8; ++x)
+                if (count[x] < per && (best < 0 || load[x] < load[best])) best = x;
+            order[best * per + count[best]] = hd;
+            count[best] += 1;
+            load[best] += kept[hd];
+        }
+    }
+}
+
+bool head_order_enabled(int BH) { return BH % 8 == 0 && BH >= 8 && BH <= kOrderMax; }
+
+hipError_t launch_head_order(const long long* kept, int BH, int* order, hipStream_t s) {
+    hipLaunchKernelGGL(head_order_kernel, dim3(1), dim3(kOrderMax), 0, s, kept, BH, order);
+    return hipGetLastError();
+}
+
 // ---- launchers ---------------------------------------------------------------
 
 template <typename T, int D>

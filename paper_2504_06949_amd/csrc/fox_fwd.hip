@@ -355,11 +355,12 @@ template <int D>
 __global__ __launch_bounds__(kFwdThreads) void fwd_bf16_kernel(
     const __bf16* __restrict__ Q, const __bf16* __restrict__ K, const __bf16* __restrict__ V,
     const float* __restrict__ cg, const int* __restrict__ row_start,
-    const double* __restrict__ bound_u, __bf16* __restrict__ O, float* __restrict__ lse,
-    float* __restrict__ lse2, int L, int M, int nqb, int nblocks, float kscale) {
+    const double* __restrict__ bound_u, const int* __restrict__ order, __bf16* __restrict__ O,
+    float* __restrict__ lse, float* __restrict__ lse2, int L, int M, int nqb, int nblocks,
+    float kscale) {
     __shared__ FwdSmem<D> sm;
     const int lid = xcd_logical_id(blockIdx.x, nblocks);
-    const int bh = lid / nqb;
+    const int bh = order != nullptr ? order[lid / nqb] : lid / nqb;
     const double u_head = bound_u[bh];
     if (u_head <= kUFixedMax)
         fwd_bf16_body<D, true>(sm, lid, bh, u_head, Q, K, V, cg, row_start, O, lse, lse2, L, M,
@@ -437,7 +438,7 @@ static void launch_fwd_bf16(const FwdArgs& a, int M, float kscale, hipStream_t s
     const int nblocks = BH * nqb;
     hipLaunchKernelGGL((fwd_bf16_kernel<D>), dim3(nblocks), dim3(kFwdThreads), 0, s,
                        (const __bf16*)a.Q, (const __bf16*)a.K, (const __bf16*)a.V, a.c,
-                       a.row_start, a.u, (__bf16*)a.O, a.lse, a.lse2, a.L, M, nqb,
+                       a.row_start, a.u, a.order, (__bf16*)a.O, a.lse, a.lse2, a.L, M, nqb,
                        nblocks, kscale);
 }
 
