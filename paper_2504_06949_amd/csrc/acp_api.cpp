@@ -31,7 +31,8 @@ acp_status ok() {
 }
 
 struct Layout {
-    size_t c, u, delta, rs, ce, kept, flags, part, lse2, dsum, rowsum, colsum, order, total;
+    size_t c, u, delta, rs, ce, kept, flags, part, lse2, dsum, rowsum, colsum, sched_q, sched_k,
+        total;
     int nchunk;
 };
 
@@ -57,7 +58,9 @@ Layout layout(int B, int H, int L, int d) {
     y.dsum = take(BHL * 4);
     y.rowsum = take(BHL * 4);
     y.colsum = take(BHL * 4);
-    y.order = take(BH * 4);
+    const size_t nb = ((size_t)L + 127) / 128;   // 128-row blocks of the attention kernels
+    y.sched_q = take(BH * nb * 4);
+    y.sched_k = take(BH * nb * 4);
     y.total = off;
     return y;
 }
@@ -316,11 +319,11 @@ static acp_status fwd_common(const void* Q, const void* K, const void* V, const 
     p.norms_ready = norms_ready;
     hipError_t e = acp::launch_plan(p, (hipStream_t)stream);
     if (e != hipSuccess) return hip_status(e, "fox_attn_fwd boundary launch");
-    const bool ordered = dt == ACP_BF16 && acp::head_order_enabled(B * H);
-    if (ordered) {
-        e = acp::launch_head_order((const long long*)(w + y.kept), B * H, (int*)(w + y.order),
-                                   (hipStream_t)stream);
-        if (e != hipSuccess) return hip_status(e, "fox_attn_fwd head placement launch");
+    if (dt == ACP_BF16) {
+        e = acp::launch_schedule((const long long*)(w + y.kept), (const int*)(w + y.rs),
+                                 (const int*)(w + y.ce), B * H, L / 64, (L + 127) / 128,
+                                 (int*)(w + y.sched_q), (int*)(w + y.sched_k), (hipStream_t)stream);
+        if (e != hipSuccess) return hip_status(e, "fox_attn_fwd schedule launch");
     }
     acp::FwdArgs f{};
     f.Q = Q; f.K = K; f.V = V; f.bf16 = dt == ACP_BF16;
@@ -328,7 +331,7 @@ static acp_status fwd_common(const void* Q, const void* K, const void* V, const 
     f.c = (const float*)(w + y.c);
     f.row_start = (const int*)(w + y.rs);
     f.u = (const double*)(w + y.u);
-    f.order = ordered ? (const int*)(w + y.order) : nullptr;
+    f.sched = (const int*)(w + y.sched_q);
     f.O = O;
     f.lse = lse;
     f.lse2 = (float*)(w + y.lse2);
@@ -410,7 +413,8 @@ acp_status fox_attn_bwd(const void* Q, const void* K, const void* V, const void*
     b.row_start = (const int*)(w + y.rs);
     b.col_end = (const int*)(w + y.ce);
     b.lse2 = (const float*)(w + y.lse2);
-    b.order = dt == ACP_BF16 && acp::head_order_enabled(B * H) ? (const int*)(w + y.order) : nullptr;
+    b.sched_q = (const int*)(w + y.sched_q);
+    b.sched_k = (const int*)(w + y.sched_k);
     b.dsum = (float*)(w + y.dsum);
     b.rowsum = (float*)(w + y.rowsum);
     b.colsum = (float*)(w + y.colsum);

@@ -39,7 +39,7 @@ struct FwdArgs {
     const float* c;
     const int* row_start;
     const double* u;          // [B*H] logit bound U
-    const int* order;         // [B*H] heads in XCD placement order, or null: bh order
+    const int* sched;         // [B*H*nb] query-block schedule (bh * nb + block)
     void* O;
     float* lse;
     float* lse2;
@@ -57,7 +57,8 @@ struct BwdArgs {
     const int* row_start;
     const int* col_end;
     const float* lse2;
-    const int* order;         // as in FwdArgs
+    const int* sched_q;       // query-block schedule (dQ pass)
+    const int* sched_k;       // key-block schedule (dK/dV pass)
     float* dsum;              // Delta (float32 path), then Delta' from the dQ pass
     float* rowsum;
     float* colsum;
@@ -122,10 +123,11 @@ void trace_begin(int kernel, hipStream_t s);
 void trace_end(int kernel, hipStream_t s);
 
 int norm_chunks(int L);
-// Heads are placed on the XCDs by their kept-block counts when there are few per
-// XCD (B*H a multiple of 8, at most 8 heads per XCD); otherwise in bh order.
-bool head_order_enabled(int BH);
-hipError_t launch_head_order(const long long* kept, int BH, int* order, hipStream_t s);
+// Which (head, 128-row block) each logical workgroup id of the attention kernels
+// takes: per XCD, heads placed by kept count when there are few, blocks largest
+// first.  Tables of B*H*nb entries bh * nb + block, nb = ceil(L / 128).
+hipError_t launch_schedule(const long long* kept, const int* row_start, const int* col_end,
+                           int BH, int M, int nb, int* sched_q, int* sched_k, hipStream_t s);
 hipError_t launch_plan(const PlanArgs& a, hipStream_t s);
 hipError_t launch_fwd(const FwdArgs& a, hipStream_t s);
 hipError_t launch_bwd(const BwdArgs& a, hipStream_t s);

@@ -303,53 +303,111 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
     }
 }
 
-// ---- head placement -------------------------------------------------------------
-// The attention kernels give each XCD (one L2 each) a contiguous range of heads,
-// so that a head's K and V stay in one L2.  With few heads per XCD, ACP's uneven
-// work per head would leave some XCDs busy long after the others; this kernel
-// orders the heads so that every XCD's range holds the same number of heads and
-// about the same kept-block count: heads sorted by count (largest first), each
-// placed on the least loaded XCD that still has room, each XCD's heads in
-// decreasing count.  order[x * BH / 8 + i] is the i-th head of XCD x.
-constexpr int kOrderMax = 64;
+// ---- workgroup schedule of the attention kernels ---------------------------------
+// The attention kernels' workgroups each take 128 query rows (forward, dQ) or
+// 128 keys (dK/dV) of one head.  Workgroup ids are dealt round-robin to the 8
+// XCDs; xcd_logical_id turns that into a contiguous range of logical ids per XCD,
+// and this kernel fills, per XCD range, which (head, block) each logical id
+// takes, so that
+//   - a head's workgroups all run on one XCD (its K and V stay in one L2);
+//   - with at most 8 heads per XCD (B*H a multiple of 8, <= 64) the heads are
+//     placed by kept-block count: sorted largest first, each on the least loaded
+//     XCD that still has room (the same number of heads per XCD, so every range
+//     holds whole heads); with more heads per XCD they stay in bh order;
+//   - inside each XCD range the workgroups run largest first (a counting sort
+//     on their kept-tile counts), so that the range ends on small ones.
+// Grid (8, 2): x = XCD, y = 0 for the query-block table, 1 for the key-block one.
+// Entry = bh * nb + block.  Equal counts keep no particular order.
+constexpr int kPlaceMax = 64;
+constexpr int kSchedThreads = 1024;
 
-__global__ __launch_bounds__(kOrderMax) void head_order_kernel(
-    const long long* __restrict__ kept, int BH, int* __restrict__ order) {
-    __shared__ int s_sorted[kOrderMax];
-    const int t = threadIdx.x;
-    if (t < BH) {
-        const long long mine = kept[t];
-        int rank = 0;
-        for (int j = 0; j < BH; ++j) {
-            const long long o = kept[j];
-            rank += (o > mine || (o == mine && j < t)) ? 1 : 0;
+__global__ __launch_bounds__(kSchedThreads) void schedule_kernel(
+    const long long* __restrict__ kept, const int* __restrict__ row_start,
+    const int* __restrict__ col_end, int BH, int M, int nb, int* __restrict__ sched_q,
+    int* __restrict__ sched_k) {
+    __shared__ int s_sorted[kPlaceMax];
+    __shared__ int s_place[kPlaceMax];
+    __shared__ int s_hist[2 * kMaxBlocks + 2];   // a block's count is at most 2M <= 4096
+    const int x = blockIdx.x, table = blockIdx.y, t = threadIdx.x;
+    const bool place = BH % 8 == 0 && BH >= 8 && BH <= kPlaceMax;
+    if (place) {
+        if (t < BH) {
+            const long long mine = kept[t];
+            int rank = 0;
+            for (int j = 0; j < BH; ++j) {
+                const long long o = kept[j];
+                rank += (o > mine || (o == mine && j < t)) ? 1 : 0;
+            }
+            s_sorted[rank] = t;
         }
-        s_sorted[rank] = t;
+        __syncthreads();
+        if (t == 0) {
+            const int per = BH / 8;
+            long long load[8];
+            int count[8];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) { load[i] = 0; count[i] = 0; }
+            for (int i = 0; i < BH; ++i) {
+                const int hd = s_sorted[i];
+                int best = -1;
+#pragma unroll
+                for (int j = 0; j < 8; ++j)
+                    if (count[j] < per && (best < 0 || load[j] < load[best])) best = j;
+                s_place[best * per + count[best]] = hd;
+                count[best] += 1;
+                load[best] += kept[hd];
+            }
+        }
+    }
+    const int nbins = 2 * M + 2;
+    for (int i = t; i < nbins; i += kSchedThreads) s_hist[i] = 0;
+    __syncthreads();
+
+    // this XCD's range of logical ids (as xcd_logical_id deals them)
+    const int nblocks = BH * nb, q = nblocks >> 3, r = nblocks & 7;
+    const int lo = x * q + min(x, r), hi = lo + q + (x < r ? 1 : 0);
+    int* out = table == 0 ? sched_q : sched_k;
+    // the item of a logical id in the unsorted order and its kept-tile count
+    auto item = [&](int lid, int& work) {
+        const int slot = lid / nb, idx = lid % nb;
+        const int bh = place ? s_place[slot] : slot;
+        const int blk = table == 0 ? nb - 1 - idx : idx;   // longest rows / first keys first
+        work = 0;
+        for (int u = 0; u < 2; ++u) {
+            const int m = 2 * blk + u;
+            if (m < M) {
+                work += table == 0 ? m - row_start[(size_t)bh * M + m] + 1
+                                   : col_end[(size_t)bh * M + m] - m + 1;
+            }
+        }
+        return bh * nb + blk;
+    };
+    for (int lid = lo + t; lid < hi; lid += kSchedThreads) {
+        int work;
+        item(lid, work);
+        atomicAdd(&s_hist[work], 1);
     }
     __syncthreads();
-    if (t == 0) {
-        const int per = BH / 8;
-        long long load[8];
-        int count[8];
-#pragma unroll
-        for (int x = 0; x < 8; ++x) { load[x] = 0; count[x] = 0; }
-        for (int i = 0; i < BH; ++i) {
-            const int hd = s_sorted[i];
-            int best = -1;
-#pragma unroll
-            for (int x = 0; x < 8; ++x)
-                if (count[x] < per && (best < 0 || load[x] < load[best])) best = x;
-            order[best * per + count[best]] = hd;
-            count[best] += 1;
-            load[best] += kept[hd];
+    if (t == 0) {   // start of each count's run, largest count first
+        int run = lo;
+        for (int w = nbins - 1; w >= 0; --w) {
+            const int n = s_hist[w];
+            s_hist[w] = run;
+            run += n;
         }
+    }
+    __syncthreads();
+    for (int lid = lo + t; lid < hi; lid += kSchedThreads) {
+        int work;
+        const int it = item(lid, work);
+        out[atomicAdd(&s_hist[work], 1)] = it;
     }
 }
 
-bool head_order_enabled(int BH) { return BH % 8 == 0 && BH >= 8 && BH <= kOrderMax; }
-
-hipError_t launch_head_order(const long long* kept, int BH, int* order, hipStream_t s) {
-    hipLaunchKernelGGL(head_order_kernel, dim3(1), dim3(kOrderMax), 0, s, kept, BH, order);
+hipError_t launch_schedule(const long long* kept, const int* row_start, const int* col_end,
+                           int BH, int M, int nb, int* sched_q, int* sched_k, hipStream_t s) {
+    hipLaunchKernelGGL(schedule_kernel, dim3(8, 2), dim3(kSchedThreads), 0, s, kept, row_start,
+                       col_end, BH, M, nb, sched_q, sched_k);
     return hipGetLastError();
 }
 

@@ -42,15 +42,15 @@ __global__ __launch_bounds__(kBwdThreads) void dq_bf16_kernel(
     const __bf16* __restrict__ O, const __bf16* __restrict__ dO, const float* __restrict__ cg,
     const int* __restrict__ row_start, const float* __restrict__ lse2,
     float* __restrict__ dsum, __bf16* __restrict__ dQ, float* __restrict__ rowsum,
-    const int* __restrict__ order, int L, int M, int nqb, int nblocks, float kscale,
+    const int* __restrict__ sched, int L, int M, int nqb, int nblocks, float kscale,
     float qscale) {
     constexpr int NDS = D / 32;
     constexpr int NDT = D / 16;
     __shared__ DqSmem<D> sm;
 
-    const int lid = xcd_logical_id(blockIdx.x, nblocks);
-    const int bh = order != nullptr ? order[lid / nqb] : lid / nqb;
-    const int qb = nqb - 1 - (lid % nqb);
+    const int item = sched[xcd_logical_id(blockIdx.x, nblocks)];   // bh * nqb + query block
+    const int bh = item / nqb;
+    const int qb = item % nqb;
     const int tid = threadIdx.x, lane = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int g = lane >> 4, r16 = lane & 15;
@@ -328,15 +328,15 @@ __global__ __launch_bounds__(kBwdThreads) void dkdv_bf16_kernel(
     const __bf16* __restrict__ dO, const float* __restrict__ cg,
     const int* __restrict__ col_end, const float* __restrict__ lse2,
     const float* __restrict__ dsum, __bf16* __restrict__ dK, __bf16* __restrict__ dV,
-    float* __restrict__ colsum, const int* __restrict__ order, int L, int M, int nkb,
+    float* __restrict__ colsum, const int* __restrict__ sched, int L, int M, int nkb,
     int nblocks, float kscale, float qscale) {
     constexpr int NDS = D / 32;
     constexpr int NDT = D / 16;
     __shared__ DkvSmem<D> sm;
 
-    const int lid = xcd_logical_id(blockIdx.x, nblocks);
-    const int bh = order != nullptr ? order[lid / nkb] : lid / nkb;
-    const int kb = lid % nkb;                       // first key blocks have the most work
+    const int item = sched[xcd_logical_id(blockIdx.x, nblocks)];   // bh * nkb + key block
+    const int bh = item / nkb;
+    const int kb = item % nkb;
     const int tid = threadIdx.x, lane = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int g = lane >> 4, r16 = lane & 15;
@@ -600,13 +600,13 @@ hipError_t launch_dq_bf16(const BwdArgs& a, hipStream_t s) {
         hipLaunchKernelGGL(dq_bf16_kernel<64>, dim3(nblocks), dim3(kBwdThreads), 0, s,
                            (const __bf16*)a.Q, (const __bf16*)a.K, (const __bf16*)a.V,
                            (const __bf16*)a.O, (const __bf16*)a.dO, a.c, a.row_start, a.lse2,
-                           a.dsum, (__bf16*)a.dQ, a.rowsum, a.order, a.L, M, nqb, nblocks, kscale,
+                           a.dsum, (__bf16*)a.dQ, a.rowsum, a.sched_q, a.L, M, nqb, nblocks, kscale,
                            qscale);
     else
         hipLaunchKernelGGL(dq_bf16_kernel<128>, dim3(nblocks), dim3(kBwdThreads), 0, s,
                            (const __bf16*)a.Q, (const __bf16*)a.K, (const __bf16*)a.V,
                            (const __bf16*)a.O, (const __bf16*)a.dO, a.c, a.row_start, a.lse2,
-                           a.dsum, (__bf16*)a.dQ, a.rowsum, a.order, a.L, M, nqb, nblocks, kscale,
+                           a.dsum, (__bf16*)a.dQ, a.rowsum, a.sched_q, a.L, M, nqb, nblocks, kscale,
                            qscale);
     return hipGetLastError();
 }
@@ -621,13 +621,13 @@ hipError_t launch_dkdv_bf16(const BwdArgs& a, hipStream_t s) {
         hipLaunchKernelGGL(dkdv_bf16_kernel<64>, dim3(nblocks), dim3(kBwdThreads), 0, s,
                            (const __bf16*)a.Q, (const __bf16*)a.K, (const __bf16*)a.V,
                            (const __bf16*)a.dO, a.c, a.col_end, a.lse2, a.dsum,
-                           (__bf16*)a.dK, (__bf16*)a.dV, a.colsum, a.order, a.L, M, nkb,
+                           (__bf16*)a.dK, (__bf16*)a.dV, a.colsum, a.sched_k, a.L, M, nkb,
                            nblocks, kscale, qscale);
     else
         hipLaunchKernelGGL(dkdv_bf16_kernel<128>, dim3(nblocks), dim3(kBwdThreads), 0, s,
                            (const __bf16*)a.Q, (const __bf16*)a.K, (const __bf16*)a.V,
                            (const __bf16*)a.dO, a.c, a.col_end, a.lse2, a.dsum,
-                           (__bf16*)a.dK, (__bf16*)a.dV, a.colsum, a.order, a.L, M, nkb,
+                           (__bf16*)a.dK, (__bf16*)a.dV, a.colsum, a.sched_k, a.L, M, nkb,
                            nblocks, kscale, qscale);
     return hipGetLastError();
 }

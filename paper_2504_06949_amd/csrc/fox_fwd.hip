@@ -59,14 +59,13 @@ struct alignas(1024) FwdSmem {
 
 template <int D, bool kFixed>
 __device__ __forceinline__ void fwd_bf16_body(
-    FwdSmem<D>& sm, int lid, int bh, double u_head,
+    FwdSmem<D>& sm, int qb, int bh, double u_head,
     const __bf16* __restrict__ Q, const __bf16* __restrict__ K, const __bf16* __restrict__ V,
     const float* __restrict__ cg, const int* __restrict__ row_start,
     __bf16* __restrict__ O, float* __restrict__ lse,
     float* __restrict__ lse2, int L, int M, int nqb, float kscale) {
     constexpr int NDS = D / 32;                     // k-steps over the head dim
     constexpr int NDT = D / 16;                     // output tiles over the head dim
-    const int qb = nqb - 1 - (lid % nqb);           // longest rows first
     const int tid = threadIdx.x, lane = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int g = lane >> 4, r16 = lane & 15;
@@ -355,19 +354,19 @@ template <int D>
 __global__ __launch_bounds__(kFwdThreads) void fwd_bf16_kernel(
     const __bf16* __restrict__ Q, const __bf16* __restrict__ K, const __bf16* __restrict__ V,
     const float* __restrict__ cg, const int* __restrict__ row_start,
-    const double* __restrict__ bound_u, const int* __restrict__ order, __bf16* __restrict__ O,
+    const double* __restrict__ bound_u, const int* __restrict__ sched, __bf16* __restrict__ O,
     float* __restrict__ lse, float* __restrict__ lse2, int L, int M, int nqb, int nblocks,
     float kscale) {
     __shared__ FwdSmem<D> sm;
-    const int lid = xcd_logical_id(blockIdx.x, nblocks);
-    const int bh = order != nullptr ? order[lid / nqb] : lid / nqb;
+    const int item = sched[xcd_logical_id(blockIdx.x, nblocks)];   // bh * nqb + query block
+    const int bh = item / nqb;
     const double u_head = bound_u[bh];
     if (u_head <= kUFixedMax)
-        fwd_bf16_body<D, true>(sm, lid, bh, u_head, Q, K, V, cg, row_start, O, lse, lse2, L, M,
-                               nqb, kscale);
+        fwd_bf16_body<D, true>(sm, item % nqb, bh, u_head, Q, K, V, cg, row_start, O, lse, lse2,
+                               L, M, nqb, kscale);
     else
-        fwd_bf16_body<D, false>(sm, lid, bh, u_head, Q, K, V, cg, row_start, O, lse, lse2, L, M,
-                                nqb, kscale);
+        fwd_bf16_body<D, false>(sm, item % nqb, bh, u_head, Q, K, V, cg, row_start, O, lse, lse2,
+                                L, M, nqb, kscale);
 }
 
 // ---------------------------------------------------------------------------
@@ -438,7 +437,7 @@ static void launch_fwd_bf16(const FwdArgs& a, int M, float kscale, hipStream_t s
     const int nblocks = BH * nqb;
     hipLaunchKernelGGL((fwd_bf16_kernel<D>), dim3(nblocks), dim3(kFwdThreads), 0, s,
                        (const __bf16*)a.Q, (const __bf16*)a.K, (const __bf16*)a.V, a.c,
-                       a.row_start, a.u, a.order, (__bf16*)a.O, a.lse, a.lse2, a.L, M, nqb,
+                       a.row_start, a.u, a.sched, (__bf16*)a.O, a.lse, a.lse2, a.L, M, nqb,
                        nblocks, kscale);
 }
 
