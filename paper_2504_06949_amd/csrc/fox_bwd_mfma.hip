@@ -37,7 +37,8 @@ struct alignas(1024) DqSmem {
 };
 
 template <int D>
-__global__ __launch_bounds__(kBwdThreads) void dq_bf16_kernel(
+__global__ __launch_bounds__(kBwdThreads) __attribute__((amdgpu_waves_per_eu(D == 64 ? 3 : 1)))
+void dq_bf16_kernel(
     const __bf16* __restrict__ Q, const __bf16* __restrict__ K, const __bf16* __restrict__ V,
     const __bf16* __restrict__ O, const __bf16* __restrict__ dO, const float* __restrict__ cg,
     const int* __restrict__ row_start, const float* __restrict__ lse2,
@@ -128,7 +129,9 @@ __global__ __launch_bounds__(kBwdThreads) void dq_bf16_kernel(
     f32x4 sinit[2], dinit[2];
 #pragma unroll
     for (int qt = 0; qt < 2; ++qt) {
-        const float a = aq[qt] / kscale, b = -dl[qt];
+        const float a = aq[qt] / kscale;
+        float b = -dl[qt];
+        asm volatile("" : "+v"(b));   // the epilogue reads -Delta_i back from dinit
         sinit[qt] = f32x4{a, a, a, a};
         dinit[qt] = f32x4{b, b, b, b};
     }
@@ -136,9 +139,12 @@ __global__ __launch_bounds__(kBwdThreads) void dq_bf16_kernel(
 
     // Each key tile is taken in two halves of 32 keys, each in three phases: A
     // forms S^T and dP^T (MFMA; key rows from LDS), B the softmax terms (VALU),
-    // C accumulates dQ (MFMA; key columns from LDS).  As in the dK/dV pass, each
-    // LDS operand is read one phase before it is used, and the barrier that
-    // publishes the next tile sits before the second half's phase C.
+    // C accumulates dQ (MFMA; key columns from LDS).  At d = 64 each phase reads
+    // its own LDS operands, so that the kernel fits 168 VGPRs: three waves per
+    // SIMD, whose interleaving hides the LDS latency.  At d = 128 (one wave per
+    // SIMD) each LDS operand is read one phase before it is used, as in the
+    // dK/dV pass, and the barrier that publishes the next tile sits before the
+    // second half's phase C.
     struct OpA {
         bf16x8 a[2][NDS], b[2][NDS];
         float4 lo, hi;                 // key biases of the lane's 8 keys
@@ -236,10 +242,41 @@ __global__ __launch_bounds__(kBwdThreads) void dq_bf16_kernel(
     __syncthreads();
     float4 cnext = make_float4(0.f, 0.f, 0.f, 0.f);
     if (n_lo < n_hi) cnext = issue(n_lo + 1, 1);
+    int buf = 0;
+    if constexpr (D == 64) {
+    auto step = [&](auto mask_tag, int n) __attribute__((always_inline)) {
+        const bool act = n >= w_lo && n <= mw;
+        const int qk0 = 32 * (w & 1) + r16 - 8 * g + (n == mw ? 0 : 4096);
+        if (act) {
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const OpA ra = load_a(buf, h);
+                const SdP x = phase_a(ra);
+                const DsH y = phase_b(mask_tag, x, ra, h, qk0);
+                const OpC rc = load_c(buf, h);
+                phase_c(rc, y);
+            }
+        }
+        if (n < n_hi) put_kb(cnext, buf ^ 1);
+        // tile n + 1 has landed and every wave's reads of tile n are complete
+        wait_vmcnt0_lgkmcnt0();
+        __syncthreads();
+        const bool more = n + 1 < n_hi;
+        if (more && tid < 16) cnext = *reinterpret_cast<const float4*>(cg + head + 64 * (n + 2) + 4 * tid);
+        if (more) dma.issue(sm.k[buf], K + (head + (size_t)64 * (n + 2)) * D, w);
+        if (more) dma.issue(sm.v[buf], V + (head + (size_t)64 * (n + 2)) * D, w);
+        buf ^= 1;
+    };
+    // The diagonal tiles (m0 for waves 0-1, m0 + 1 = n_hi for waves 2-3) are the
+    // last two and go through the masking variant.
+    const int n_mask = max(n_lo, n_hi - 1);
+    int n = n_lo;
+    for (; n < n_mask; ++n) step(std::false_type{}, n);
+    for (; n <= n_hi; ++n) step(std::true_type{}, n);
+    } else {
     // (read whether or not this wave takes the tile: no path keeps an older set
     // of them live through the loop)
     OpA ra = load_a(0, 0);
-    int buf = 0;
     auto step = [&](auto mask_tag, int n) __attribute__((always_inline)) {
         const bool act = n >= w_lo && n <= mw;
         const int qk0 = 32 * (w & 1) + r16 - 8 * g + (n == mw ? 0 : 4096);
@@ -277,6 +314,7 @@ __global__ __launch_bounds__(kBwdThreads) void dq_bf16_kernel(
     int n = n_lo;
     for (; n < n_mask; ++n) step(std::false_type{}, n);
     for (; n <= n_hi; ++n) step(std::true_type{}, n);
+    }
 
     if (!wave_on) return;
 #pragma unroll
@@ -301,7 +339,7 @@ __global__ __launch_bounds__(kBwdThreads) void dq_bf16_kernel(
         a += __shfl_xor(a, 16);
         a += __shfl_xor(a, 32);
         if (g == 0) {
-            dsum[head + query] = a + dl[qt];
+            dsum[head + query] = a - dinit[qt][0];
             rowsum[head + query] = 0.f;
         }
     }

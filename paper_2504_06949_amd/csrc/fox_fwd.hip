@@ -140,9 +140,10 @@ __device__ __forceinline__ void fwd_bf16_body(
 
     // Each key tile is taken in three phases: A forms S^T (MFMA; key rows and
     // key biases from LDS), B the weights P (VALU), C accumulates O^T (MFMA; V^T
-    // columns from LDS).  Every LDS operand is read one phase before it is used:
-    // the V^T columns during phase A, the next tile's key rows during phase C,
-    // which runs after the barrier that publishes that tile.
+    // columns from LDS).  Each phase reads its LDS operands itself, holding no
+    // operand across a phase: that keeps the kernel within 168 VGPRs at d = 64
+    // (three waves per SIMD, whose interleaving hides the LDS latency) and 256
+    // at d = 128 (two waves).
     struct OpA {
         bf16x8 a[4][NDS];
         float4 nk[4];   // key biases of the lane's keys 32 ks + 8 g + (0..3 | 4..7)
@@ -259,10 +260,10 @@ __device__ __forceinline__ void fwd_bf16_body(
         }
         return pt;
     };
-    // O^T += V^T P^T, head-dim tiles [part NDT/2, (part + 1) NDT/2)
-    auto phase_c_part = [&](const OpC& rc, const PTile& pt, int part) __attribute__((always_inline)) {
+    // O^T += V^T P^T
+    auto phase_c = [&](const OpC& rc, const PTile& pt) __attribute__((always_inline)) {
 #pragma unroll
-        for (int dt = part * NDT / 2; dt < (part + 1) * NDT / 2; ++dt)
+        for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
             for (int ks = 0; ks < 2; ++ks) {
                 acc[0][dt] = mfma16(rc.v[dt][ks], pt.p[0][ks], acc[0][dt]);
@@ -276,33 +277,24 @@ __device__ __forceinline__ void fwd_bf16_body(
     __syncthreads();
     float4 cnext = make_float4(0.f, 0.f, 0.f, 0.f);
     if (n_lo < n_hi) cnext = issue(n_lo + 1, 1);
-    // (read whether or not this wave takes the tile: no path keeps an older set
-    // of them live through the loop)
-    OpA ra = load_a(0);
     int buf = 0;
     auto step = [&](auto mask_tag, int n) __attribute__((always_inline)) {
         const bool act = n >= w_lo && n <= mw;
         const int qk0 = 32 * (w & 1) + r16 - 8 * g + (n == mw ? 0 : 4096);
-        OpC rc;
-        PTile pt;
         if (act) {
-            rc = load_c(buf);
+            const OpA ra = load_a(buf);
             const STile x = phase_a(ra);
-            pt = phase_b(mask_tag, x, ra, qk0);
+            const PTile pt = phase_b(mask_tag, x, ra, qk0);
+            const OpC rc = load_c(buf);
+            phase_c(rc, pt);
         }
         if (n < n_hi) put_kb(cnext, buf ^ 1);
         // tile n + 1 has landed and every wave's reads of tile n are complete
         wait_vmcnt0_lgkmcnt0();
         __syncthreads();
-        // The next tile's loads are spread over this tile's last MFMAs: issued in
-        // one clump right after the barrier, the four waves' DMA instructions
-        // queue for the CU's address unit and stall the waves' issue.
         const bool more = n + 1 < n_hi;
         if (more && tid < 16) cnext = *reinterpret_cast<const float4*>(cg + head + 64 * (n + 2) + 4 * tid);
-        if (n < n_hi) ra = load_a(buf ^ 1);
-        if (act) phase_c_part(rc, pt, 0);
         if (more) dma.issue(sm.k[buf], K + (head + (size_t)64 * (n + 2)) * D, w);
-        if (act) phase_c_part(rc, pt, 1);
         if (more) dma.issue(sm.v[buf], V + (head + (size_t)64 * (n + 2)) * D, w);
         buf ^= 1;
     };
@@ -351,7 +343,8 @@ __device__ __forceinline__ void fwd_bf16_body(
 // One launch for both variants: the head's bound picks the body (uniform over
 // the workgroup), and the two bodies share the workgroup's LDS.
 template <int D>
-__global__ __launch_bounds__(kFwdThreads) void fwd_bf16_kernel(
+__global__ __launch_bounds__(kFwdThreads) __attribute__((amdgpu_waves_per_eu(D == 64 ? 3 : 2)))
+void fwd_bf16_kernel(
     const __bf16* __restrict__ Q, const __bf16* __restrict__ K, const __bf16* __restrict__ V,
     const float* __restrict__ cg, const int* __restrict__ row_start,
     const double* __restrict__ bound_u, const int* __restrict__ sched, __bf16* __restrict__ O,
