@@ -81,6 +81,11 @@ typedef struct {
     size_t col_end;    /* [B,H,M]  int32   last query block that keeps each key block */
     size_t kept;       /* [B,H]    int64   kept 64 x 64 blocks (diagonal included)   */
     size_t flags;      /* [B,H]    int32   data-error bits, see above                */
+    size_t sched_q;    /* [B*H*nb] int32  workgroup schedule of the bf16 forward and dQ
+                        * pass (nb = ceil(L / 128)): entry i = bh * nb + the 128-row
+                        * query block that logical workgroup i runs; logical ids are
+                        * split into 8 contiguous ranges, one per XCD                */
+    size_t sched_k;    /* [B*H*nb] int32  the same for the dK/dV pass (key blocks)    */
     size_t total;      /* bytes in use = acp_workspace_size()                        */
 } acp_plan_layout;
 

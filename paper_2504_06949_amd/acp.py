@@ -36,7 +36,8 @@ class AcpError(RuntimeError):
 
 class PlanLayout(ctypes.Structure):
     _fields_ = [(n, ctypes.c_size_t) for n in
-                ("c", "bound_u", "delta", "row_start", "col_end", "kept", "flags", "total")]
+                ("c", "bound_u", "delta", "row_start", "col_end", "kept", "flags", "sched_q",
+                 "sched_k", "total")]
 
 
 class DecodeLayout(ctypes.Structure):
@@ -412,6 +413,7 @@ def plan_views(ws: torch.Tensor, B: int, H: int, L: int, d: int, dtype) -> dict:
     dt = ACP_F32 if dtype == torch.float32 else ACP_BF16
     lay = acp_plan_offsets(B, H, L, d, dt)
     M = L // 64
+    nb = (L + 127) // 128
 
     def view(off, n, t):
         nbytes = n * torch.empty((), dtype=t).element_size()
@@ -425,6 +427,8 @@ def plan_views(ws: torch.Tensor, B: int, H: int, L: int, d: int, dtype) -> dict:
         "col_end": view(lay.col_end, B * H * M, torch.int32).view(B, H, M),
         "kept": view(lay.kept, B * H, torch.int64).view(B, H),
         "flags": view(lay.flags, B * H, torch.int32).view(B, H),
+        "sched_q": view(lay.sched_q, B * H * nb, torch.int32),
+        "sched_k": view(lay.sched_k, B * H * nb, torch.int32),
     }
 
 

@@ -231,6 +231,8 @@ acp_status acp_plan_offsets(int B, int H, int L, int d, acp_dtype dt, acp_plan_l
     out->col_end = y.ce;
     out->kept = y.kept;
     out->flags = y.flags;
+    out->sched_q = y.sched_q;
+    out->sched_k = y.sched_k;
     out->total = y.total;
     return ok();
 }

@@ -328,36 +328,45 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(
     __shared__ int s_sorted[kPlaceMax];
     __shared__ int s_place[kPlaceMax];
     __shared__ int s_hist[2 * kMaxBlocks + 2];   // a block's count is at most 2M <= 4096
+    __shared__ double s_wave[kPlanWaves];
+    static_assert(kSchedThreads == kPlanThreads, "block_inclusive_scan takes 1024 threads");
     const int x = blockIdx.x, table = blockIdx.y, t = threadIdx.x;
     const bool place = BH % 8 == 0 && BH >= 8 && BH <= kPlaceMax;
-    if (place) {
-        if (t < BH) {
-            const long long mine = kept[t];
-            int rank = 0;
-            for (int j = 0; j < BH; ++j) {
-                const long long o = kept[j];
-                rank += (o > mine || (o == mine && j < t)) ? 1 : 0;
-            }
-            s_sorted[rank] = t;
+    if (place && t < 64) {
+        // Wave 0 alone: rank the heads by kept count (largest first, ties by
+        // index), then place them in that order.  Lanes 0-7 hold the load and head
+        // count of XCD 0-7; each step takes the least loaded XCD with room (lowest
+        // index on ties) as the minimum of load << 3 | xcd over lanes 0-7.  A head
+        // keeps at most M (M + 1) / 2 < 2^22 blocks and an XCD at most 8 heads, so
+        // the key fits 32 bits.  (A single wave's LDS accesses complete in order,
+        // so no barrier is needed between its write and read of s_sorted.)
+        const int kt_l = t < BH ? (int)min(max(kept[t], 0ll), 1ll << 22) : 0;
+        int rank = 0;
+        for (int j = 0; j < BH; ++j) {
+            const int kj = __builtin_amdgcn_readlane(kt_l, j);
+            rank += (kj > kt_l || (kj == kt_l && j < t)) ? 1 : 0;
         }
-        __syncthreads();
-        if (t == 0) {
-            const int per = BH / 8;
-            long long load[8];
-            int count[8];
-#pragma unroll
-            for (int i = 0; i < 8; ++i) { load[i] = 0; count[i] = 0; }
-            for (int i = 0; i < BH; ++i) {
-                const int hd = s_sorted[i];
-                int best = -1;
-#pragma unroll
-                for (int j = 0; j < 8; ++j)
-                    if (count[j] < per && (best < 0 || load[j] < load[best])) best = j;
-                s_place[best * per + count[best]] = hd;
-                count[best] += 1;
-                load[best] += kept[hd];
+        if (t < BH) s_sorted[rank] = t;
+        const int hd_l = t < BH ? s_sorted[t] : 0;
+        const int k_l = __shfl(kt_l, hd_l);
+        const int per = BH / 8;
+        unsigned load = 0u;
+        int count = 0, mypos = 0;
+        for (int i = 0; i < BH; ++i) {
+            unsigned key = t < 8 && count < per ? (load << 3) | (unsigned)t : 0xffffffffu;
+            // minimum over each group of 8 lanes: swap neighbours, pairs, quads
+            key = min(key, (unsigned)__builtin_amdgcn_mov_dpp((int)key, 0xB1, 0xF, 0xF, false));
+            key = min(key, (unsigned)__builtin_amdgcn_mov_dpp((int)key, 0x4E, 0xF, 0xF, false));
+            key = min(key, (unsigned)__builtin_amdgcn_mov_dpp((int)key, 0x141, 0xF, 0xF, false));
+            const int best = (int)((unsigned)__builtin_amdgcn_readfirstlane((int)key) & 7u);
+            const int pos = per * best + __builtin_amdgcn_readlane(count, best);
+            if (t == best) {
+                count += 1;
+                load += (unsigned)__builtin_amdgcn_readlane(k_l, i);
             }
+            if (t == i) mypos = pos;
         }
+        if (t < BH) s_place[mypos] = hd_l;
     }
     const int nbins = 2 * M + 2;
     for (int i = t; i < nbins; i += kSchedThreads) s_hist[i] = 0;
@@ -388,12 +397,26 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(
         atomicAdd(&s_hist[work], 1);
     }
     __syncthreads();
-    if (t == 0) {   // start of each count's run, largest count first
-        int run = lo;
-        for (int w = nbins - 1; w >= 0; --w) {
-            const int n = s_hist[w];
-            s_hist[w] = run;
-            run += n;
+    {
+        // start of each count's run, largest count first: the bins in descending
+        // order, thread t owning positions [kPer t, kPer t + kPer) of that order
+        constexpr int kPer = (2 * kMaxBlocks + 2 + kSchedThreads - 1) / kSchedThreads;
+        int cnt[kPer];
+        int tot = 0;
+#pragma unroll
+        for (int i = 0; i < kPer; ++i) {
+            const int e = kPer * t + i;
+            cnt[i] = e < nbins ? s_hist[nbins - 1 - e] : 0;
+            tot += cnt[i];
+        }
+        // (the scan's barriers also order every thread's reads above before the
+        // writes below)
+        int run = lo + (int)block_inclusive_scan((double)tot, s_wave) - tot;
+#pragma unroll
+        for (int i = 0; i < kPer; ++i) {
+            const int e = kPer * t + i;
+            if (e < nbins) s_hist[nbins - 1 - e] = run;
+            run += cnt[i];
         }
     }
     __syncthreads();

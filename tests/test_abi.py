@@ -40,11 +40,14 @@ def test_workspace_size_and_layout():
     lay = acp.acp_plan_offsets(8, 12, 4096, 64, acp.ACP_BF16)
     assert lay.total == n
     offs = [lay.c, lay.bound_u, lay.delta, lay.row_start, lay.col_end, lay.kept,
-            lay.flags]
+            lay.flags, lay.sched_q, lay.sched_k]
     assert all(o % 256 == 0 for o in offs)
     assert offs == sorted(offs) and len(set(offs)) == len(offs)
     BHL = 8 * 12 * 4096
     assert lay.bound_u - lay.c >= 4 * BHL
+    # the two workgroup schedules: one int32 per (head, 128-row block)
+    assert lay.sched_k - lay.sched_q >= 4 * 8 * 12 * 32
+    assert lay.total - lay.sched_k >= 4 * 8 * 12 * 32
     # five float32 rows per position (c, L_i, Delta', row and column sums of dS)
     # dominate, and nothing scales with the head dim
     assert n >= 5 * 4 * BHL
