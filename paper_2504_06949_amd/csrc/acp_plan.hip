@@ -17,58 +17,89 @@
 
 namespace acp {
 
-constexpr int kNormRows = 128;  // rows per norm workgroup, one per thread
+constexpr int kNormRows = 128;     // rows per chunk (one float64 maximum each)
+constexpr int kNormThreads = 256;  // a workgroup takes two chunks per step, a thread per row
 
+// LDS of one workgroup of rownorm_max_kernel: two chunks, rows padded by 16 bytes
 template <typename T, int D>
-__global__ __launch_bounds__(kNormRows) void rownorm_max_kernel(
-    const T* __restrict__ Q, const T* __restrict__ K, int L, int nchunk,
+constexpr int norm_lds_bytes() { return 2 * kNormRows * (D * (int)sizeof(T) + 16); }
+
+// Persistent over pairs of chunks: while a pair is reduced from LDS, the next
+// pair's rows are already on their way into registers.  Chunk u of the grid is
+// (bh, which, chunk) with u = (2 bh + which) nchunk + chunk, which is also its
+// slot in part.
+template <typename T, int D>
+__global__ __launch_bounds__(kNormThreads) void rownorm_max_kernel(
+    const T* __restrict__ Q, const T* __restrict__ K, int BH, int L, int nchunk,
     double* __restrict__ part) {
     constexpr int kRowBytes = D * (int)sizeof(T);
-    constexpr int kChunks = kRowBytes / 16;   // 16-byte pieces per row
+    constexpr int kPieces = kRowBytes / 16;   // 16-byte pieces per row (and per thread)
     constexpr int kStride = kRowBytes + 16;   // padded LDS row (spreads banks)
     constexpr int kPer = 16 / (int)sizeof(T); // elements per piece
-    __shared__ __attribute__((aligned(16))) unsigned char tile[kNormRows * kStride];
-    __shared__ double wave_max[kNormRows / 64];
+    __shared__ __attribute__((aligned(16))) unsigned char tile[2][kNormRows * kStride];
+    __shared__ double wave_max[kNormThreads / 64];
 
-    const int chunk = blockIdx.x, bh = blockIdx.y, which = blockIdx.z;
-    const int row0 = chunk * kNormRows;
-    const int rows = min(kNormRows, L - row0);
-    const T* X = (which == 0 ? Q : K) + ((size_t)bh * L + row0) * D;
-    const unsigned char* src = reinterpret_cast<const unsigned char*>(X);
-
-    // Coalesced copy of the chunk into LDS, one padded row per query/key.
-    for (int i = threadIdx.x; i < rows * kChunks; i += kNormRows) {
-        const uint4 v = *reinterpret_cast<const uint4*>(src + (size_t)i * 16);
-        *reinterpret_cast<uint4*>(tile + (i / kChunks) * kStride + (i % kChunks) * 16) = v;
-    }
-    __syncthreads();
-
-    // Each thread: sum of squares of its row in ascending feature order, in
-    // float64.  Squares of float32/bfloat16 values are exact in float64, so
-    // fma(x, x, acc) rounds exactly like acc + x*x.
-    double acc = 0.0;
-    if ((int)threadIdx.x < rows) {
-        const unsigned char* rp = tile + threadIdx.x * kStride;
-        for (int ch = 0; ch < kChunks; ++ch) {
-            const uint4 v = *reinterpret_cast<const uint4*>(rp + ch * 16);
-            const T* e = reinterpret_cast<const T*>(&v);
+    const int tid = threadIdx.x, half = tid >> 7, r = tid & (kNormRows - 1);
+    const int npairs = BH * nchunk;           // 2 BH nchunk chunks
+    auto chunk_of = [&](int p, const unsigned char*& src, int& rows) {
+        const int u = 2 * p + half;
+        const int bh = u / (2 * nchunk), which = (u / nchunk) & 1, c = u % nchunk;
+        const T* X = (which == 0 ? Q : K) + ((size_t)bh * L + (size_t)c * kNormRows) * D;
+        src = reinterpret_cast<const unsigned char*>(X);
+        rows = min(kNormRows, L - c * kNormRows);
+        return u;
+    };
+    // Thread r of a half loads pieces r, r + 128, ... of its chunk (coalesced).
+    uint4 buf[kPieces];
+    auto load = [&](int p) __attribute__((always_inline)) {
+        const unsigned char* src;
+        int rows;
+        chunk_of(p, src, rows);
 #pragma unroll
-            for (int t = 0; t < kPer; ++t) {
-                const double x = to_f64(e[t]);
-                acc = __builtin_fma(x, x, acc);
+        for (int k = 0; k < kPieces; ++k) {
+            const int i = r + kNormRows * k;
+            buf[k] = i < rows * kPieces ? *reinterpret_cast<const uint4*>(src + (size_t)i * 16)
+                                        : make_uint4(0u, 0u, 0u, 0u);
+        }
+    };
+    int p = blockIdx.x;
+    if (p < npairs) load(p);
+    for (; p < npairs; p += gridDim.x) {
+        const unsigned char* src;
+        int rows;
+        const int u = chunk_of(p, src, rows);
+        __syncthreads();                      // the previous pair's tile reads are done
+#pragma unroll
+        for (int k = 0; k < kPieces; ++k) {
+            const int i = r + kNormRows * k;
+            *reinterpret_cast<uint4*>(tile[half] + (i / kPieces) * kStride + (i % kPieces) * 16) = buf[k];
+        }
+        if (p + (int)gridDim.x < npairs) load(p + gridDim.x);
+        __syncthreads();
+
+        // Each thread: sum of squares of its row in ascending feature order, in
+        // float64.  Squares of float32/bfloat16 values are exact in float64, so
+        // fma(x, x, acc) rounds exactly like acc + x*x.
+        double acc = 0.0;
+        if (r < rows) {
+            const unsigned char* rp = tile[half] + r * kStride;
+            for (int ch = 0; ch < kPieces; ++ch) {
+                const uint4 v = *reinterpret_cast<const uint4*>(rp + ch * 16);
+                const T* e = reinterpret_cast<const T*>(&v);
+#pragma unroll
+                for (int t = 0; t < kPer; ++t) {
+                    const double x = to_f64(e[t]);
+                    acc = __builtin_fma(x, x, acc);
+                }
             }
         }
-    }
-    // max over the workgroup (order-free)
-    double m = acc;
+        // max over the chunk's rows (order-free), two waves per chunk
+        double m = acc;
 #pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) m = nan_max(m, __shfl_xor(m, off));
-    if ((threadIdx.x & 63) == 0) wave_max[threadIdx.x >> 6] = m;
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        double r = wave_max[0];
-        for (int w = 1; w < kNormRows / 64; ++w) r = nan_max(r, wave_max[w]);
-        part[((size_t)bh * 2 + which) * nchunk + chunk] = r;
+        for (int off = 32; off >= 1; off >>= 1) m = nan_max(m, __shfl_xor(m, off));
+        if ((tid & 63) == 0) wave_max[tid >> 6] = m;
+        __syncthreads();
+        if (r == 0) part[u] = nan_max(wave_max[2 * half], wave_max[2 * half + 1]);
     }
 }
 
@@ -439,8 +470,11 @@ hipError_t launch_schedule(const long long* kept, const int* row_start, const in
 template <typename T, int D>
 static hipError_t launch_norm_t(const void* Q, const void* K, int BH, int L, int nchunk,
                                 double* part, hipStream_t s) {
-    hipLaunchKernelGGL((rownorm_max_kernel<T, D>), dim3(nchunk, BH, 2), dim3(kNormRows), 0, s,
-                       (const T*)Q, (const T*)K, L, nchunk, part);
+    // as many workgroups as the CUs hold at once (LDS-bound), at most one per pair
+    const int per_cu = (160 * 1024) / norm_lds_bytes<T, D>();
+    const int grid = min(BH * nchunk, 256 * per_cu);
+    hipLaunchKernelGGL((rownorm_max_kernel<T, D>), dim3(grid), dim3(kNormThreads), 0, s,
+                       (const T*)Q, (const T*)K, BH, L, nchunk, part);
     return hipGetLastError();
 }
 

@@ -41,3 +41,20 @@ def oracle_head(x: dict, b: int, h: int, eps: float, grads: bool = True, method=
 
 def f64(t: torch.Tensor) -> np.ndarray:
     return t.detach().float().cpu().numpy().astype(np.float64)
+
+
+def assert_same_plan(plan: dict, plan2: dict):
+    """Two plans of the same inputs: every field bit for bit, except that the
+    workgroup schedules (sched_q, sched_k) only fix which items each XCD's range
+    of logical ids holds, not their order among items of equal work."""
+    nblocks = plan["sched_q"].numel()
+    q, r = divmod(nblocks, 8)
+    for n in plan:
+        if n.startswith("sched"):
+            a, b = plan[n].cpu(), plan2[n].cpu()
+            for x in range(8):
+                lo = x * q + min(x, r)
+                hi = lo + q + (1 if x < r else 0)
+                assert torch.equal(a[lo:hi].sort().values, b[lo:hi].sort().values), (n, x)
+        else:
+            assert torch.equal(plan[n], plan2[n]), n

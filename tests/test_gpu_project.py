@@ -8,7 +8,7 @@ import torch
 
 import oracle as orc
 from paper_2504_06949_amd import acp, workloads
-from tests._helpers import EPS, ensure_built, to_gpu
+from tests._helpers import EPS, assert_same_plan, ensure_built, to_gpu
 
 pytestmark = pytest.mark.gpu
 
@@ -49,8 +49,7 @@ def test_projection_and_projected_forward(B, L, Dm, H, d):
     o2, lse2, ws2 = acp.forward(q, k, g["v"], g["log_f"], EPS)
     plan2 = acp.plan_views(ws2, B, H, L, d, torch.bfloat16)
     torch.cuda.synchronize()
-    for n in plan:
-        assert torch.equal(plan[n], plan2[n]), n
+    assert_same_plan(plan, plan2)
     assert torch.equal(o, o2) and torch.equal(lse, lse2)
     # U from the oracle's norms of the stored Q and K, bit for bit
     qn, kn = q.float().cpu().numpy(), k.float().cpu().numpy()
@@ -83,8 +82,7 @@ def test_projection_at_the_bench_shape_sampled():
     o2, lse2, ws2 = acp.forward(q, k, g["v"], g["log_f"], EPS)
     plan2 = acp.plan_views(ws2, B, H, L, d, torch.bfloat16)
     torch.cuda.synchronize()
-    for n in plan:
-        assert torch.equal(plan[n], plan2[n]), n
+    assert_same_plan(plan, plan2)
     assert torch.equal(o, o2) and torch.equal(lse, lse2)
     rng = np.random.default_rng(3)
     rows = np.sort(rng.choice(B * L, 256, replace=False))
