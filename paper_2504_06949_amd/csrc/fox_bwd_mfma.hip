@@ -10,7 +10,7 @@
 // Both passes use 4 waves of 32 rows (two 64-row pruning blocks per workgroup),
 // so a pruned or non-causal tile is skipped wave-uniformly, and work through
 // each 64-row tile of the other operand in two halves of 32 to keep register
-// pressure low.  Tiles are double-buffered in LDS (swizzled panels filled by DMA
+// pressure low.  At d = 64 both fit 168 VGPRs, i.e. three waves per SIMD.  Tiles are double-buffered in LDS (swizzled panels filled by DMA
 // loads while the previous tile is computed); operands whose contraction runs
 // over sequence positions come from LDS transpose reads.
 #include <type_traits>
@@ -358,10 +358,13 @@ struct alignas(1024) DkvSmem {
     unsigned char o[2][128 * D];   // dO
     float la[2][64];               // a_i / k',  a_i = (c_i - r) log2(e) - L_i
     float dl[2][64];               // -Delta'_i
+    // d = 64: the workgroup's 128 keys (two tiles), read as the B operand of S
+    unsigned char k[D == 64 ? 2 : 1][D == 64 ? 128 * D : 16];
 };
 
 template <int D>
-__global__ __launch_bounds__(kBwdThreads) void dkdv_bf16_kernel(
+__global__ __launch_bounds__(kBwdThreads) __attribute__((amdgpu_waves_per_eu(D == 64 ? 3 : 1)))
+void dkdv_bf16_kernel(
     const __bf16* __restrict__ Q, const __bf16* __restrict__ K, const __bf16* __restrict__ V,
     const __bf16* __restrict__ dO, const float* __restrict__ cg,
     const int* __restrict__ col_end, const float* __restrict__ lse2,
@@ -390,7 +393,8 @@ __global__ __launch_bounds__(kBwdThreads) void dkdv_bf16_kernel(
     const float kinv = 1.0f / kscale;
     const float cref = cg[head + k0];
 
-    bf16x8 kf[2][NDS], vf[2][NDS];
+    constexpr bool kKinLds = D == 64;
+    bf16x8 kf[2][NDS], vf[2][NDS];   // kf unused at d = 64 (K is in LDS)
     float nk[2] = {0.f, 0.f};
     if (wave_on) {
 #pragma unroll
@@ -398,7 +402,8 @@ __global__ __launch_bounds__(kBwdThreads) void dkdv_bf16_kernel(
             const size_t row = head + wk0 + 16 * kt + r16;
 #pragma unroll
             for (int ds = 0; ds < NDS; ++ds) {
-                kf[kt][ds] = *reinterpret_cast<const bf16x8*>(K + row * D + 32 * ds + 8 * g);
+                if constexpr (!kKinLds)
+                    kf[kt][ds] = *reinterpret_cast<const bf16x8*>(K + row * D + 32 * ds + 8 * g);
                 vf[kt][ds] = *reinterpret_cast<const bf16x8*>(V + row * D + 32 * ds + 8 * g);
             }
             nk[kt] = -((cg[row] - cref) * kLog2e);
@@ -444,11 +449,13 @@ __global__ __launch_bounds__(kBwdThreads) void dkdv_bf16_kernel(
     // Each query tile is taken in two halves of 32 queries, each in three
     // phases: A forms S and dP (MFMA; query rows and the accumulator starts from
     // LDS), B the softmax terms (VALU), C accumulates dV and dK (MFMA; query
-    // columns from LDS).  Every LDS operand is read one phase before it is used,
-    // so its latency passes under other work: the columns of a half during its
-    // phase A, the rows of the second half during the first half's phase C, and
-    // the rows of the next tile's first half during the second half's phase C,
-    // which runs after the barrier that publishes that tile.
+    // columns from LDS).  At d = 64 (three waves per SIMD, below) each phase reads
+    // its own operands.  At d = 128 (one wave per SIMD) every LDS operand is read
+    // one phase before it is used, so its latency passes under other work: the
+    // columns of a half during its phase A, the rows of the second half during
+    // the first half's phase C, and the rows of the next tile's first half during
+    // the second half's phase C, which runs after the barrier that publishes that
+    // tile.
     struct OpA {
         bf16x8 a[2][NDS], b[2][NDS];
         f32x4 si[2], di[2];
@@ -549,6 +556,123 @@ __global__ __launch_bounds__(kBwdThreads) void dkdv_bf16_kernel(
             }
     };
 
+    if constexpr (kKinLds) {
+    // d = 64: three waves per SIMD.  No operand is held across a phase, phase A is
+    // split into S (query rows and K from LDS) and dP (dO rows, V in registers),
+    // and the keys' K rows come from LDS, so that the kernel fits 168 VGPRs.
+    struct OpS {
+        bf16x8 a[2][NDS];
+        f32x4 si[2];
+    };
+    struct OpD {
+        bf16x8 b[2][NDS];
+        f32x4 di[2];
+    };
+    auto load_s = [&](int buf, int h) __attribute__((always_inline)) {
+        OpS r;
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+            r.si[t] = *reinterpret_cast<const f32x4*>(&sm.la[buf][32 * h + 8 * g + 4 * t]);
+            const int rstep = 128 * (32 * h + 4 * t);
+#pragma unroll
+            for (int ds = 0; ds < NDS; ++ds)
+                r.a[t][ds] = *reinterpret_cast<const bf16x8*>(sm.q[buf] + roff[ds] + rstep);
+        }
+        return r;
+    };
+    auto load_d = [&](int buf, int h) __attribute__((always_inline)) {
+        OpD r;
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+            r.di[t] = *reinterpret_cast<const f32x4*>(&sm.dl[buf][32 * h + 8 * g + 4 * t]);
+            const int rstep = 128 * (32 * h + 4 * t);
+#pragma unroll
+            for (int ds = 0; ds < NDS; ++ds)
+                r.b[t][ds] = *reinterpret_cast<const bf16x8*>(sm.o[buf] + roff[ds] + rstep);
+        }
+        return r;
+    };
+    // the wave's keys: rows 32 (w % 2) + 16 kt + (lane % 16) of K tile w / 2
+    auto phase_s = [&](const OpS& rs, SdP& x) __attribute__((always_inline)) {
+        bf16x8 kr[2][NDS];
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+            for (int ds = 0; ds < NDS; ++ds)
+                kr[kt][ds] = tile_row8(sm.k[w >> 1], 32 * (w & 1) + 16 * kt + r16, 32 * ds + 8 * g);
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+            for (int ds = 0; ds < NDS; ++ds)
+#pragma unroll
+                for (int kt = 0; kt < 2; ++kt)
+                    x.s[t][kt] = mfma16(rs.a[t][ds], kr[kt][ds], ds == 0 ? rs.si[t] : x.s[t][kt]);
+    };
+    auto phase_d = [&](const OpD& rd, SdP& x) __attribute__((always_inline)) {
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+            for (int ds = 0; ds < NDS; ++ds)
+#pragma unroll
+                for (int kt = 0; kt < 2; ++kt)
+                    x.dp[t][kt] = mfma16(rd.b[t][ds], vf[kt][ds], ds == 0 ? rd.di[t] : x.dp[t][kt]);
+    };
+
+    // the workgroup's K tiles (when only 64 keys are left, waves 2-3 hold none)
+    dma.issue(sm.k[0], K + (head + k0) * D, w);
+    if (k0 + 64 < L) dma.issue(sm.k[1], K + (head + k0 + 64) * D, w);
+    // tile m_lo in LDS and published (with K); tile m_lo + 1 on its way
+    put_rows(issue(m_lo, 0), 0);
+    wait_vmcnt0();
+    __syncthreads();
+    float3 rnext = make_float3(0.f, 0.f, 0.f);
+    if (m_lo < m_hi) rnext = issue(m_lo + 1, 1);
+    int buf = 0;
+    auto step = [&](auto mask_tag, int m) __attribute__((always_inline)) {
+        const bool act = m >= nw && m <= w_hi;
+        const int kq0 = 32 * (w & 1) + r16 - 8 * g - (m == nw ? 0 : 4096);
+        if (act) {
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                // (scheduling barriers keep each phase's LDS reads from being
+                // hoisted into the phase before, which would not fit 168 VGPRs)
+                __builtin_amdgcn_sched_barrier(0);
+                SdP x;
+                {
+                    const OpS rs = load_s(buf, h);
+                    phase_s(rs, x);
+                }
+                __builtin_amdgcn_sched_barrier(0);
+                {
+                    const OpD rd = load_d(buf, h);
+                    phase_d(rd, x);
+                }
+                __builtin_amdgcn_sched_barrier(0);
+                const PdS y = phase_b(mask_tag, x, h, kq0);
+                __builtin_amdgcn_sched_barrier(0);
+                const OpC rc = load_c(buf, h);
+                phase_c(rc, y);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        if (m < m_hi) put_rows(rnext, buf ^ 1);
+        // tile m + 1 has landed and every wave's reads of tile m are complete
+        wait_vmcnt0_lgkmcnt0();
+        __syncthreads();
+        const bool more = m + 1 < m_hi;
+        if (more && tid < 64) {
+            const size_t row = head + 64 * (m + 2) + tid;
+            rnext = make_float3(cg[row], lse2[row], dsum[row]);
+        }
+        if (more) dma.issue(sm.q[buf], Q + (head + (size_t)64 * (m + 2)) * D, w);
+        if (more) dma.issue(sm.o[buf], dO + (head + (size_t)64 * (m + 2)) * D, w);
+        buf ^= 1;
+    };
+    const int m_diag = min(m_lo + 1, m_hi);
+    int m = m_lo;
+    for (; m <= m_diag; ++m) step(std::true_type{}, m);
+    for (; m <= m_hi; ++m) step(std::false_type{}, m);
+    } else {
     // tile m_lo in LDS and published; tile m_lo + 1 on its way
     put_rows(issue(m_lo, 0), 0);
     wait_vmcnt0();
@@ -604,6 +728,8 @@ __global__ __launch_bounds__(kBwdThreads) void dkdv_bf16_kernel(
     int m = m_lo;
     for (; m <= m_diag; ++m) step(std::true_type{}, m);
     for (; m <= m_hi; ++m) step(std::false_type{}, m);
+
+    }
 
     if (!wave_on) return;
 #pragma unroll
