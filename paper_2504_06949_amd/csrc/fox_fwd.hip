@@ -138,137 +138,122 @@ __device__ __forceinline__ void fwd_bf16_body(
 #pragma unroll
     for (int dt = 0; dt < NDT; ++dt) voff[dt] = tile_off(8 * g + (r16 >> 2), 16 * dt + 4 * (r16 & 3));
 
-    // Each key tile is taken in three phases: A forms S^T (MFMA; key rows and
-    // key biases from LDS), B the weights P (VALU), C accumulates O^T (MFMA; V^T
-    // columns from LDS).  Each phase reads its LDS operands itself, holding no
-    // operand across a phase: that keeps the kernel within 168 VGPRs at d = 64
-    // (three waves per SIMD, whose interleaving hides the LDS latency) and 256
-    // at d = 128 (two waves).
+    // Each key tile is taken in two halves of 32 keys (ks = 0, 1), each in three
+    // phases: A forms S^T (MFMA; key rows and key biases from LDS), B the weights
+    // P (VALU), C accumulates O^T (MFMA; V^T columns from LDS).  Each phase reads
+    // its LDS operands itself, holding no operand across a phase, and scheduling
+    // barriers keep the compiler from hoisting them: that keeps the kernel within
+    // 128 VGPRs at d = 64 (four waves per SIMD, whose interleaving hides the LDS
+    // latency) and 256 at d = 128 (two waves).
     struct OpA {
-        bf16x8 a[4][NDS];
-        float4 nk[4];   // key biases of the lane's keys 32 ks + 8 g + (0..3 | 4..7)
+        bf16x8 a[2][NDS];   // key subtiles 2 ks, 2 ks + 1
+        float4 nk[2];       // key biases of the lane's keys 32 ks + 8 g + (0..3 | 4..7)
     };
     struct OpC {
-        bf16x8 v[NDT][2];
+        bf16x8 v[NDT];
     };
-    struct STile {
-        f32x4 s[4][2];
+    struct SHalf {
+        f32x4 s[2][2];      // [subtile][qt]
     };
-    struct PTile {
-        bf16x8 p[2][2];
-    };
-    auto load_a = [&](int buf) __attribute__((always_inline)) {
+    auto load_a = [&](int buf, int ks) __attribute__((always_inline)) {
         OpA r;
         const unsigned char* ktile = sm.k[buf];
 #pragma unroll
-        for (int kt = 0; kt < 4; ++kt)
+        for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
             for (int ds = 0; ds < NDS; ++ds)
-                // row krow = 32 (kt / 2) + 4 (kt % 2) + (row of koff)
-                r.a[kt][ds] = *reinterpret_cast<const bf16x8*>(
-                    ktile + koff[ds] + 128 * (32 * (kt >> 1) + 4 * (kt & 1)));
+                // row krow = 32 ks + 4 kk + (row of koff)
+                r.a[kk][ds] = *reinterpret_cast<const bf16x8*>(
+                    ktile + koff[ds] + 128 * (32 * ks + 4 * kk));
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-            r.nk[i] = *reinterpret_cast<const float4*>(&sm.kb[buf][32 * (i >> 1) + 8 * g + 4 * (i & 1)]);
+        for (int i = 0; i < 2; ++i)
+            r.nk[i] = *reinterpret_cast<const float4*>(&sm.kb[buf][32 * ks + 8 * g + 4 * i]);
         return r;
     };
-    auto load_c = [&](int buf) __attribute__((always_inline)) {
+    auto load_c = [&](int buf, int ks) __attribute__((always_inline)) {
         OpC r;
 #pragma unroll
-        for (int dt = 0; dt < NDT; ++dt)
-#pragma unroll
-            for (int ks = 0; ks < 2; ++ks) r.v[dt][ks] = tile_col8_at(sm.v[buf] + voff[dt] + 128 * 32 * ks);
+        for (int dt = 0; dt < NDT; ++dt) r.v[dt] = tile_col8_at(sm.v[buf] + voff[dt] + 128 * 32 * ks);
         return r;
     };
     auto phase_a = [&](const OpA& ra) __attribute__((always_inline)) {
-        STile x;
+        SHalf x;
 #pragma unroll
-        for (int kt = 0; kt < 4; ++kt)
+        for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
             for (int ds = 0; ds < NDS; ++ds) {
-                x.s[kt][0] = mfma16(ra.a[kt][ds], qf[0][ds], ds == 0 ? sinit[0] : x.s[kt][0]);
-                x.s[kt][1] = mfma16(ra.a[kt][ds], qf[1][ds], ds == 0 ? sinit[1] : x.s[kt][1]);
+                x.s[kk][0] = mfma16(ra.a[kk][ds], qf[0][ds], ds == 0 ? sinit[0] : x.s[kk][0]);
+                x.s[kk][1] = mfma16(ra.a[kk][ds], qf[1][ds], ds == 0 ? sinit[1] : x.s[kk][1]);
             }
         return x;
     };
-    // The lane's keys are 32 ks + 8 g + j, j = 0..7 (j < 4 from subtile 2 ks),
-    // its query qloc = 32 (w % 2) + 16 qt + r16 within the tile.  kMask: the tile
-    // may be this wave's diagonal one, where keys after the query are dropped.
-    // The test is 32 ks + j > qk with the lane's qk = qloc - 8 g, raised out of
-    // reach on tiles that are not diagonal, so that the comparisons take
-    // immediate operands.
-    auto phase_b = [&](auto mask_tag, const STile& x, const OpA& ra, int qk0) __attribute__((always_inline)) {
+    // The lane's keys in half ks are 32 ks + 8 g + j, j = 0..7 (j < 4 from
+    // subtile 2 ks), its query qloc = 32 (w % 2) + 16 qt + r16 within the tile.
+    // kMask: the tile may be this wave's diagonal one, where keys after the query
+    // are dropped.  The test is 32 ks + j > qk with the lane's qk = qloc - 8 g,
+    // raised out of reach on tiles that are not diagonal, so that the comparisons
+    // take immediate operands.  Returns P of the half for both query subtiles.
+    struct PHalf {
+        bf16x8 p[2];
+    };
+    auto phase_b = [&](auto mask_tag, const SHalf& x, const OpA& ra, int qk0, int ks) __attribute__((always_inline)) {
         constexpr bool kMask = decltype(mask_tag)::value;
-        float nk[2][8];
-#pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
-            const float4 lo = ra.nk[2 * ks], hi = ra.nk[2 * ks + 1];
-            nk[ks][0] = lo.x; nk[ks][1] = lo.y; nk[ks][2] = lo.z; nk[ks][3] = lo.w;
-            nk[ks][4] = hi.x; nk[ks][5] = hi.y; nk[ks][6] = hi.z; nk[ks][7] = hi.w;
-        }
-        PTile pt;
+        const float nk[8] = {ra.nk[0].x, ra.nk[0].y, ra.nk[0].z, ra.nk[0].w,
+                             ra.nk[1].x, ra.nk[1].y, ra.nk[1].z, ra.nk[1].w};
+        PHalf pt;
 #pragma unroll
         for (int qt = 0; qt < 2; ++qt) {
             int qk = qk0 + 16 * qt;
             if constexpr (kMask) asm volatile("" : "+v"(qk));
             if constexpr (kFixed) {
-                float l = lrun[qt], lb = lbf[qt];
+                float l = lrun[qt];
 #pragma unroll
-                for (int ks = 0; ks < 2; ++ks) {
-#pragma unroll
-                    for (int j = 0; j < 8; ++j) {
-                        float p = fast_exp2(
-                            __builtin_fmaf(x.s[2 * ks + (j >> 2)][qt][j & 3], kscale, nk[ks][j]));
-                        if (kMask && 32 * ks + j > qk) p = 0.f;
-                        l += p;
-                        pt.p[qt][ks][j] = (__bf16)p;
-                    }
-                    lb = sum_bf16x8(pt.p[qt][ks], lb);
+                for (int j = 0; j < 8; ++j) {
+                    float p = fast_exp2(__builtin_fmaf(x.s[j >> 2][qt][j & 3], kscale, nk[j]));
+                    if (kMask && 32 * ks + j > qk) p = 0.f;
+                    l += p;
+                    pt.p[qt][j] = (__bf16)p;
                 }
                 lrun[qt] = l;
-                lbf[qt] = lb;
+                lbf[qt] = sum_bf16x8(pt.p[qt], lbf[qt]);
             } else {
-                float y[2][8];
+                float y[8];
                 float mx = -INFINITY;
 #pragma unroll
-                for (int ks = 0; ks < 2; ++ks)
-#pragma unroll
-                    for (int j = 0; j < 8; ++j) {
-                        float v = __builtin_fmaf(x.s[2 * ks + (j >> 2)][qt][j & 3], kscale, nk[ks][j]);
-                        if (kMask && 32 * ks + j > qk) v = -INFINITY;
-                        y[ks][j] = v;
-                        mx = fmaxf(mx, v);
-                    }
+                for (int j = 0; j < 8; ++j) {
+                    float v = __builtin_fmaf(x.s[j >> 2][qt][j & 3], kscale, nk[j]);
+                    if (kMask && 32 * ks + j > qk) v = -INFINITY;
+                    y[j] = v;
+                    mx = fmaxf(mx, v);
+                }
                 mx = fmaxf(mx, __shfl_xor(mx, 16));
                 mx = fmaxf(mx, __shfl_xor(mx, 32));
                 const float mnew = fmaxf(mrun[qt], mx);
+                // (finite: the first half of every tile holds at least one key that
+                // no row of the wave masks)
                 const float alpha = fast_exp2(mrun[qt] - mnew);
                 mrun[qt] = mnew;
                 float l = lrun[qt] * alpha;
 #pragma unroll
                 for (int dt = 0; dt < NDT; ++dt) acc[qt][dt] *= alpha;
 #pragma unroll
-                for (int ks = 0; ks < 2; ++ks)
-#pragma unroll
-                    for (int j = 0; j < 8; ++j) {
-                        const float p = fast_exp2(y[ks][j] - mnew);
-                        l += p;
-                        pt.p[qt][ks][j] = (__bf16)p;
-                    }
+                for (int j = 0; j < 8; ++j) {
+                    const float p = fast_exp2(y[j] - mnew);
+                    l += p;
+                    pt.p[qt][j] = (__bf16)p;
+                }
                 lrun[qt] = l;
             }
         }
         return pt;
     };
-    // O^T += V^T P^T
-    auto phase_c = [&](const OpC& rc, const PTile& pt) __attribute__((always_inline)) {
+    // O^T += V^T P^T over the half's 32 keys
+    auto phase_c = [&](const OpC& rc, const PHalf& pt) __attribute__((always_inline)) {
 #pragma unroll
-        for (int dt = 0; dt < NDT; ++dt)
-#pragma unroll
-            for (int ks = 0; ks < 2; ++ks) {
-                acc[0][dt] = mfma16(rc.v[dt][ks], pt.p[0][ks], acc[0][dt]);
-                acc[1][dt] = mfma16(rc.v[dt][ks], pt.p[1][ks], acc[1][dt]);
-            }
+        for (int dt = 0; dt < NDT; ++dt) {
+            acc[0][dt] = mfma16(rc.v[dt], pt.p[0], acc[0][dt]);
+            acc[1][dt] = mfma16(rc.v[dt], pt.p[1], acc[1][dt]);
+        }
     };
 
     // tile n_lo in LDS and published; tile n_lo + 1 on its way
@@ -282,11 +267,18 @@ __device__ __forceinline__ void fwd_bf16_body(
         const bool act = n >= w_lo && n <= mw;
         const int qk0 = 32 * (w & 1) + r16 - 8 * g + (n == mw ? 0 : 4096);
         if (act) {
-            const OpA ra = load_a(buf);
-            const STile x = phase_a(ra);
-            const PTile pt = phase_b(mask_tag, x, ra, qk0);
-            const OpC rc = load_c(buf);
-            phase_c(rc, pt);
+#pragma unroll
+            for (int ks = 0; ks < 2; ++ks) {
+                __builtin_amdgcn_sched_barrier(0);
+                const OpA ra = load_a(buf, ks);
+                const SHalf x = phase_a(ra);
+                __builtin_amdgcn_sched_barrier(0);
+                const PHalf pt = phase_b(mask_tag, x, ra, qk0, ks);
+                __builtin_amdgcn_sched_barrier(0);
+                const OpC rc = load_c(buf, ks);
+                phase_c(rc, pt);
+            }
+            __builtin_amdgcn_sched_barrier(0);
         }
         if (n < n_hi) put_kb(cnext, buf ^ 1);
         // tile n + 1 has landed and every wave's reads of tile n are complete
@@ -343,7 +335,7 @@ __device__ __forceinline__ void fwd_bf16_body(
 // One launch for both variants: the head's bound picks the body (uniform over
 // the workgroup), and the two bodies share the workgroup's LDS.
 template <int D>
-__global__ __launch_bounds__(kFwdThreads) __attribute__((amdgpu_waves_per_eu(D == 64 ? 3 : 2)))
+__global__ __launch_bounds__(kFwdThreads) __attribute__((amdgpu_waves_per_eu(D == 64 ? 4 : 2)))
 void fwd_bf16_kernel(
     const __bf16* __restrict__ Q, const __bf16* __restrict__ K, const __bf16* __restrict__ V,
     const float* __restrict__ cg, const int* __restrict__ row_start,
