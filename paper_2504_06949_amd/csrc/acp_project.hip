@@ -76,7 +76,11 @@ __global__ __launch_bounds__(256) void qk_project_kernel(
     double* __restrict__ part, int nchunk) {
     __shared__ PrjSmem sm;
     const int HD = H * D;
-    const int tn = blockIdx.x, tm = blockIdx.y;
+    // All column tiles of a 128-row block of X run on one XCD (a contiguous range
+    // of logical ids per XCD), so that the block is fetched into one L2 only.
+    const int ntn = 2 * H * D / kPrjTile;
+    const int lid = xcd_logical_id(blockIdx.x, gridDim.x);
+    const int tn = lid % ntn, tm = lid / ntn;
     const int tid = threadIdx.x, lane = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = w >> 1, wn = w & 1;            // the wave's 64 x 64 quarter
@@ -189,7 +193,7 @@ __global__ __launch_bounds__(256) void qk_project_kernel(
 
 hipError_t launch_qk_project(const ProjectArgs& a, hipStream_t s) {
     const int HD = a.H * a.d;
-    dim3 grid(2 * HD / kPrjTile, a.B * a.L / kPrjTile);
+    dim3 grid((2 * HD / kPrjTile) * (a.B * a.L / kPrjTile));
     trace_begin(ACP_K_PROJECT, s);
     if (a.d == 64)
         hipLaunchKernelGGL(qk_project_kernel<64>, grid, dim3(256), 0, s, (const __bf16*)a.X,
