@@ -10,9 +10,10 @@
 // Both passes use 4 waves of 32 rows (two 64-row pruning blocks per workgroup),
 // so a pruned or non-causal tile is skipped wave-uniformly, and work through
 // each 64-row tile of the other operand in two halves of 32 to keep register
-// pressure low.  At d = 64 both fit 168 VGPRs, i.e. three waves per SIMD.  Tiles are double-buffered in LDS (swizzled panels filled by DMA
-// loads while the previous tile is computed); operands whose contraction runs
-// over sequence positions come from LDS transpose reads.
+// pressure low; at d = 64 both fit 168 VGPRs, i.e. three waves per SIMD.  Tiles
+// are double-buffered in LDS (swizzled panels filled by DMA loads while the
+// previous tile is computed); operands whose contraction runs over sequence
+// positions come from LDS transpose reads.
 #include <type_traits>
 
 #include "acp_device.h"
