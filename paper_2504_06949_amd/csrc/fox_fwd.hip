@@ -128,7 +128,10 @@ __device__ __forceinline__ void fwd_bf16_body(
         for (int dt = 0; dt < NDT; ++dt) acc[qt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
     float mrun[2] = {-INFINITY, -INFINITY};
     float lrun[2] = {0.f, 0.f};   // sum of the float32 weights (for the log-sum-exp)
-    float lbf[2] = {0.f, 0.f};    // sum of the bfloat16 weights that enter P V
+    // Sum of the bfloat16 weights that enter P V, formed by the matrix cores: one
+    // more 16-row output tile against an all-ones operand, whose rows all come out
+    // as the lane's query's weight sum (fixed stabiliser only).
+    f32x4 lbf[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
 
     // Per-lane LDS offsets.  The swizzle of a fragment row depends only on the
     // lane, so the tile-row steps below are compile-time offsets.
@@ -215,7 +218,6 @@ __device__ __forceinline__ void fwd_bf16_body(
                     pt.p[qt][j] = (__bf16)p;
                 }
                 lrun[qt] = l;
-                lbf[qt] = sum_bf16x8(pt.p[qt], lbf[qt]);
             } else {
                 float y[8];
                 float mx = -INFINITY;
@@ -253,6 +255,13 @@ __device__ __forceinline__ void fwd_bf16_body(
         for (int dt = 0; dt < NDT; ++dt) {
             acc[0][dt] = mfma16(rc.v[dt], pt.p[0], acc[0][dt]);
             acc[1][dt] = mfma16(rc.v[dt], pt.p[1], acc[1][dt]);
+        }
+        if constexpr (kFixed) {
+            bf16x8 ones;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) ones[e] = (__bf16)1.0f;
+            lbf[0] = mfma16(ones, pt.p[0], lbf[0]);
+            lbf[1] = mfma16(ones, pt.p[1], lbf[1]);
         }
     };
 
@@ -306,11 +315,7 @@ __device__ __forceinline__ void fwd_bf16_body(
         // O is normalised by the sum of the weights it was built from: with the
         // fixed stabiliser the largest weight is not 1, and normalising the
         // bfloat16-weighted sum by the float32 sum would leave its rounding in O.
-        float lo = kFixed ? lbf[qt] : lt;
-        if (kFixed) {
-            lo += __shfl_xor(lo, 16);
-            lo += __shfl_xor(lo, 32);
-        }
+        const float lo = kFixed ? lbf[qt][0] : lt;
         const float inv = 1.0f / lo;
         const int query = wq0 + 16 * qt + r16;
 #pragma unroll
