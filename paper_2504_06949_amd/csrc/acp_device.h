@@ -37,17 +37,6 @@ __device__ __forceinline__ double nan_max(double a, double b) {
     return (b > a || b != b) ? b : a;
 }
 
-// acc + sum of the eight bfloat16 values of v (v_dot2c_f32_bf16 against ones)
-__device__ __forceinline__ float sum_bf16x8(bf16x8 v, float acc) {
-    typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-    const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
-    acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(v, v, 0, 1), ones, acc, false);
-    acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(v, v, 2, 3), ones, acc, false);
-    acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(v, v, 4, 5), ones, acc, false);
-    acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(v, v, 6, 7), ones, acc, false);
-    return acc;
-}
-
 // ---- MFMA ------------------------------------------------------------------
 // v_mfma_f32_16x16x32_bf16.  Lane l = 16 g + r (g = l / 16, r = l % 16):
 //   A[i][k]: i = r, k = 8 g + t (t = 0..7, element t of the lane's bf16x8)
