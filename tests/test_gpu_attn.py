@@ -144,18 +144,14 @@ def test_forward_is_deterministic():
         assert torch.equal(a[n], b[n]), n
 
 
-@pytest.mark.parametrize("name", ["360m", "760m", "adv"])
-def test_long_layers_sampled(name):
-    w = workloads.WORKLOADS[name]
-    print(f"case: fwd/bwd sampled {w.describe()}", flush=True)
-    x = workloads.generate(w)
-    got = _run_gpu(x, w.eps)
+def _check_sampled(w, x, got, heads, method="bruteforce"):
+    """Sampled rows (O, lse, dQ) and the last key block (dK, dV, dlog f) of some
+    heads against the oracle's row and column functions."""
     tol = TOL[w.dtype]
     L = w.L
     for n in ("o", "lse", "dq", "dk", "dv", "dlog_f"):
         assert torch.isfinite(got[n].float()).all(), n
     rng = np.random.default_rng(w.seed)
-    heads = [(0, 0), (w.B - 1, w.H - 1), (0, int(rng.integers(w.H)))]
     rows = sorted({0, 63, 64, L // 2, L - 65, L - 64, L - 1, *rng.integers(0, L, 5).tolist()})
     tail = list(range(L - 64, L))
     for b, h in heads:
@@ -163,8 +159,10 @@ def test_long_layers_sampled(name):
         k = x["k"][b, h].float().numpy().astype(np.float64)
         v = x["v"][b, h].float().numpy().astype(np.float64)
         do = x["do"][b, h].float().numpy().astype(np.float64)
-        plan = orc.plan_head(q, k, x["log_f"][b, h].numpy(), w.eps)
+        plan = orc.plan_head(q, k, x["log_f"][b, h].numpy(), w.eps, method=method)
         rs, c = plan["row_start"], plan["c"]
+        pv = acp.plan_views(got["ws"], w.B, w.H, w.L, w.d, x["q"].dtype)
+        np.testing.assert_array_equal(pv["row_start"][b, h].cpu().numpy(), rs)
         o, lse = orc.forward_rows(q, k, v, c, rs, rows)
         dq, rsum = orc.backward_rows(q, k, v, c, rs, do, rows)
         assert np.max(np.abs(f64(got["o"][b, h])[rows] - o)) <= tol
@@ -180,6 +178,29 @@ def test_long_layers_sampled(name):
     sdv = got["dv"].double().sum(dim=2).cpu()
     sdo = x["do"].double().sum(dim=2)
     assert torch.max(torch.abs(sdv - sdo)).item() <= 0.02 * math.sqrt(L)
+
+
+@pytest.mark.parametrize("name", ["360m", "760m", "adv"])
+def test_long_layers_sampled(name):
+    w = workloads.WORKLOADS[name]
+    print(f"case: fwd/bwd sampled {w.describe()}", flush=True)
+    x = workloads.generate(w)
+    got = _run_gpu(x, w.eps)
+    rng = np.random.default_rng(w.seed)
+    heads = [(0, 0), (w.B - 1, w.H - 1), (0, int(rng.integers(w.H)))]
+    _check_sampled(w, x, got, heads)
+
+
+def test_max_length_sampled():
+    """L = 131072, the longest sequence the ABI takes (2048 pruning blocks per
+    head; stage 1 off its register path, 1024 row-norm chunks): a fast- and a
+    slow-decay head, sampled against the oracle (its boundary decided on the
+    blocks' top-right entries, since the entry-by-entry form needs L x L)."""
+    w = workloads.custom("maxlen", 1, 2, 64 * 2048, 64, "bf16", 71, mu=(1.0, 6.0))
+    print(f"case: fwd/bwd sampled {w.describe()}", flush=True)
+    x = workloads.generate(w)
+    got = _run_gpu(x, w.eps)
+    _check_sampled(w, x, got, [(0, 0), (0, 1)], method="topright")
 
 
 def test_online_max_variant_for_large_logit_bound():
