@@ -15,7 +15,7 @@ def pytest_configure(config):
 
 def pytest_collection_modifyitems(config, items):
     # GPU tests are skipped, not failed, where no GPU is visible; selecting them
-    # with -m gpu on a GPU machine runs them.
+    # with -m gpu on a machine with the GPU runs them.
     try:
         import torch
         has_gpu = torch.cuda.is_available()
