@@ -5,10 +5,13 @@ fox_attn_bwd on the 125M-shaped layer (B=8, H=12, L=4096, d=64, bf16), with
 all inputs already in HBM.  Prints one JSON line.
 
     python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--workload 125m]
-                    [--no-cpu-baseline] [--no-decode] [--extra]
+                    [--no-cpu-baseline] [--no-decode] [--no-extra]
 
-The line also carries a decoding measurement (fox_attn_decode after a 4096-token
-prompt on the same layer shape) unless --no-decode is given.
+The line also carries the 360M/760M-shaped and adversarial layers with their
+speedups over nothing pruned (unless --no-extra), a decoding measurement
+(fox_attn_decode after a 4096-token prompt on the 125M layer shape) and the Q/K
+projection (unless --no-decode), and the runtime reduction the paper reports, as
+context.
 """
 from __future__ import annotations
 
@@ -24,6 +27,15 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 METRIC = "FoX attn fwd+bwd ms & effective TFLOP/s at L=4k-16k; % blocks pruned; MFMA util"
+# What the paper reports for its own kernels (Sec. 4 and App. D), quoted as context only:
+# other hardware, trained models and real gates instead of synthetic ones.
+PAPER_CONTEXT = {
+    "attention_runtime_reduction": "about 50-70% (2-3x) for one forward + backward, boundary search "
+                                   "included",
+    "boundary_search_share": "2-6% of the attention-kernel time (L = 4k-16k)",
+    "setting": "Triton kernels on NVIDIA L40S (325 W), bf16, trained FoX (Pro) 125M/360M/760M at "
+               "L = 4k/8k/16k",
+}
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0
 
@@ -57,6 +69,12 @@ def measured_traffic(kernel: str, workload: str):
                 now = hashlib.sha1(open(src_path, "rb").read()).hexdigest()[:12]
                 return int(f[3]) if now == digest else None
     return None
+
+
+def _stage1_ms(pk: dict) -> float:
+    """Stage 1 per step: row norms (when they run), the plan and the workgroup
+    schedule."""
+    return pk["rownorm"] + pk["plan"] + pk.get("schedule", 0.0)
 
 
 def _hbm_gbps(w, pk: dict) -> dict:
@@ -272,8 +290,8 @@ def main():
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="first run one plain device-to-device copy of MIB MiB (a known "
                          "byte count for calibrating HBM traffic counters under a profiler)")
-    ap.add_argument("--extra", action="store_true",
-                    help="also time the 360M/760M-shaped and adversarial layers")
+    ap.add_argument("--no-extra", action="store_true",
+                    help="skip the 360M/760M-shaped and adversarial layers")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
@@ -324,22 +342,24 @@ def main():
         "ms_unpruned": None if args.skip_unpruned else round(res["ms_dense"], 4),
         "speedup_vs_unpruned": None if args.skip_unpruned else round(res["ms_dense"] / res["ms"], 3),
         "per_kernel_ms": {k: round(v, 4) for k, v in pk.items()},
-        "boundary_share": round((pk["rownorm"] + pk["plan"]) / res["ms"], 4),
+        "boundary_share": round(_stage1_ms(pk) / res["ms"], 4),
         "hbm_gbps": _hbm_gbps(w, pk),
         "roofline": {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 2),
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                      "traffic": measured_traffic(dom, args.workload)},
     }
-    if args.extra:
+    if not args.no_extra:
         extra = {}
         for name in ("360m", "760m", "adv"):
             r = run_workload(name, max(3, args.steps // 4), 2)
             f = _flops(r["w"], r["kept"])
             extra[name] = {"ms": round(r["ms"], 3), "ms_unpruned": round(r["ms_dense"], 3),
+                           "speedup_vs_unpruned": round(r["ms_dense"] / r["ms"], 3),
                            "effective_tflops": round(f["effective"] / (r["ms"] * 1e-3) / 1e12, 1),
                            "executed_tflops": round(f["executed"] / (r["ms"] * 1e-3) / 1e12, 1),
                            "pruned_fraction": round(1 - r["kept"] / r["causal"], 4),
+                           "boundary_share": round(_stage1_ms(r["per_kernel_ms"]) / r["ms"], 4),
                            "per_kernel_ms": {k: round(v, 4) for k, v in r["per_kernel_ms"].items()}}
         # the 125m layer again with QK-normed queries and keys: the bound comes from
         # the norm scales and stage 1 makes no pass over Q and K
@@ -350,9 +370,10 @@ def main():
         f = _flops(r["w"], r["kept"])
         rpk = r["per_kernel_ms"]
         extra["125m_qknorm"] = {"ms": round(r["ms"], 3), "ms_unpruned": round(r["ms_dense"], 3),
+                                "speedup_vs_unpruned": round(r["ms_dense"] / r["ms"], 3),
                                 "effective_tflops": round(f["effective"] / (r["ms"] * 1e-3) / 1e12, 1),
                                 "pruned_fraction": round(1 - r["kept"] / r["causal"], 4),
-                                "boundary_share": round((rpk["rownorm"] + rpk["plan"]) / r["ms"], 4),
+                                "boundary_share": round(_stage1_ms(rpk) / r["ms"], 4),
                                 "per_kernel_ms": {k: round(v, 4) for k, v in rpk.items()}}
         out["other_workloads"] = extra
     if not args.no_decode:
@@ -360,6 +381,7 @@ def main():
         prj = run_projection()
         prj["norm_pass_us_saved"] = round(pk["rownorm"] * 1e3, 2)
         out["projection"] = prj
+    out["paper_context"] = PAPER_CONTEXT
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(res)
     print(json.dumps(out), flush=True)

@@ -279,7 +279,9 @@ enum {
     ACP_K_DECODE = 8,   /* one decoding step (append, attention
                            over kept keys, split combine)        */
     ACP_K_PROJECT = 9,  /* Q/K projection with norm epilogue    */
-    ACP_K_COUNT = 10
+    ACP_K_SCHEDULE = 10, /* workgroup schedule of the bf16 attention
+                            kernels (after stage 1)             */
+    ACP_K_COUNT = 11
 };
 typedef struct {
     int64_t launches[ACP_K_COUNT];

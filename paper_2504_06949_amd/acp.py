@@ -46,7 +46,7 @@ class DecodeLayout(ctypes.Structure):
 
 
 K_NAMES = ("rownorm", "plan", "fwd", "dsum", "dq", "dkdv", "dlogf", "decode_init", "decode",
-           "project")
+           "project", "schedule")
 
 
 class KernelTimes(ctypes.Structure):

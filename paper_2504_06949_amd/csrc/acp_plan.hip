@@ -460,9 +460,12 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(
 
 hipError_t launch_schedule(const long long* kept, const int* row_start, const int* col_end,
                            int BH, int M, int nb, int* sched_q, int* sched_k, hipStream_t s) {
+    trace_begin(ACP_K_SCHEDULE, s);
     hipLaunchKernelGGL(schedule_kernel, dim3(8, 2), dim3(kSchedThreads), 0, s, kept, row_start,
                        col_end, BH, M, nb, sched_q, sched_k);
-    return hipGetLastError();
+    const hipError_t e = hipGetLastError();
+    if (e == hipSuccess) trace_end(ACP_K_SCHEDULE, s);
+    return e;
 }
 
 // ---- launchers ---------------------------------------------------------------
