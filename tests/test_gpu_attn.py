@@ -203,17 +203,19 @@ def test_max_length_sampled():
     _check_sampled(w, x, got, [(0, 0), (0, 1)], method="topright")
 
 
-def test_online_max_variant_for_large_logit_bound():
+@pytest.mark.parametrize("d", [64, 128])
+def test_online_max_variant_for_large_logit_bound(d):
     # rho_q ~ 40 makes U ~ 50 > 32 on head 0, so its forward takes the
     # online-maximum variant; head 1 keeps the fixed stabiliser.  Gradients
     # scale with |q|, so the bound is 2e-2 relative to the largest reference value.
-    w = workloads.custom("bigU", 1, 2, 384, 64, "bf16", 29, mu=(1.0, 4.0))
+    w = workloads.custom("bigU", 1, 2, 384, d, "bf16", 29, mu=(1.0, 4.0))
+    print(f"case: online maximum {w.describe()}", flush=True)
     x = workloads.generate(w)
     q = x["q"].float()
     q[0, 0] = q[0, 0] / q[0, 0].norm(dim=-1, keepdim=True) * 40.0
     x["q"] = q.bfloat16()
     got = _run_gpu(x, w.eps)
-    u = acp.plan_views(got["ws"], 1, 2, 384, 64, torch.bfloat16)["bound_u"].cpu().numpy()
+    u = acp.plan_views(got["ws"], 1, 2, 384, d, torch.bfloat16)["bound_u"].cpu().numpy()
     assert u[0, 0] > 32.0 and u[0, 1] < 32.0
     for h in range(2):
         ref = oracle_head(x, 0, h, w.eps)
