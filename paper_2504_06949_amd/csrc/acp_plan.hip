@@ -211,19 +211,40 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
         s_mk[wid] = mk;
     }
     lds_barrier();
-    double before = 0.0, total_abs = 0.0;
-    int flags = 0;
-    min_lsb = 1 << 30;
-    mq = 0.0;
-    mk = 0.0;
-#pragma unroll 4
-    for (int w2 = 0; w2 < kPlanWaves; ++w2) {
-        if (w2 < wid) before += s_sum[w2];
-        total_abs += s_abs[w2];
-        min_lsb = min(min_lsb, s_lsb[w2]);
-        flags |= s_flg[w2];
-        mq = nan_max(mq, s_mq[w2]);
-        mk = nan_max(mk, s_mk[w2]);
+    // Every wave combines the 16 waves' entries itself, lane l < 16 taking wave l's
+    // (one LDS read per quantity, then a reduction over the row of 16 lanes; row 0
+    // is read out).  The float64 sums are exact whenever the span check passes, so
+    // their association does not matter.
+    double before, total_abs;
+    int flags;
+    {
+        const bool in = lane < kPlanWaves;
+        const int l = in ? lane : 0;
+        const auto add = [](double a, double b) { return a + b; };
+        double vs = in && lane < wid ? s_sum[l] : 0.0;
+        double va = in ? s_abs[l] : 0.0;
+        int vl = in ? s_lsb[l] : (1 << 30);
+        int vf = in ? s_flg[l] : 0;
+        double vq = in ? s_mq[l] : 0.0;   // squared norms are >= 0; a NaN wins nan_max
+        double vk = in ? s_mk[l] : 0.0;
+        vs = row16_reduce(vs, add);
+        va = row16_reduce(va, add);
+        vl = row16_reduce(vl, [](int a, int b) { return min(a, b); });
+        vf = row16_reduce(vf, [](int a, int b) { return a | b; });
+        vq = row16_reduce(vq, [](double a, double b) { return nan_max(a, b); });
+        vk = row16_reduce(vk, [](double a, double b) { return nan_max(a, b); });
+        auto first = [](double v) {
+            const unsigned long long b = __double_as_longlong(v);
+            const unsigned lo = (unsigned)__builtin_amdgcn_readfirstlane((int)(unsigned)b);
+            const unsigned hi = (unsigned)__builtin_amdgcn_readfirstlane((int)(unsigned)(b >> 32));
+            return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
+        };
+        before = first(vs);
+        total_abs = first(va);
+        min_lsb = __builtin_amdgcn_readfirstlane(vl);
+        flags = __builtin_amdgcn_readfirstlane(vf);
+        mq = first(vq);
+        mk = first(vk);
     }
     if (total_abs > 0.0) {
         // every partial sum is a multiple of 2^min_lsb and below 2^(ilogb+2)

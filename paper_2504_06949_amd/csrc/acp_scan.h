@@ -50,6 +50,45 @@ __device__ inline V block_reduce(V v, V* s_wave, Op op) {
     return r;
 }
 
+// Reductions over the 16 lanes of each row of a wave (DPP: swap neighbours, swap
+// pairs, mirror halves of 8, mirror the 16); every lane of the row ends with the
+// row's result.
+__device__ __forceinline__ double dpp_f64(double v, int ctrl_id) {
+    const unsigned long long b = __double_as_longlong(v);
+    int lo = (int)(unsigned)b, hi = (int)(unsigned)(b >> 32);
+    switch (ctrl_id) {
+        case 0: lo = __builtin_amdgcn_mov_dpp(lo, 0xB1, 0xF, 0xF, false);
+                hi = __builtin_amdgcn_mov_dpp(hi, 0xB1, 0xF, 0xF, false); break;
+        case 1: lo = __builtin_amdgcn_mov_dpp(lo, 0x4E, 0xF, 0xF, false);
+                hi = __builtin_amdgcn_mov_dpp(hi, 0x4E, 0xF, 0xF, false); break;
+        case 2: lo = __builtin_amdgcn_mov_dpp(lo, 0x141, 0xF, 0xF, false);
+                hi = __builtin_amdgcn_mov_dpp(hi, 0x141, 0xF, 0xF, false); break;
+        default: lo = __builtin_amdgcn_mov_dpp(lo, 0x140, 0xF, 0xF, false);
+                 hi = __builtin_amdgcn_mov_dpp(hi, 0x140, 0xF, 0xF, false); break;
+    }
+    return __longlong_as_double((long long)(((unsigned long long)(unsigned)hi << 32) | (unsigned)lo));
+}
+__device__ __forceinline__ int dpp_i32(int v, int ctrl_id) {
+    switch (ctrl_id) {
+        case 0: return __builtin_amdgcn_mov_dpp(v, 0xB1, 0xF, 0xF, false);
+        case 1: return __builtin_amdgcn_mov_dpp(v, 0x4E, 0xF, 0xF, false);
+        case 2: return __builtin_amdgcn_mov_dpp(v, 0x141, 0xF, 0xF, false);
+        default: return __builtin_amdgcn_mov_dpp(v, 0x140, 0xF, 0xF, false);
+    }
+}
+template <typename Op>
+__device__ __forceinline__ double row16_reduce(double v, Op op) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c) v = op(v, dpp_f64(v, c));
+    return v;
+}
+template <typename Op>
+__device__ __forceinline__ int row16_reduce(int v, Op op) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c) v = op(v, dpp_i32(v, c));
+    return v;
+}
+
 // Position of the last bit of a float32 value: it is an integer multiple of
 // 2^lsb_exp(x).  Subnormals share the exponent of the smallest normal.
 __device__ __forceinline__ int lsb_exp(float x) {
