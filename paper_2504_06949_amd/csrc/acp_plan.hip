@@ -183,24 +183,26 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
     }
 
     // ---- one round through LDS --------------------------------------------------------
-    double incl = local;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-        const double o = __shfl_up(incl, off);
-        if (lane >= off) incl += o;
-    }
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) {
-        local_abs += __shfl_xor(local_abs, off);
-        min_lsb = min(min_lsb, __shfl_xor(min_lsb, off));
+    // (cross-lane steps by DPP within rows of 16, then the four rows' results by
+    // readlane: lane 0 writes the wave's entries)
+    const double incl = wave_inclusive_scan_f64(local);
+    {
+        const auto add = [](double a, double b) { return a + b; };
+        const double ra = row16_reduce(local_abs, add);
+        local_abs = ((readlane_f64(ra, 0) + readlane_f64(ra, 16)) + readlane_f64(ra, 32)) +
+                    readlane_f64(ra, 48);
+        const int rl = row16_reduce(min_lsb, [](int a, int b) { return min(a, b); });
+        min_lsb = min(min(__builtin_amdgcn_readlane(rl, 0), __builtin_amdgcn_readlane(rl, 16)),
+                      min(__builtin_amdgcn_readlane(rl, 32), __builtin_amdgcn_readlane(rl, 48)));
     }
     const int wflags = (__ballot(positive) != 0ull ? 1 : 0) | (__ballot(nonfinite) != 0ull ? 2 : 0);
     if (norms && wid * 64 < nchunk) {   // only waves that loaded partials
-#pragma unroll
-        for (int off = 32; off >= 1; off >>= 1) {
-            mq = nan_max(mq, __shfl_xor(mq, off));
-            mk = nan_max(mk, __shfl_xor(mk, off));
-        }
+        const auto mx = [](double a, double b) { return nan_max(a, b); };
+        const double rq = row16_reduce(mq, mx), rk = row16_reduce(mk, mx);
+        mq = nan_max(nan_max(readlane_f64(rq, 0), readlane_f64(rq, 16)),
+                     nan_max(readlane_f64(rq, 32), readlane_f64(rq, 48)));
+        mk = nan_max(nan_max(readlane_f64(rk, 0), readlane_f64(rk, 16)),
+                     nan_max(readlane_f64(rk, 32), readlane_f64(rk, 48)));
     }
     if (lane == 63) s_sum[wid] = incl;
     if (lane == 0) {

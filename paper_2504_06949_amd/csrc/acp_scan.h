@@ -89,6 +89,37 @@ __device__ __forceinline__ int row16_reduce(int v, Op op) {
     return v;
 }
 
+// DPP move of a double (both halves): lanes whose source lies outside their row,
+// and rows outside ROW_MASK, receive 0.
+template <int CTRL, int ROW_MASK = 0xF>
+__device__ __forceinline__ double dpp_f64_or_zero(double v) {
+    const unsigned long long b = __double_as_longlong(v);
+    const int lo = __builtin_amdgcn_update_dpp(0, (int)(unsigned)b, CTRL, ROW_MASK, 0xF, true);
+    const int hi = __builtin_amdgcn_update_dpp(0, (int)(unsigned)(b >> 32), CTRL, ROW_MASK, 0xF, true);
+    return __longlong_as_double((long long)(((unsigned long long)(unsigned)hi << 32) | (unsigned)lo));
+}
+
+// Inclusive prefix sum over the 64 lanes of a wave: within each row of 16 by
+// zero-filled shifts of 1, 2, 4 and 8, then the last lane of row 0 into row 1 and
+// of row 2 into row 3, then lane 31 into rows 2 and 3 (any association: the
+// callers only add values whose float64 sums are exact).
+__device__ __forceinline__ double wave_inclusive_scan_f64(double v) {
+    v += dpp_f64_or_zero<0x111>(v);         // row_shr:1
+    v += dpp_f64_or_zero<0x112>(v);         // row_shr:2
+    v += dpp_f64_or_zero<0x114>(v);         // row_shr:4
+    v += dpp_f64_or_zero<0x118>(v);         // row_shr:8
+    v += dpp_f64_or_zero<0x142, 0xA>(v);    // row_bcast:15
+    v += dpp_f64_or_zero<0x143, 0xC>(v);    // row_bcast:31
+    return v;
+}
+
+__device__ __forceinline__ double readlane_f64(double v, int l) {
+    const unsigned long long b = __double_as_longlong(v);
+    const unsigned lo = (unsigned)__builtin_amdgcn_readlane((int)(unsigned)b, l);
+    const unsigned hi = (unsigned)__builtin_amdgcn_readlane((int)(unsigned)(b >> 32), l);
+    return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
+}
+
 // Position of the last bit of a float32 value: it is an integer multiple of
 // 2^lsb_exp(x).  Subnormals share the exponent of the smallest normal.
 __device__ __forceinline__ int lsb_exp(float x) {
