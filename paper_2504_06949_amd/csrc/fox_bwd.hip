@@ -21,6 +21,7 @@
 // accumulation from the key-block pass, so every output is written once.
 #include "acp_device.h"
 #include "acp_internal.h"
+#include "acp_scan.h"
 
 namespace acp {
 
@@ -177,10 +178,26 @@ __global__ __launch_bounds__(kScanThreads) void dlogf_kernel(const float* __rest
     const int per = (L + kScanThreads - 1) / kScanThreads;
     const int beg = min(t * per, L), n = min(beg + per, L) - beg;
     const bool held = per <= kScanHeld;
+    const bool vec = held && (per & 3) == 0;   // then n is per or 0: float4 accesses
     double dv[kScanHeld];
+    if (vec) {
 #pragma unroll
-    for (int i = 0; i < kScanHeld; ++i)
-        dv[i] = held && i < n ? (double)rowsum[head + beg + i] - (double)colsum[head + beg + i] : 0.0;
+        for (int i = 0; i < kScanHeld; i += 4) {
+            float4 r = make_float4(0.f, 0.f, 0.f, 0.f), c = r;
+            if (i < n) {
+                r = *reinterpret_cast<const float4*>(rowsum + head + beg + i);
+                c = *reinterpret_cast<const float4*>(colsum + head + beg + i);
+            }
+            dv[i] = (double)r.x - (double)c.x;
+            dv[i + 1] = (double)r.y - (double)c.y;
+            dv[i + 2] = (double)r.z - (double)c.z;
+            dv[i + 3] = (double)r.w - (double)c.w;
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < kScanHeld; ++i)
+            dv[i] = held && i < n ? (double)rowsum[head + beg + i] - (double)colsum[head + beg + i] : 0.0;
+    }
     double local = 0.0;
     if (held) {
 #pragma unroll
@@ -188,20 +205,41 @@ __global__ __launch_bounds__(kScanThreads) void dlogf_kernel(const float* __rest
     } else {
         for (int i = 0; i < n; ++i) local += (double)rowsum[head + beg + i] - (double)colsum[head + beg + i];
     }
-    // inclusive suffix sums over the lanes of the wave, then over the waves after it
+    // inclusive suffix sums over the lanes of the wave: within each row of 16 by
+    // zero-filled shifts toward lower lanes, then the totals of the later rows
+    // (lane 16 r holds row r's)
     double suf = local;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-        const double o = __shfl_down(suf, off);
-        if (lane + off < 64) suf += o;
+    suf += dpp_f64_or_zero<0x101>(suf);   // row_shl:1
+    suf += dpp_f64_or_zero<0x102>(suf);   // row_shl:2
+    suf += dpp_f64_or_zero<0x104>(suf);   // row_shl:4
+    suf += dpp_f64_or_zero<0x108>(suf);   // row_shl:8
+    {
+        const double t1 = readlane_f64(suf, 16), t2 = readlane_f64(suf, 32), t3 = readlane_f64(suf, 48);
+        const int row = lane >> 4;
+        suf += row == 0 ? (t1 + t2) + t3 : row == 1 ? t2 + t3 : row == 2 ? t3 : 0.0;
     }
     if (lane == 0) s_tot[wid] = suf;
     __syncthreads();
-    double after = 0.0;
-#pragma unroll 4
-    for (int w2 = kWaves - 1; w2 > wid; --w2) after += s_tot[w2];
+    // the waves after this one: lane l < 16 takes wave l's total, summed over the row
+    double after;
+    {
+        const double v = lane < kWaves && lane > wid ? s_tot[lane] : 0.0;
+        after = readlane_f64(row16_reduce(v, [](double x, double y) { return x + y; }), 0);
+    }
     double run = after + (suf - local);   // sum over the threads after this one
-    if (held) {
+    if (vec) {
+#pragma unroll
+        for (int i = kScanHeld - 4; i >= 0; i -= 4) {
+            if (i < n) {
+                float4 o;
+                run += dv[i + 3]; o.w = (float)run;
+                run += dv[i + 2]; o.z = (float)run;
+                run += dv[i + 1]; o.y = (float)run;
+                run += dv[i];     o.x = (float)run;
+                *reinterpret_cast<float4*>(dlog_f + head + beg + i) = o;
+            }
+        }
+    } else if (held) {
 #pragma unroll
         for (int i = kScanHeld - 1; i >= 0; --i) {
             if (i < n) {
