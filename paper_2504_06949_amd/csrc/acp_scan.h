@@ -10,46 +10,6 @@ namespace acp {
 constexpr int kPlanThreads = 1024;
 constexpr int kPlanWaves = kPlanThreads / 64;
 
-// Inclusive prefix sum over the workgroup of one double per thread (any
-// association: the callers only add values whose float64 sums are exact).
-__device__ inline double block_inclusive_scan(double v, double* s_wave) {
-    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-        const double o = __shfl_up(v, off);
-        if (lane >= off) v += o;
-    }
-    if (lane == 63) s_wave[wid] = v;
-    __syncthreads();
-    if (wid == 0) {
-        double w = lane < kPlanWaves ? s_wave[lane] : 0.0;
-#pragma unroll
-        for (int off = 1; off < kPlanWaves; off <<= 1) {
-            const double o = __shfl_up(w, off);
-            if (lane >= off) w += o;
-        }
-        if (lane < kPlanWaves) s_wave[lane] = w;   // inclusive wave totals
-    }
-    __syncthreads();
-    const double before = wid > 0 ? s_wave[wid - 1] : 0.0;
-    const double out = v + before;
-    __syncthreads();  // s_wave may be reused by the caller
-    return out;
-}
-
-template <typename V, typename Op>
-__device__ inline V block_reduce(V v, V* s_wave, Op op) {
-    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) v = op(v, __shfl_xor(v, off));
-    if (lane == 0) s_wave[wid] = v;
-    __syncthreads();
-    V r = s_wave[0];
-    for (int w = 1; w < kPlanWaves; ++w) r = op(r, s_wave[w]);
-    __syncthreads();
-    return r;
-}
-
 // Reductions over the 16 lanes of each row of a wave (DPP: swap neighbours, swap
 // pairs, mirror halves of 8, mirror the 16); every lane of the row ends with the
 // row's result.
@@ -113,11 +73,47 @@ __device__ __forceinline__ double wave_inclusive_scan_f64(double v) {
     return v;
 }
 
+__device__ __forceinline__ int readlane_any(int v, int l) { return __builtin_amdgcn_readlane(v, l); }
+__device__ __forceinline__ double readlane_f64(double v, int l);
+__device__ __forceinline__ double readlane_any(double v, int l) { return readlane_f64(v, l); }
 __device__ __forceinline__ double readlane_f64(double v, int l) {
     const unsigned long long b = __double_as_longlong(v);
     const unsigned lo = (unsigned)__builtin_amdgcn_readlane((int)(unsigned)b, l);
     const unsigned hi = (unsigned)__builtin_amdgcn_readlane((int)(unsigned)(b >> 32), l);
     return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
+}
+
+
+// Inclusive prefix sum over the workgroup of one double per thread (any
+// association: the callers only add values whose float64 sums are exact).
+__device__ inline double block_inclusive_scan(double v, double* s_wave) {
+    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+    v = wave_inclusive_scan_f64(v);
+    if (lane == 63) s_wave[wid] = v;
+    __syncthreads();
+    if (wid == 0) {
+        double w = lane < kPlanWaves ? s_wave[lane] : 0.0;
+        w = wave_inclusive_scan_f64(w);
+        if (lane < kPlanWaves) s_wave[lane] = w;   // inclusive wave totals
+    }
+    __syncthreads();
+    const double before = wid > 0 ? s_wave[wid - 1] : 0.0;
+    const double out = v + before;
+    __syncthreads();  // s_wave may be reused by the caller
+    return out;
+}
+
+template <typename V, typename Op>
+__device__ inline V block_reduce(V v, V* s_wave, Op op) {
+    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+    const V rr = row16_reduce(v, op);   // then the four rows' results
+    v = op(op(readlane_any(rr, 0), readlane_any(rr, 16)), op(readlane_any(rr, 32), readlane_any(rr, 48)));
+    if (lane == 0) s_wave[wid] = v;
+    __syncthreads();
+    V r = s_wave[0];
+    for (int w = 1; w < kPlanWaves; ++w) r = op(r, s_wave[w]);
+    __syncthreads();
+    return r;
 }
 
 // Position of the last bit of a float32 value: it is an integer multiple of
