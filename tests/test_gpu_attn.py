@@ -191,16 +191,41 @@ def test_long_layers_sampled(name):
     _check_sampled(w, x, got, heads)
 
 
-def test_max_length_sampled():
+@pytest.mark.parametrize("d", [64, 128])
+def test_max_length_sampled(d):
     """L = 131072, the longest sequence the ABI takes (2048 pruning blocks per
-    head; stage 1 off its register path, 1024 row-norm chunks): a fast- and a
-    slow-decay head, sampled against the oracle (its boundary decided on the
-    blocks' top-right entries, since the entry-by-entry form needs L x L)."""
-    w = workloads.custom("maxlen", 1, 2, 64 * 2048, 64, "bf16", 71, mu=(1.0, 6.0))
+    head; stage 1 off its register path, 1024 row-norm chunks), at both head
+    sizes: a fast- and a slow-decay head, sampled against the oracle (its
+    boundary decided on the blocks' top-right entries, since the entry-by-entry
+    form needs L x L)."""
+    w = workloads.custom(f"maxlen{d}", 1, 2, 64 * 2048, d, "bf16", 71, mu=(1.0, 6.0))
     print(f"case: fwd/bwd sampled {w.describe()}", flush=True)
     x = workloads.generate(w)
     got = _run_gpu(x, w.eps)
     _check_sampled(w, x, got, [(0, 0), (0, 1)], method="topright")
+
+
+def test_max_head_count_sampled():
+    """B * H = 65535, the most heads the ABI takes (grid sizes, per-head tables
+    and the head-order schedule at their limit), L = 128: heads with strong
+    forgetting (block (1, 0) pruned), moderate and weak, sampled against the
+    oracle head by head; every head must keep sum_j dV_j = sum_i dO_i."""
+    w = workloads.custom("maxheads", 3, 21845, 128, 64, "bf16", 73, mu=(-80.0, 0.0, 6.0))
+    print(f"case: fwd/bwd sampled {w.describe()}", flush=True)
+    x = workloads.generate(w)
+    got = _run_gpu(x, w.eps)
+    kept = acp.plan_views(got["ws"], w.B, w.H, w.L, w.d, x["q"].dtype)["kept"].cpu().numpy()
+    want = np.where(np.arange(w.H) % 3 == 0, 2, 3)   # log f near -80 prunes block (1, 0)
+    np.testing.assert_array_equal(kept.reshape(w.B, w.H), np.broadcast_to(want, (w.B, w.H)))
+    tol = TOL[w.dtype]
+    rng = np.random.default_rng(w.seed)
+    heads = [(0, 0), (0, 1), (0, 2), (w.B - 1, w.H - 1)] + \
+        [(int(rng.integers(w.B)), int(rng.integers(w.H))) for _ in range(4)]
+    for b, h in heads:
+        _compare_head(got, oracle_head(x, b, h, w.eps), b, h, tol)
+    sdv = got["dv"].double().sum(dim=2).cpu()
+    sdo = x["do"].double().sum(dim=2)
+    assert torch.max(torch.abs(sdv - sdo)).item() <= 0.02 * math.sqrt(w.L)
 
 
 @pytest.mark.parametrize("d", [64, 128])
