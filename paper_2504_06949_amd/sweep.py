@@ -58,7 +58,7 @@ def _time_step(g, eps, ws, out_f, out_b, steps, warmup) -> float:
 
 
 def eps_sweep(w: workloads.Workload, eps_list=DEFAULT_EPS, time_it: bool = False,
-              steps: int = 10, warmup: int = 3) -> dict:
+              steps: int = 20, warmup: int = 5) -> dict:
     x = workloads.generate(w, with_grad=time_it)
     dev = torch.device("cuda:0")
     g = {k: (v.to(dev) if torch.is_tensor(v) else v) for k, v in x.items()}
