@@ -299,7 +299,7 @@ def main():
                     help="skip the 360M/760M-shaped and adversarial layers")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
+        print(f"bench.py: measures one GPU only (asked for --gpus {args.gpus}); "
               "the attention path shards over (batch, head) but no multi-GPU run is provided",
               file=sys.stderr)
         sys.exit(2)
