@@ -1,0 +1,57 @@
+"""Host-side logic of bench.py (no GPU): the one-GPU refusal, the FLOP
+accounting behind `value` and `roofline.achieved`, and the rule that the
+reported HBM traffic is dropped once the profiled kernel's source changes."""
+import hashlib
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+import bench  # noqa: E402
+from paper_2504_06949_amd import workloads  # noqa: E402
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr and r.stdout == ""
+
+
+@pytest.mark.parametrize("d", [64, 128])
+def test_flop_accounting(d):
+    w = workloads.custom("acct", 2, 3, 256, d, "bf16", 1)
+    kept = 17
+    f = bench._flops(w, kept)
+    tile = 64 * 64 * d
+    # dense causal fwd + bwd: 2 B H L^2 d forward (two products over half the
+    # square) and 5 B H L^2 d backward (five)
+    assert f["effective"] == 7 * 2 * 3 * 256 * 256 * d
+    assert f["executed"] == kept * 14 * tile
+    # the per-kernel algorithmic shares add up to the executed total
+    assert f["fwd"] + f["dq"] + f["dkdv"] == f["executed"]
+    # with every causal block kept, the executed count covers the dense causal
+    # count plus the diagonal blocks' upper halves
+    M = 256 // 64
+    full = bench._flops(w, 2 * 3 * M * (M + 1) // 2)["executed"]
+    assert full == pytest.approx(f["effective"] + 7 * 2 * 3 * M * 64 * 64 * d)
+
+
+def test_traffic_follows_the_kernel_source(tmp_path, monkeypatch):
+    src_dir = tmp_path / "paper_2504_06949_amd" / "csrc"
+    src_dir.mkdir(parents=True)
+    (tmp_path / "profiles").mkdir()
+    src = src_dir / "kern.hip"
+    src.write_bytes(b"// kernel v1\n")
+    digest = hashlib.sha1(src.read_bytes()).hexdigest()[:12]
+    (tmp_path / "profiles" / "k.md").write_text(
+        "# summary\n\n    traffic kern 125m 123456 kern.hip:%s\n" % digest)
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    assert bench.measured_traffic("kern", "125m") == 123456
+    assert bench.measured_traffic("kern", "360m") is None      # no line for this workload
+    assert bench.measured_traffic("other", "125m") is None
+    src.write_bytes(b"// kernel v2\n")                          # the kernel changed since
+    assert bench.measured_traffic("kern", "125m") is None
