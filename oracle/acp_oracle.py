@@ -26,7 +26,7 @@ is silent or garbled are settled as follows (the same readings bind the HIP path
   first kept block; the reading used here is "first kept block of the row"
   (the boundary block the text defines), so the pointer is tested before it is
   advanced.
-* decoding (Sec. 5): the bound U must be known before the tokens are (QK-norm
+* decoding (App. F): the bound U must be known before the tokens are (QK-norm
   scales, App. E), and the threshold is sized for the longest sequence L_max,
   delta = -(2U + log L_max - log eps), so that it stays fixed as t grows (App. A
   needs only that a row holds at most L_max entries).  A cache of fixed size
@@ -49,11 +49,13 @@ BLOCK = 64
 
 __all__ = [
     "BLOCK", "cumsum_log_gates", "cumsum_exact_fraction", "cumsum_span_bits",
+    "cumsum_inexact_flag",
     "row_norm_sq_max", "logit_bound", "logit_bound_qknorm", "log_len_over_eps", "threshold",
     "entry_keep", "block_keep_bruteforce", "block_keep_topright", "boundary_from_block_keep",
     "boundary_alg1", "col_end_from_row_start", "kept_tiles", "causal_tiles",
     "block_mask", "entry_mask", "causal_mask", "forward", "backward", "pruned_mass",
     "plan_head", "run_head", "forward_rows", "backward_rows", "backward_cols",
+    "backward_row_range",
     "decode_pointer", "decode_row", "decode_ring_row", "qk_projection",
 ]
 
@@ -111,9 +113,13 @@ def _fraction_to_f32(fr: Fraction) -> np.float32:
 def cumsum_span_bits(log_f_1d) -> int:
     """Bits spanned by the partial sums of float32 addends (0 if all are zero).
 
-    Every float32 addend is an integer multiple of 2^(e_min - 23) and every partial
-    sum is below 2^E with E = ceil(log2(sum |x|)); when E - (e_min - 23) <= 53,
-    all float64 partial sums are exact, so any summation order gives the same c.
+    Every float32 addend is an integer multiple of 2^lsb, lsb = e_min - 23 the
+    exponent of the smallest ulp among the nonzero addends (subnormals share the
+    smallest normal exponent), and every partial sum lies below 2^E, the least
+    power of two above the exact sum of |x|.  Such a value needs at most E - lsb
+    significant bits, so when E - lsb <= 53 all float64 partial sums are exact and
+    any summation order gives the same c.  The total is summed exactly (fsum
+    rounds once, to nearest, and so is below 2^E exactly when the exact sum is).
     """
     x = np.asarray(log_f_1d, dtype=np.float32).astype(np.float64)
     nz = x[x != 0]
@@ -121,9 +127,18 @@ def cumsum_span_bits(log_f_1d) -> int:
         return 0
     _, e = np.frexp(np.abs(nz))          # |x| = m * 2^e, m in [0.5, 1)
     lsb = int(np.min(np.maximum(e - 1, -126))) - 23
-    total = float(np.sum(np.abs(nz)))
-    E = math.frexp(total)[1]             # total < 2^E
+    total = math.fsum(np.abs(nz).tolist())
+    E = math.frexp(total)[1]             # 2^(E-1) <= total < 2^E
     return E - lsb
+
+
+def cumsum_inexact_flag(log_f_1d) -> bool:
+    """Flag bit 2 of stage 1 (reading of Sec. 2's cumulative sum, whose precision
+    the paper leaves open): raised when the span is 53 bits or more.  A span of
+    53 is still exact; it is flagged because a summation of |x| in float64 that
+    rounds (possible only beyond 53 bits) can place its total one power of two
+    low and so read a span of 54 as 53.  Clear, the flag guarantees exact c."""
+    return cumsum_span_bits(log_f_1d) >= 53
 
 
 def row_norm_sq_max(x) -> float:
@@ -468,8 +483,66 @@ def backward_cols(q, k, v, c, row_start, do, cols, block: int = BLOCK):
     return dk, dv, cs
 
 
+def backward_row_range(q, k, v, c, row_start, do, r0: int, r1: int, ls=(), group: int = 256,
+                       block: int = BLOCK):
+    """The dense definition of `forward` / `backward` evaluated for the query rows
+    r0 <= i < r1 only, a group of rows at a time, so that a long head never needs
+    its L x L matrices at once.  Each row's softmax is taken over its own kept keys
+    (eq. 2 with the block-level mask of Sec. 3; a row depends on no other row), and
+    its gradient terms follow the chain rule of `backward`.
+
+    Returns o, lse, dq, rowsum for rows r0..r1-1, and, summed over those rows only,
+    dk, dv ([L, d]) and colsum ([L]); these are the full column values for every
+    key j all of whose keeping rows lie in the range (rows i >= j of the blocks up
+    to col_end of j's block).  rect[l] for each l in `ls` is the part of the
+    rectangle identity dlog f_l = sum_{i >= l} sum_{j < l} dS_ij that these rows
+    hold (all of it when the range covers every row >= l that keeps a key < l).
+    """
+    q = np.asarray(q, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    v = np.asarray(v, dtype=np.float64)
+    do = np.asarray(do, dtype=np.float64)
+    c64 = np.asarray(c).astype(np.float64)
+    rs = np.asarray(row_start)
+    L, d = q.shape
+    sd = math.sqrt(d)
+    n = r1 - r0
+    out = {"o": np.empty((n, d)), "lse": np.empty(n), "dq": np.empty((n, d)),
+           "rowsum": np.empty(n), "dk": np.zeros((L, d)), "dv": np.zeros((L, d)),
+           "colsum": np.zeros(L), "rect": {int(l): 0.0 for l in ls}}
+    for g0 in range(r0, r1, group):
+        rows = np.arange(g0, min(g0 + group, r1))
+        lo = block * int(rs[rows[0] // block])        # the boundary only moves right
+        hi = int(rows[-1]) + 1
+        j = np.arange(lo, hi)
+        keep = (j[None, :] <= rows[:, None]) & ((j[None, :] // block) >= rs[rows // block][:, None])
+        x = (q[rows] @ k[lo:hi].T) / sd + (c64[rows][:, None] - c64[lo:hi][None, :])
+        x = np.where(keep, x, -np.inf)
+        m = np.max(x, axis=1, keepdims=True)
+        e = np.exp(x - m)
+        z = np.sum(e, axis=1, keepdims=True)
+        p = e / z
+        o = p @ v[lo:hi]
+        dp = do[rows] @ v[lo:hi].T
+        delta_row = np.sum(do[rows] * o, axis=1)
+        ds = p * (dp - delta_row[:, None])
+        sl = slice(g0 - r0, g0 - r0 + len(rows))
+        out["o"][sl] = o
+        out["lse"][sl] = (m + np.log(z))[:, 0]
+        out["dq"][sl] = (ds @ k[lo:hi]) / sd
+        out["rowsum"][sl] = np.sum(ds, axis=1)
+        out["dk"][lo:hi] += (ds.T @ q[rows]) / sd
+        out["dv"][lo:hi] += p.T @ do[rows]
+        out["colsum"][lo:hi] += np.sum(ds, axis=0)
+        for l in out["rect"]:
+            sel = rows >= l
+            if np.any(sel) and l > lo:
+                out["rect"][l] += float(np.sum(ds[sel][:, : l - lo]))
+    return out
+
+
 # --------------------------------------------------------------------------
-# Decoding (Sec. 5, inference: a per-head boundary pointer that only moves
+# Decoding (App. F, inference-time ACP: a per-head boundary pointer that only moves
 # forward, with the cache entries behind it dropped)
 # --------------------------------------------------------------------------
 
@@ -514,7 +587,7 @@ def decode_row(q_t, k, v, c, t: int, delta: float, block: int = BLOCK):
 
 def decode_ring_row(q_t, k, v, c, t: int, delta: float, capacity: int, block: int = BLOCK):
     """Decoding from a cache that holds only the last `capacity` positions,
-    t - capacity + 1 .. t.  Sec. 5 proposes dropping the entries behind the
+    t - capacity + 1 .. t.  App. F proposes dropping the entries behind the
     pointer; a cache of fixed size may also have to drop kept ones.  Reading
     used here: the query then attends to the kept keys still held,
     j in [max(64 n_t, t - capacity + 1), t], `lost` says whether a kept key was

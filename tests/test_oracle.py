@@ -47,6 +47,50 @@ def test_cumsum_span_of_paper_like_gates_is_far_below_53_bits():
         assert orc.cumsum_span_bits(_gates(_rng(2), 32768, mu)) <= 45
 
 
+def _span_gates(span):
+    """63 gates of -6 (|sum| in [256, 512), so E = 9) and, last, one gate with a
+    full 24-bit significand, -(1 + 2^-23) 2^a, whose ulp 2^(a - 23) is the
+    smallest: the span is E - (a - 23) by construction."""
+    a = 9 + 23 - span
+    lf = np.full(64, -6.0, dtype=np.float32)
+    lf[-1] = np.float32(-(1.0 + 2.0 ** -23) * 2.0 ** a)
+    assert float(lf[-1]) == -(1.0 + 2.0 ** -23) * 2.0 ** a   # representable
+    return lf
+
+
+def _float64_prefix_sums_exact(lf) -> bool:
+    """Every float64 running partial sum equals the exact rational one."""
+    from fractions import Fraction
+    acc, exact = 0.0, Fraction(0)
+    for v in np.asarray(lf, dtype=np.float32).astype(np.float64):
+        acc += float(v)
+        exact += Fraction(float(v))
+        if Fraction(acc) != exact:
+            return False
+    return True
+
+
+@pytest.mark.parametrize("span", [52, 53, 54])
+def test_cumsum_span_bits_hand_built(span):
+    # the count itself (an off-by-one in E or in the ulp exponent fails here)
+    lf = _span_gates(span)
+    assert orc.cumsum_span_bits(lf) == span
+    # what the count promises: up to 53 bits every float64 partial sum is exact;
+    # at 54 the last one (bits 2^8 .. 2^-45) is not
+    assert _float64_prefix_sums_exact(lf) == (span <= 53)
+    # flag bit 2 is raised from 53 bits on
+    assert orc.cumsum_inexact_flag(lf) == (span >= 53)
+
+
+def test_cumsum_span_bits_power_of_two_total_and_subnormal():
+    # |sum| = 256 exactly: 2^8 <= 256 < 2^9, so E = 9; ulp of -4 is 2^-21
+    assert orc.cumsum_span_bits(np.full(64, -4.0, dtype=np.float32)) == 9 + 21
+    # a subnormal gate takes the smallest normal's ulp exponent, -149
+    lf = np.array([-1.0, -2.0 ** -140], dtype=np.float32)
+    assert orc.cumsum_span_bits(lf) == 1 + 149   # 1 <= |sum| < 2: E = 1
+    assert orc.cumsum_span_bits(np.zeros(8, dtype=np.float32)) == 0
+
+
 def test_fraction_rounding_is_single_rounding():
     # 1 + 2^-24 + 2^-60 must round up to 1 + 2^-23 (a float64 detour would round
     # 1 + 2^-24 + 2^-60 to 1 + 2^-24 and then tie to even, giving 1).
@@ -383,7 +427,7 @@ def test_backward_no_forgetting_is_sdpa_autograd():
 
 
 # --------------------------------------------------------------------------
-# Decoding with an online boundary pointer (Sec. 5)
+# Decoding with an online boundary pointer (App. F)
 # --------------------------------------------------------------------------
 
 @pytest.mark.parametrize("mu", [1.0, 3.0])
