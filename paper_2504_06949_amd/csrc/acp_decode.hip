@@ -1,4 +1,4 @@
-// Decoding with ACP (paper Sec. 5, inference; the threshold of Sec. 3).
+// Decoding with ACP (paper App. F, inference-time ACP; the threshold of Sec. 3).
 //
 // With a logit bound U fixed for the whole sequence (from QK-norm scales,
 // App. E) the threshold delta is fixed too, and since the cumulative gate c_t
@@ -95,9 +95,11 @@ __global__ __launch_bounds__(kPlanThreads) void decode_init_kernel(
     const double total_abs = block_reduce(local_abs, s_dbl2, sum);
     min_lsb = block_reduce(min_lsb, s_int, imin);
     if (t == 0 && total_abs > 0.0) {
+        // the rule of the plan kernel: flagged from a span of 53 bits on
         const int biased = (int)((__double_as_longlong(total_abs) >> 52) & 0x7ff);
-        const int top = (biased > 0 ? biased : 1) - 1023 + 2;
-        if (top - min_lsb > 53) flags |= 4;
+        const int top = (biased > 0 ? biased : 1) - 1023 + 1;
+        if (top - min_lsb >= 53) flags |= 4;
+        if (!__builtin_isfinite((float)total_abs)) flags |= 2;
     }
     for (int i = beg; i < end; ++i) {
         run += (double)x[i];

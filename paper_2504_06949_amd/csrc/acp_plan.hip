@@ -249,10 +249,16 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
         mk = first(vk);
     }
     if (total_abs > 0.0) {
-        // every partial sum is a multiple of 2^min_lsb and below 2^(ilogb+2)
+        // Every partial sum is a multiple of 2^min_lsb and below 2^E, the least
+        // power of two above sum |log f| (E = ilogb + 1).  Flag from E - lsb = 53
+        // on: up to 53 bits total_abs itself is exact, so E is right; beyond, its
+        // rounding can lose one power of two, and 54 bits would read as 53.
         const int biased = (int)((__double_as_longlong(total_abs) >> 52) & 0x7ff);
-        const int top = (biased > 0 ? biased : 1) - 1023 + 2;
-        if (top - min_lsb > 53) flags |= 4;
+        const int top = (biased > 0 ? biased : 1) - 1023 + 1;
+        if (top - min_lsb >= 53) flags |= 4;
+        // c leaves the float32 range (|c| <= sum |log f|, reached at the end when
+        // no gate is positive)
+        if (!__builtin_isfinite((float)total_abs)) flags |= 2;
     }
 
     // ---- U and delta ---------------------------------------------------------------------

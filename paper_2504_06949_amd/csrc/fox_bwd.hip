@@ -53,7 +53,10 @@ __global__ __launch_bounds__(256) void dsum_kernel(const float* __restrict__ dO,
 
 // ---------------------------------------------------------------------------
 // fp32 path (plain VALU): dQ/rowsum with one thread per query, dK/dV/colsum
-// with one thread per key, tiles staged in LDS.
+// with one thread per key, tiles staged in LDS.  Off the diagonal tile the decay
+// c_i - c_j is split at R, the gate at the boundary of the thread's own block
+// (first query, resp. last key), into two parts of the same sign; on the
+// diagonal tile it is formed per entry (see fox_fwd.hip).
 // ---------------------------------------------------------------------------
 template <int D>
 __global__ __launch_bounds__(64) void dq_f32_kernel(
@@ -64,15 +67,16 @@ __global__ __launch_bounds__(64) void dq_f32_kernel(
     int L, int M, float kscale, float qscale) {
     __shared__ float ks[64 * D];
     __shared__ float vs[64 * D];
-    __shared__ float nc[64];
+    __shared__ float nc[64];   // (R - c_j) log2(e), or c_j on the diagonal tile
     const int bh = blockIdx.x / M, m = blockIdx.x % M, t = threadIdx.x;
     const size_t head = (size_t)bh * L;
     const size_t row = head + 64 * m + t;
     float q[D], go[D], acc[D];
 #pragma unroll
     for (int k = 0; k < D; ++k) { q[k] = Q[row * D + k]; go[k] = dO[row * D + k]; acc[k] = 0.f; }
-    const float cref = cg[head + 64 * m];
-    const float l2 = (cg[row] - cref) * kLog2e - lse2[row], dl = dsum[row];
+    const float rref = cg[head + 64 * m];
+    const float ci = cg[row];
+    const float l2 = (ci - rref) * kLog2e - lse2[row], l2d = -lse2[row], dl = dsum[row];
     float pdp = 0.f, psum = 0.f;
     for (int n = row_start[(size_t)bh * M + m]; n <= m; ++n) {
         __syncthreads();
@@ -80,7 +84,8 @@ __global__ __launch_bounds__(64) void dq_f32_kernel(
             ks[i] = K[(head + 64 * n) * D + i];
             vs[i] = V[(head + 64 * n) * D + i];
         }
-        nc[t] = -((cg[head + 64 * n + t] - cref) * kLog2e);
+        const float cj = cg[head + 64 * n + t];
+        nc[t] = n == m ? cj : (rref - cj) * kLog2e;
         __syncthreads();
         const int jmax = (n == m) ? t : 63;
         for (int j = 0; j <= jmax; ++j) {
@@ -90,7 +95,8 @@ __global__ __launch_bounds__(64) void dq_f32_kernel(
                 s = __builtin_fmaf(q[k], ks[j * D + k], s);
                 dp = __builtin_fmaf(go[k], vs[j * D + k], dp);
             }
-            const float p = fast_exp2(__builtin_fmaf(s, kscale, nc[j]) + l2);
+            const float p = n == m ? fast_exp2(__builtin_fmaf(s, kscale, (ci - nc[j]) * kLog2e) + l2d)
+                                   : fast_exp2(__builtin_fmaf(s, kscale, nc[j]) + l2);
             const float dsv = p * (dp - dl);
             pdp = __builtin_fmaf(p, dp, pdp);
             psum += p;
@@ -113,7 +119,8 @@ __global__ __launch_bounds__(64) void dkdv_f32_kernel(
     float* __restrict__ colsum, int L, int M, float kscale, float qscale) {
     __shared__ float qs[64 * D];
     __shared__ float os[64 * D];
-    __shared__ float ls[64];
+    __shared__ float ls[64];   // (c_i - R) log2(e) - L_i, or -L_i on the diagonal tile
+    __shared__ float lcs[64];  // c_i (diagonal tile)
     __shared__ float dls[64];
     const int bh = blockIdx.x / M, n = blockIdx.x % M, t = threadIdx.x;
     const size_t head = (size_t)bh * L;
@@ -121,8 +128,9 @@ __global__ __launch_bounds__(64) void dkdv_f32_kernel(
     float kk[D], vv[D], gk[D], gv[D];
 #pragma unroll
     for (int k = 0; k < D; ++k) { kk[k] = K[row * D + k]; vv[k] = V[row * D + k]; gk[k] = 0.f; gv[k] = 0.f; }
-    const float cref = cg[head + 64 * n];
-    const float nk = -((cg[row] - cref) * kLog2e);
+    const float rref = cg[head + 64 * n + 63];
+    const float cj = cg[row];
+    const float nk = (rref - cj) * kLog2e;
     float cs = 0.f;
     const int mend = col_end[(size_t)bh * M + n];
     for (int m = n; m <= mend; ++m) {
@@ -131,7 +139,9 @@ __global__ __launch_bounds__(64) void dkdv_f32_kernel(
             qs[i] = Q[(head + 64 * m) * D + i];
             os[i] = dO[(head + 64 * m) * D + i];
         }
-        ls[t] = (cg[head + 64 * m + t] - cref) * kLog2e - lse2[head + 64 * m + t];
+        const float cr = cg[head + 64 * m + t];
+        ls[t] = m == n ? -lse2[head + 64 * m + t] : (cr - rref) * kLog2e - lse2[head + 64 * m + t];
+        lcs[t] = cr;
         dls[t] = dsum[head + 64 * m + t];
         __syncthreads();
         const int i0 = (m == n) ? t : 0;
@@ -142,7 +152,8 @@ __global__ __launch_bounds__(64) void dkdv_f32_kernel(
                 s = __builtin_fmaf(qs[i * D + k], kk[k], s);
                 dp = __builtin_fmaf(os[i * D + k], vv[k], dp);
             }
-            const float p = fast_exp2(__builtin_fmaf(s, kscale, nk) + ls[i]);
+            const float p = m == n ? fast_exp2(__builtin_fmaf(s, kscale, (lcs[i] - cj) * kLog2e) + ls[i])
+                                   : fast_exp2(__builtin_fmaf(s, kscale, nk) + ls[i]);
             const float dsv = p * (dp - dls[i]);
             cs += dsv;
 #pragma unroll

@@ -1,11 +1,15 @@
 // bf16 backward passes of Forgetting Attention over the blocks kept by ACP
 // (v_mfma_f32_16x16x32_bf16, fp32 accumulation).  The formulas are the chain
 // rule through eq. 2 and the cumulative gates (see fox_bwd.hip); P is
-// recomputed from the forward's frame-free log-sum-exp L_i = LSE_i log2(e):
-//   P_ij = 2^(q_i.k_j log2(e)/sqrt(d) + (c_i - c_j) log2(e) - L_i),
-// in a frame r local to each workgroup (the cumulative gate at its first row),
-// so that P_ij = 2^(fma(q.k, log2(e)/sqrt(d), -(c_j - r) log2(e)) + a_i) with
-// a_i = (c_i - r) log2(e) - L_i.
+// recomputed from the forward's log-sum-exp L_i = LSE_i log2(e):
+//   P_ij = 2^(q_i.k_j log2(e)/sqrt(d) + (c_i - c_j) log2(e) - L_i).
+// The decay is split as in the forward (fox_fwd.hip): off the diagonal block,
+// c_i - c_j = (c_i - R) + (R - c_j) with R the cumulative gate at the boundary
+// of the pruning block the wave owns (its first query in the dQ pass, its last
+// key in the dK/dV pass), so that both parts share the sign of c_i - c_j and
+// neither is larger; on the diagonal tiles c_i - c_j is formed per entry.  The
+// part that belongs to the wave's own rows goes into the MFMA accumulator start
+// together with -L_i, the other part is a bias held per column.
 //
 // Both passes use 4 waves of 32 rows (two 64-row pruning blocks per workgroup),
 // so a pruned or non-causal tile is skipped wave-uniformly, and work through
@@ -34,7 +38,8 @@ template <int D>
 struct alignas(1024) DqSmem {
     unsigned char k[2][128 * D];   // 64 x D bf16 tiles (see tile_off)
     unsigned char v[2][128 * D];
-    float kb[2][64];               // key bias -(c_j - r) log2(e)
+    float kb[2][2][64];            // key bias (R - c_j) log2(e), per query block of the workgroup
+    float kc[2][64];               // c_j (diagonal tiles)
 };
 
 template <int D>
@@ -65,10 +70,13 @@ void dq_bf16_kernel(
     const int n_lo = row_start[(size_t)bh * M + m0];
     const int n_hi = min(m0 + 1, M - 1);
     const int w_lo = wave_on ? row_start[(size_t)bh * M + mw] : (1 << 30);
-    const float cref = cg[head + q0];
+    // R of the workgroup's two query blocks and of this wave's
+    const float rb0 = cg[head + q0];
+    const float rb1 = q0 + 64 < L ? cg[head + q0 + 64] : rb0;
+    const float rw = (w >> 1) ? rb1 : rb0;
 
     bf16x8 qf[2][NDS], dof[2][NDS];
-    float aq[2] = {0.f, 0.f}, dl[2] = {0.f, 0.f};
+    float aq[2] = {0.f, 0.f}, dl[2] = {0.f, 0.f}, cq[2] = {0.f, 0.f}, lq[2] = {0.f, 0.f};
     if (wave_on) {
 #pragma unroll
         for (int qt = 0; qt < 2; ++qt) {
@@ -78,7 +86,9 @@ void dq_bf16_kernel(
                 qf[qt][ds] = *reinterpret_cast<const bf16x8*>(Q + row * D + 32 * ds + 8 * g);
                 dof[qt][ds] = *reinterpret_cast<const bf16x8*>(dO + row * D + 32 * ds + 8 * g);
             }
-            aq[qt] = (cg[row] - cref) * kLog2e - lse2[row];
+            cq[qt] = cg[row];
+            lq[qt] = lse2[row];
+            aq[qt] = (cq[qt] - rw) * kLog2e - lq[qt];
             // Delta_i = rowdot(dO, O) over the lane's columns, then across the four
             // lanes that hold row i
             float dd = 0.f;
@@ -107,9 +117,13 @@ void dq_bf16_kernel(
     };
     auto put_kb = [&](float4 c, int buf) __attribute__((always_inline)) {
         if (tid < 16) {
-            const float4 b = make_float4(-((c.x - cref) * kLog2e), -((c.y - cref) * kLog2e),
-                                         -((c.z - cref) * kLog2e), -((c.w - cref) * kLog2e));
-            *reinterpret_cast<float4*>(&sm.kb[buf][4 * tid]) = b;
+            const float4 b0 = make_float4((rb0 - c.x) * kLog2e, (rb0 - c.y) * kLog2e,
+                                          (rb0 - c.z) * kLog2e, (rb0 - c.w) * kLog2e);
+            const float4 b1 = make_float4((rb1 - c.x) * kLog2e, (rb1 - c.y) * kLog2e,
+                                          (rb1 - c.z) * kLog2e, (rb1 - c.w) * kLog2e);
+            *reinterpret_cast<float4*>(&sm.kb[buf][0][4 * tid]) = b0;
+            *reinterpret_cast<float4*>(&sm.kb[buf][1][4 * tid]) = b1;
+            *reinterpret_cast<float4*>(&sm.kc[buf][4 * tid]) = c;
         }
     };
     // per-lane LDS offsets (the swizzle of a fragment row depends only on the lane)
@@ -125,12 +139,15 @@ void dq_bf16_kernel(
 #pragma unroll
         for (int dt = 0; dt < NDT; ++dt) acc[qt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
     // Row terms folded into the MFMA accumulator starts: S starts at a_i / k' so
-    // that fma(S, k', key bias) is the exponent, and dP starts at -Delta_i so that
-    // it comes out as dP - Delta.
+    // that fma(S, k', key bias) is the exponent (a_i = (c_i - R) log2(e) - L_i off
+    // the diagonal, -L_i on it), and dP starts at -Delta_i so that it comes out
+    // as dP - Delta.
     f32x4 sinit[2], dinit[2];
+    float sdiag[2];   // (made into accumulator starts where the diagonal tiles use them)
 #pragma unroll
     for (int qt = 0; qt < 2; ++qt) {
         const float a = aq[qt] / kscale;
+        sdiag[qt] = -lq[qt] / kscale;
         float b = -dl[qt];
         asm volatile("" : "+v"(b));   // the epilogue reads -Delta_i back from dinit
         sinit[qt] = f32x4{a, a, a, a};
@@ -148,7 +165,7 @@ void dq_bf16_kernel(
     // second half's phase C.
     struct OpA {
         bf16x8 a[2][NDS], b[2][NDS];
-        float4 lo, hi;                 // key biases of the lane's 8 keys
+        float4 lo, hi;                 // key biases (diagonal tiles: gates c_j) of the lane's 8 keys
     };
     struct OpC {
         bf16x8 ak[NDT];
@@ -159,7 +176,9 @@ void dq_bf16_kernel(
     struct DsH {   // dS of the half in the B-operand layout of the dQ product
         bf16x8 d[2];
     };
-    auto load_a = [&](int buf, int h) __attribute__((always_inline)) {
+    // diag: the tile goes through the masking variant (gates instead of biases)
+    auto load_a = [&](bool diag, int buf, int h) __attribute__((always_inline)) {
+        const float* nkrow = diag ? sm.kc[buf] : sm.kb[buf][w >> 1];
         OpA r;
         const unsigned char* ktile = sm.k[buf];
         const unsigned char* vtile = sm.v[buf];
@@ -173,8 +192,8 @@ void dq_bf16_kernel(
                 r.b[t][ds] = *reinterpret_cast<const bf16x8*>(vtile + roff[ds] + rstep);
             }
         }
-        r.lo = *reinterpret_cast<const float4*>(&sm.kb[buf][32 * h + 8 * g]);
-        r.hi = *reinterpret_cast<const float4*>(&sm.kb[buf][32 * h + 8 * g + 4]);
+        r.lo = *reinterpret_cast<const float4*>(&nkrow[32 * h + 8 * g]);
+        r.hi = *reinterpret_cast<const float4*>(&nkrow[32 * h + 8 * g + 4]);
         return r;
     };
     auto load_c = [&](int buf, int h) __attribute__((always_inline)) {
@@ -183,7 +202,20 @@ void dq_bf16_kernel(
         for (int dt = 0; dt < NDT; ++dt) r.ak[dt] = tile_col8_at(sm.k[buf] + coff[dt] + 128 * 32 * h);
         return r;
     };
-    auto phase_a = [&](const OpA& ra) __attribute__((always_inline)) {
+    auto phase_a = [&](auto mask_tag, const OpA& ra) __attribute__((always_inline)) {
+        constexpr bool kMask = decltype(mask_tag)::value;
+        f32x4 init[2];
+#pragma unroll
+        for (int qt = 0; qt < 2; ++qt) {
+            if constexpr (kMask) {
+                // formed here, so that no copy of it stays live through the loop
+                float a = sdiag[qt];
+                asm volatile("" : "+v"(a));
+                init[qt] = f32x4{a, a, a, a};
+            } else {
+                init[qt] = sinit[qt];
+            }
+        }
         SdP x;
 #pragma unroll
         for (int t = 0; t < 2; ++t)
@@ -191,7 +223,7 @@ void dq_bf16_kernel(
             for (int ds = 0; ds < NDS; ++ds)
 #pragma unroll
                 for (int qt = 0; qt < 2; ++qt) {
-                    x.s[t][qt] = mfma16(ra.a[t][ds], qf[qt][ds], ds == 0 ? sinit[qt] : x.s[t][qt]);
+                    x.s[t][qt] = mfma16(ra.a[t][ds], qf[qt][ds], ds == 0 ? init[qt] : x.s[t][qt]);
                     x.dp[t][qt] = mfma16(ra.b[t][ds], dof[qt][ds], ds == 0 ? dinit[qt] : x.dp[t][qt]);
                 }
         return x;
@@ -201,6 +233,7 @@ void dq_bf16_kernel(
     // be this wave's diagonal one, where keys after the query are dropped.  The
     // test is 32 h + j > qk with the lane's qk = qloc - 8 g, raised out of reach
     // on tiles that are not diagonal, so that the comparisons take immediates.
+    // Such tiles form the decay c_i - c_j per entry.
     auto phase_b = [&](auto mask_tag, const SdP& x, const OpA& ra, int h, int qk0) __attribute__((always_inline)) {
         constexpr bool kMask = decltype(mask_tag)::value;
         const float nk[8] = {ra.lo.x, ra.lo.y, ra.lo.z, ra.lo.w, ra.hi.x, ra.hi.y, ra.hi.z, ra.hi.w};
@@ -212,7 +245,8 @@ void dq_bf16_kernel(
 #pragma unroll
             for (int j = 0; j < 8; ++j) {
                 const int t = j >> 2, u = j & 3;
-                float p = fast_exp2(__builtin_fmaf(x.s[t][qt][u], kscale, nk[j]));
+                const float bias = kMask ? (cq[qt] - nk[j]) * kLog2e : nk[j];
+                float p = fast_exp2(__builtin_fmaf(x.s[t][qt][u], kscale, bias));
                 if (kMask && 32 * h + j > qk) p = 0.f;
                 const float dsv = p * x.dp[t][qt][u];
                 sds[qt] += dsv;
@@ -251,8 +285,8 @@ void dq_bf16_kernel(
         if (act) {
 #pragma unroll
             for (int h = 0; h < 2; ++h) {
-                const OpA ra = load_a(buf, h);
-                const SdP x = phase_a(ra);
+                const OpA ra = load_a(decltype(mask_tag)::value, buf, h);
+                const SdP x = phase_a(mask_tag, ra);
                 const DsH y = phase_b(mask_tag, x, ra, h, qk0);
                 const OpC rc = load_c(buf, h);
                 phase_c(rc, y);
@@ -275,23 +309,27 @@ void dq_bf16_kernel(
     for (; n < n_mask; ++n) step(std::false_type{}, n);
     for (; n <= n_hi; ++n) step(std::true_type{}, n);
     } else {
+    // The diagonal tiles (m0 for waves 0-1, m0 + 1 = n_hi for waves 2-3) are the
+    // last two and go through the masking variant.
+    const int n_mask = max(n_lo, n_hi - 1);
     // (read whether or not this wave takes the tile: no path keeps an older set
     // of them live through the loop)
-    OpA ra = load_a(0, 0);
+    OpA ra = load_a(n_lo >= n_mask, 0, 0);
     auto step = [&](auto mask_tag, int n) __attribute__((always_inline)) {
+        constexpr bool kMask = decltype(mask_tag)::value;
         const bool act = n >= w_lo && n <= mw;
         const int qk0 = 32 * (w & 1) + r16 - 8 * g + (n == mw ? 0 : 4096);
         OpC rc;
         DsH y;
         if (act) {
             rc = load_c(buf, 0);
-            SdP x = phase_a(ra);
+            SdP x = phase_a(mask_tag, ra);
             y = phase_b(mask_tag, x, ra, 0, qk0);
-            ra = load_a(buf, 1);
+            ra = load_a(kMask, buf, 1);
             phase_c(rc, y);
             __builtin_amdgcn_sched_barrier(0);
             rc = load_c(buf, 1);
-            x = phase_a(ra);
+            x = phase_a(mask_tag, ra);
             y = phase_b(mask_tag, x, ra, 1, qk0);
         }
         if (n < n_hi) put_kb(cnext, buf ^ 1);
@@ -302,16 +340,13 @@ void dq_bf16_kernel(
         // pass)
         const bool more = n + 1 < n_hi;
         if (more && tid < 16) cnext = *reinterpret_cast<const float4*>(cg + head + 64 * (n + 2) + 4 * tid);
-        if (n < n_hi) ra = load_a(buf ^ 1, 0);
+        if (n < n_hi) ra = load_a(n + 1 >= n_mask, buf ^ 1, 0);
         if (act) phase_c_part(rc, y, 0);
         if (more) dma.issue(sm.k[buf], K + (head + (size_t)64 * (n + 2)) * D, w);
         if (act) phase_c_part(rc, y, 1);
         if (more) dma.issue(sm.v[buf], V + (head + (size_t)64 * (n + 2)) * D, w);
         buf ^= 1;
     };
-    // The diagonal tiles (m0 for waves 0-1, m0 + 1 = n_hi for waves 2-3) are the
-    // last two and go through the masking variant.
-    const int n_mask = max(n_lo, n_hi - 1);
     int n = n_lo;
     for (; n < n_mask; ++n) step(std::false_type{}, n);
     for (; n <= n_hi; ++n) step(std::true_type{}, n);
@@ -357,8 +392,11 @@ template <int D>
 struct alignas(1024) DkvSmem {
     unsigned char q[2][128 * D];   // 64 x D bf16 tiles (see tile_off)
     unsigned char o[2][128 * D];   // dO
-    float la[2][64];               // a_i / k',  a_i = (c_i - r) log2(e) - L_i
+    float la[2][2][64];            // a_i / k',  a_i = (c_i - R) log2(e) - L_i, per key block
+    float ll[2][64];               // -L_i / k' (diagonal tiles)
+    float lc[2][64];               // c_i (diagonal tiles)
     float dl[2][64];               // -Delta'_i
+    float kc[128];                 // c_j of the workgroup's keys (diagonal tiles)
     // d = 64: the workgroup's 128 keys (two tiles), read as the B operand of S
     unsigned char k[D == 64 ? 2 : 1][D == 64 ? 128 * D : 16];
 };
@@ -392,11 +430,17 @@ void dkdv_bf16_kernel(
     const int m_hi = col_end[(size_t)bh * M + min(n0 + 1, M - 1)];
     const int w_hi = wave_on ? col_end[(size_t)bh * M + nw] : -1;
     const float kinv = 1.0f / kscale;
-    const float cref = cg[head + k0];
+    // R of the workgroup's two key blocks (the gate at each block's last key; the
+    // second repeats the first when the sequence ends after 64 keys) and of this
+    // wave's block
+    const float rb0 = cg[head + k0 + 63];
+    const float rb1 = k0 + 64 < L ? cg[head + k0 + 127] : rb0;
+    const float rw = (w >> 1) ? rb1 : rb0;
 
     constexpr bool kKinLds = D == 64;
     bf16x8 kf[2][NDS], vf[2][NDS];   // kf unused at d = 64 (K is in LDS)
-    float nk[2] = {0.f, 0.f};
+    float nk[2] = {0.f, 0.f};   // (R - c_j) log2(e) of the lane's keys
+    if (tid < 128) sm.kc[tid] = k0 + tid < L ? cg[head + k0 + tid] : 0.f;
     if (wave_on) {
 #pragma unroll
         for (int kt = 0; kt < 2; ++kt) {
@@ -407,7 +451,7 @@ void dkdv_bf16_kernel(
                     kf[kt][ds] = *reinterpret_cast<const bf16x8*>(K + row * D + 32 * ds + 8 * g);
                 vf[kt][ds] = *reinterpret_cast<const bf16x8*>(V + row * D + 32 * ds + 8 * g);
             }
-            nk[kt] = -((cg[row] - cref) * kLog2e);
+            nk[kt] = (rw - cg[row]) * kLog2e;
         }
     }
 
@@ -427,7 +471,10 @@ void dkdv_bf16_kernel(
     };
     auto put_rows = [&](float3 r, int buf) __attribute__((always_inline)) {
         if (tid < 64) {
-            sm.la[buf][tid] = ((r.x - cref) * kLog2e - r.y) * kinv;
+            sm.la[buf][0][tid] = ((r.x - rb0) * kLog2e - r.y) * kinv;
+            sm.la[buf][1][tid] = ((r.x - rb1) * kLog2e - r.y) * kinv;
+            sm.ll[buf][tid] = -r.y * kinv;
+            sm.lc[buf][tid] = r.x;
             sm.dl[buf][tid] = -r.z;
         }
     };
@@ -470,16 +517,18 @@ void dkdv_bf16_kernel(
     struct PdS {
         bf16x8 pb[2], db[2];
     };
-    auto load_a = [&](int buf, int h) __attribute__((always_inline)) {
+    // diag: the tile goes through the masking variant (S starts at -L_i / k')
+    auto load_a = [&](bool diag, int buf, int h) __attribute__((always_inline)) {
         OpA r;
         const unsigned char* qtile = sm.q[buf];
         const unsigned char* otile = sm.o[buf];
+        const float* sirow = diag ? sm.ll[buf] : sm.la[buf][w >> 1];
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
             // rows 32 h + 4 t + (row of roff); the lane's accumulator rows are the
             // queries 32 h + 8 g + 4 t + u, whose a_i / k' and -Delta'_i start S
             // and dP, so the MFMAs leave the exponent's row term and dP - Delta'
-            r.si[t] = *reinterpret_cast<const f32x4*>(&sm.la[buf][32 * h + 8 * g + 4 * t]);
+            r.si[t] = *reinterpret_cast<const f32x4*>(&sirow[32 * h + 8 * g + 4 * t]);
             r.di[t] = *reinterpret_cast<const f32x4*>(&sm.dl[buf][32 * h + 8 * g + 4 * t]);
             const int rstep = 128 * (32 * h + 4 * t);
 #pragma unroll
@@ -516,9 +565,19 @@ void dkdv_bf16_kernel(
     // kMask: the tile may be this wave's diagonal one, where key kloc is dropped
     // for the queries before it.  The test is kq > 32 h + j with the lane's
     // kq = kloc - 8 g, lowered out of reach on tiles that are not diagonal, so
-    // that the comparisons take immediate operands.
-    auto phase_b = [&](auto mask_tag, const SdP& x, int h, int kq0) __attribute__((always_inline)) {
+    // that the comparisons take immediate operands.  Such tiles form the decay
+    // c_i - c_j per entry (c_i from LDS).
+    auto phase_b = [&](auto mask_tag, const SdP& x, int buf, int h, int kq0) __attribute__((always_inline)) {
         constexpr bool kMask = decltype(mask_tag)::value;
+        float ci[8], ck[2];
+        if constexpr (kMask) {
+            const float4 a = *reinterpret_cast<const float4*>(&sm.lc[buf][32 * h + 8 * g]);
+            const float4 b = *reinterpret_cast<const float4*>(&sm.lc[buf][32 * h + 8 * g + 4]);
+            ci[0] = a.x; ci[1] = a.y; ci[2] = a.z; ci[3] = a.w;
+            ci[4] = b.x; ci[5] = b.y; ci[6] = b.z; ci[7] = b.w;
+            ck[0] = sm.kc[32 * w + r16];
+            ck[1] = sm.kc[32 * w + 16 + r16];
+        }
         PdS y;
 #pragma unroll
         for (int kt = 0; kt < 2; ++kt) {
@@ -527,7 +586,8 @@ void dkdv_bf16_kernel(
 #pragma unroll
             for (int j = 0; j < 8; ++j) {
                 const int t = j >> 2, u = j & 3;
-                float p = fast_exp2(__builtin_fmaf(x.s[t][kt][u], kscale, nk[kt]));
+                const float bias = kMask ? (ci[j] - ck[kt]) * kLog2e : nk[kt];
+                float p = fast_exp2(__builtin_fmaf(x.s[t][kt][u], kscale, bias));
                 if (kMask && kq > 32 * h + j) p = 0.f;
                 const float dsv = p * x.dp[t][kt][u];
                 csum[kt] += dsv;
@@ -569,11 +629,12 @@ void dkdv_bf16_kernel(
         bf16x8 b[2][NDS];
         f32x4 di[2];
     };
-    auto load_s = [&](int buf, int h) __attribute__((always_inline)) {
+    auto load_s = [&](bool diag, int buf, int h) __attribute__((always_inline)) {
         OpS r;
+        const float* sirow = diag ? sm.ll[buf] : sm.la[buf][w >> 1];
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
-            r.si[t] = *reinterpret_cast<const f32x4*>(&sm.la[buf][32 * h + 8 * g + 4 * t]);
+            r.si[t] = *reinterpret_cast<const f32x4*>(&sirow[32 * h + 8 * g + 4 * t]);
             const int rstep = 128 * (32 * h + 4 * t);
 #pragma unroll
             for (int ds = 0; ds < NDS; ++ds)
@@ -640,7 +701,7 @@ void dkdv_bf16_kernel(
                 __builtin_amdgcn_sched_barrier(0);
                 SdP x;
                 {
-                    const OpS rs = load_s(buf, h);
+                    const OpS rs = load_s(decltype(mask_tag)::value, buf, h);
                     phase_s(rs, x);
                 }
                 __builtin_amdgcn_sched_barrier(0);
@@ -649,7 +710,7 @@ void dkdv_bf16_kernel(
                     phase_d(rd, x);
                 }
                 __builtin_amdgcn_sched_barrier(0);
-                const PdS y = phase_b(mask_tag, x, h, kq0);
+                const PdS y = phase_b(mask_tag, x, buf, h, kq0);
                 __builtin_amdgcn_sched_barrier(0);
                 const OpC rc = load_c(buf, h);
                 phase_c(rc, y);
@@ -680,13 +741,15 @@ void dkdv_bf16_kernel(
     __syncthreads();
     float3 rnext = make_float3(0.f, 0.f, 0.f);
     if (m_lo < m_hi) rnext = issue(m_lo + 1, 1);
-    // (the rows are read whether or not this wave takes the tile, so that no
-    // path keeps an older set of them live through the loop)
-    OpA ra = load_a(0, 0);
-    int buf = 0;
     // One query tile.  Waves 0-1 meet their diagonal tile at m_lo, waves 2-3 at
     // m_lo + 1; those two tiles go through the masking variant.
+    const int m_diag = min(m_lo + 1, m_hi);
+    // (the rows are read whether or not this wave takes the tile, so that no
+    // path keeps an older set of them live through the loop)
+    OpA ra = load_a(true, 0, 0);
+    int buf = 0;
     auto step = [&](auto mask_tag, int m) __attribute__((always_inline)) {
+        constexpr bool kMask = decltype(mask_tag)::value;
         const bool act = m >= nw && m <= w_hi;
         const int kq0 = 32 * (w & 1) + r16 - 8 * g - (m == nw ? 0 : 4096);
         OpC rc;
@@ -695,8 +758,8 @@ void dkdv_bf16_kernel(
             // first half
             rc = load_c(buf, 0);
             SdP x = phase_a(ra);
-            y = phase_b(mask_tag, x, 0, kq0);
-            ra = load_a(buf, 1);
+            y = phase_b(mask_tag, x, buf, 0, kq0);
+            ra = load_a(kMask, buf, 1);
             phase_c(rc, y);
             // (not merged with the second half's phase A: both hold four operand
             // sets and would not fit the registers of two waves per SIMD)
@@ -704,7 +767,7 @@ void dkdv_bf16_kernel(
             // second half up to its softmax terms
             rc = load_c(buf, 1);
             x = phase_a(ra);
-            y = phase_b(mask_tag, x, 1, kq0);
+            y = phase_b(mask_tag, x, buf, 1, kq0);
         }
         if (m < m_hi) put_rows(rnext, buf ^ 1);
         // tile m + 1 has landed and every wave's reads of tile m are complete
@@ -718,14 +781,13 @@ void dkdv_bf16_kernel(
             const size_t row = head + 64 * (m + 2) + tid;
             rnext = make_float3(cg[row], lse2[row], dsum[row]);
         }
-        if (m < m_hi) ra = load_a(buf ^ 1, 0);
+        if (m < m_hi) ra = load_a(m + 1 <= m_diag, buf ^ 1, 0);
         if (act) phase_c_part(rc, y, 0);
         if (more) dma.issue(sm.q[buf], Q + (head + (size_t)64 * (m + 2)) * D, w);
         if (act) phase_c_part(rc, y, 1);
         if (more) dma.issue(sm.o[buf], dO + (head + (size_t)64 * (m + 2)) * D, w);
         buf ^= 1;
     };
-    const int m_diag = min(m_lo + 1, m_hi);
     int m = m_lo;
     for (; m <= m_diag; ++m) step(std::true_type{}, m);
     for (; m <= m_hi; ++m) step(std::false_type{}, m);

@@ -3,26 +3,35 @@
 // each query block starts at its boundary block, and the K/V of pruned blocks
 // are never loaded).
 //
-// Logits are kept in log2 units, in a frame local to the workgroup: with r the
-// cumulative gate at the workgroup's first query,
-//   y_ij = (q_i . k_j) * log2(e)/sqrt(d) - (c_j - r) * log2(e).
-// The row term (c_i - r) log2(e) is constant along a row and cancels in the
-// softmax; it returns only in the log-sum-exp L_i = LSE_i log2(e).  Every
-// quantity stays of the size of the decay inside the kept window, however long
-// the sequence (c itself grows without bound).  L_i is frame-free; the backward
-// recomputes P_ij = 2^(q_i.k_j log2(e)/sqrt(d) + (c_i - c_j) log2(e) - L_i) in
-// frames of its own.
+// Logits are kept in log2 units, y_ij = (q_i . k_j) log2(e)/sqrt(d) +
+// (c_i - c_j) log2(e), and the decay term is split so that no float32 value
+// carries more than the decay it contributes:
+//   * keys of an earlier 64-key block than the query's own: with R the
+//     cumulative gate at the first query of the query's pruning block,
+//     c_i - c_j = (c_i - R) + (R - c_j), and c_i <= R <= c_j, so both parts are
+//     <= 0 and no larger in size than c_i - c_j itself.  (c_i - R) is a row term
+//     folded into the MFMA accumulator start; (R - c_j) log2(e) a key bias held
+//     in LDS per tile, one copy per query block of the workgroup.  The rounding
+//     of either part is relative to |c_i - c_j|, and the weight it enters is
+//     e^(c_i - c_j) times the logit factor, so the error it leaves in P is a few
+//     float32 ulps however strong the forgetting.
+//   * the query's own block (the peeled diagonal tiles): c_i - c_j per entry
+//     from the stored float32 gates, exact when they are within a factor of two
+//     of each other (and relative to the difference otherwise).
+// y is therefore the logit itself, with no frame to undo; c itself grows
+// without bound along the sequence and never enters a sum of its own size.
+// The backward recomputes P_ij = 2^(y_ij - L_i) from the log-sum-exp
+// L_i = LSE_i log2(e) in the same way.
 //
 // Softmax stabiliser.  ACP already bounds every logit of the head: |q.k|/sqrt(d)
-// <= U and c_i - c_j <= 0, so each row's true logits are <= U, while the
-// diagonal logit is >= -U.  Subtracting the per-row constant
-//   m_i = U log2(e) + (r - c_i) log2(e)
-// from y therefore keeps every exponent <= 0 and the largest term >= e^(-2U).
-// For U <= kUFixedMax that largest term is a normal float32 and the online
-// running maximum (and its rescaling of the accumulators) is not needed: the
-// constant is folded into the MFMA accumulator initialisation, and each logit
-// costs one FMA and one exp2.  Heads with a larger U take the online-maximum
-// variant; one launch holds both, and each workgroup takes its head's.
+// <= U and c_i - c_j <= 0, so each row's logits are <= U, while the diagonal
+// logit is >= -U.  Subtracting U log2(e) from y therefore keeps every exponent
+// <= 0 and the largest term >= e^(-2U).  For U <= kUFixedMax that largest term
+// is a normal float32 and the online running maximum (and its rescaling of the
+// accumulators) is not needed: the constant is folded into the MFMA accumulator
+// start, and each logit of an off-diagonal tile costs one FMA and one exp2.
+// Heads with a larger U take the online-maximum variant; one launch holds both,
+// and each workgroup takes its head's.
 #include <type_traits>
 
 #include "acp_device.h"
@@ -54,7 +63,9 @@ template <int D>
 struct alignas(1024) FwdSmem {
     unsigned char k[2][128 * D];   // 64 x D bf16 tiles (see tile_off)
     unsigned char v[2][128 * D];
-    float kb[2][64];               // key bias -(c_j - r) log2(e)
+    float kb[2][2][64];            // key bias (R - c_j) log2(e), per query block of the workgroup
+    float kc[2][64];               // c_j (diagonal tiles)
+    float qc[128];                 // c_i of the workgroup's queries (diagonal tiles)
 };
 
 template <int D, bool kFixed>
@@ -78,12 +89,19 @@ __device__ __forceinline__ void fwd_bf16_body(
     const int n_lo = row_start[(size_t)bh * M + m0];
     const int n_hi = min(m0 + 1, M - 1);
     const int w_lo = wave_on ? row_start[(size_t)bh * M + mw] : (1 << 30);
-    const float cref = cg[head + q0];
+    // R of the workgroup's two query blocks (the second repeats the first when
+    // the sequence ends after 64 rows) and of this wave's block
+    const float rb0 = cg[head + q0];
+    const float rb1 = q0 + 64 < L ? cg[head + q0 + 64] : rb0;
+    const float rw = (w >> 1) ? rb1 : rb0;
     const float uf = (float)u_head;
     const float sqrt_d = sqrtf((float)D);
 
     bf16x8 qf[2][NDS];
-    f32x4 sinit[2];   // fixed stabiliser folded into the S accumulator start
+    // MFMA accumulator starts: off-diagonal tiles carry the row term (c_i - R)
+    // and the fixed stabiliser, diagonal tiles the stabiliser alone (uniform)
+    f32x4 sinit[2];
+    const float sdiag = kFixed ? -uf * sqrt_d : 0.f;
     float cq[2] = {0.f, 0.f};
     if (wave_on) {
 #pragma unroll
@@ -95,9 +113,11 @@ __device__ __forceinline__ void fwd_bf16_body(
             cq[qt] = cg[head + wq0 + 16 * qt + r16];
         }
     }
+    if (tid < 128) sm.qc[tid] = q0 + tid < L ? cg[head + q0 + tid] : 0.f;
 #pragma unroll
     for (int qt = 0; qt < 2; ++qt) {
-        const float init = kFixed ? -(uf + (cref - cq[qt])) * sqrt_d : 0.f;
+        const float row = cq[qt] - rw;
+        const float init = kFixed ? (row - uf) * sqrt_d : row * sqrt_d;
         sinit[qt] = f32x4{init, init, init, init};
     }
 
@@ -115,9 +135,13 @@ __device__ __forceinline__ void fwd_bf16_body(
     };
     auto put_kb = [&](float4 c, int buf) __attribute__((always_inline)) {
         if (tid < 16) {
-            const float4 b = make_float4(-((c.x - cref) * kLog2e), -((c.y - cref) * kLog2e),
-                                         -((c.z - cref) * kLog2e), -((c.w - cref) * kLog2e));
-            *reinterpret_cast<float4*>(&sm.kb[buf][4 * tid]) = b;
+            const float4 b0 = make_float4((rb0 - c.x) * kLog2e, (rb0 - c.y) * kLog2e,
+                                          (rb0 - c.z) * kLog2e, (rb0 - c.w) * kLog2e);
+            const float4 b1 = make_float4((rb1 - c.x) * kLog2e, (rb1 - c.y) * kLog2e,
+                                          (rb1 - c.z) * kLog2e, (rb1 - c.w) * kLog2e);
+            *reinterpret_cast<float4*>(&sm.kb[buf][0][4 * tid]) = b0;
+            *reinterpret_cast<float4*>(&sm.kb[buf][1][4 * tid]) = b1;
+            *reinterpret_cast<float4*>(&sm.kc[buf][4 * tid]) = c;
         }
     };
 
@@ -150,7 +174,8 @@ __device__ __forceinline__ void fwd_bf16_body(
     // latency) and 256 at d = 128 (two waves).
     struct OpA {
         bf16x8 a[2][NDS];   // key subtiles 2 ks, 2 ks + 1
-        float4 nk[2];       // key biases of the lane's keys 32 ks + 8 g + (0..3 | 4..7)
+        float4 nk[2];       // key biases (diagonal tiles: gates c_j) of the lane's keys
+                            // 32 ks + 8 g + (0..3 | 4..7)
     };
     struct OpC {
         bf16x8 v[NDT];
@@ -158,7 +183,9 @@ __device__ __forceinline__ void fwd_bf16_body(
     struct SHalf {
         f32x4 s[2][2];      // [subtile][qt]
     };
-    auto load_a = [&](int buf, int ks) __attribute__((always_inline)) {
+    auto load_a = [&](auto mask_tag, int buf, int ks) __attribute__((always_inline)) {
+        constexpr bool kMask = decltype(mask_tag)::value;
+        const float* nkrow = kMask ? sm.kc[buf] : sm.kb[buf][w >> 1];
         OpA r;
         const unsigned char* ktile = sm.k[buf];
 #pragma unroll
@@ -170,7 +197,7 @@ __device__ __forceinline__ void fwd_bf16_body(
                     ktile + koff[ds] + 128 * (32 * ks + 4 * kk));
 #pragma unroll
         for (int i = 0; i < 2; ++i)
-            r.nk[i] = *reinterpret_cast<const float4*>(&sm.kb[buf][32 * ks + 8 * g + 4 * i]);
+            r.nk[i] = *reinterpret_cast<const float4*>(&nkrow[32 * ks + 8 * g + 4 * i]);
         return r;
     };
     auto load_c = [&](int buf, int ks) __attribute__((always_inline)) {
@@ -179,14 +206,16 @@ __device__ __forceinline__ void fwd_bf16_body(
         for (int dt = 0; dt < NDT; ++dt) r.v[dt] = tile_col8_at(sm.v[buf] + voff[dt] + 128 * 32 * ks);
         return r;
     };
-    auto phase_a = [&](const OpA& ra) __attribute__((always_inline)) {
+    auto phase_a = [&](auto mask_tag, const OpA& ra) __attribute__((always_inline)) {
+        constexpr bool kMask = decltype(mask_tag)::value;
+        const f32x4 sd = f32x4{sdiag, sdiag, sdiag, sdiag};
         SHalf x;
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
             for (int ds = 0; ds < NDS; ++ds) {
-                x.s[kk][0] = mfma16(ra.a[kk][ds], qf[0][ds], ds == 0 ? sinit[0] : x.s[kk][0]);
-                x.s[kk][1] = mfma16(ra.a[kk][ds], qf[1][ds], ds == 0 ? sinit[1] : x.s[kk][1]);
+                x.s[kk][0] = mfma16(ra.a[kk][ds], qf[0][ds], ds == 0 ? (kMask ? sd : sinit[0]) : x.s[kk][0]);
+                x.s[kk][1] = mfma16(ra.a[kk][ds], qf[1][ds], ds == 0 ? (kMask ? sd : sinit[1]) : x.s[kk][1]);
             }
         return x;
     };
@@ -195,7 +224,8 @@ __device__ __forceinline__ void fwd_bf16_body(
     // kMask: the tile may be this wave's diagonal one, where keys after the query
     // are dropped.  The test is 32 ks + j > qk with the lane's qk = qloc - 8 g,
     // raised out of reach on tiles that are not diagonal, so that the comparisons
-    // take immediate operands.  Returns P of the half for both query subtiles.
+    // take immediate operands.  Such tiles form the decay c_i - c_j per entry.
+    // Returns P of the half for both query subtiles.
     struct PHalf {
         bf16x8 p[2];
     };
@@ -208,11 +238,18 @@ __device__ __forceinline__ void fwd_bf16_body(
         for (int qt = 0; qt < 2; ++qt) {
             int qk = qk0 + 16 * qt;
             if constexpr (kMask) asm volatile("" : "+v"(qk));
+            float ci = 0.f;
+            if constexpr (kMask) ci = sm.qc[32 * w + 16 * qt + r16];
+            // exponent of entry j: the row term is in x.s off the diagonal
+            auto expo = [&](int j) __attribute__((always_inline)) {
+                const float bias = kMask ? (ci - nk[j]) * kLog2e : nk[j];
+                return __builtin_fmaf(x.s[j >> 2][qt][j & 3], kscale, bias);
+            };
             if constexpr (kFixed) {
                 float l = lrun[qt];
 #pragma unroll
                 for (int j = 0; j < 8; ++j) {
-                    float p = fast_exp2(__builtin_fmaf(x.s[j >> 2][qt][j & 3], kscale, nk[j]));
+                    float p = fast_exp2(expo(j));
                     if (kMask && 32 * ks + j > qk) p = 0.f;
                     l += p;
                     pt.p[qt][j] = (__bf16)p;
@@ -223,7 +260,7 @@ __device__ __forceinline__ void fwd_bf16_body(
                 float mx = -INFINITY;
 #pragma unroll
                 for (int j = 0; j < 8; ++j) {
-                    float v = __builtin_fmaf(x.s[j >> 2][qt][j & 3], kscale, nk[j]);
+                    float v = expo(j);
                     if (kMask && 32 * ks + j > qk) v = -INFINITY;
                     y[j] = v;
                     mx = fmaxf(mx, v);
@@ -279,8 +316,8 @@ __device__ __forceinline__ void fwd_bf16_body(
 #pragma unroll
             for (int ks = 0; ks < 2; ++ks) {
                 __builtin_amdgcn_sched_barrier(0);
-                const OpA ra = load_a(buf, ks);
-                const SHalf x = phase_a(ra);
+                const OpA ra = load_a(mask_tag, buf, ks);
+                const SHalf x = phase_a(mask_tag, ra);
                 __builtin_amdgcn_sched_barrier(0);
                 const PHalf pt = phase_b(mask_tag, x, ra, qk0, ks);
                 __builtin_amdgcn_sched_barrier(0);
@@ -328,9 +365,8 @@ __device__ __forceinline__ void fwd_bf16_body(
         }
         if (g == 0) {
             // L_i = LSE_i log2(e): fixed variant  U log2(e) + log2(l_i);
-            // online variant  max_j y_ij + log2(l_i) + (c_i - r) log2(e)
-            const float l2 = kFixed ? uf * kLog2e + fast_log2(lt)
-                                    : mrun[qt] + fast_log2(lt) + (cq[qt] - cref) * kLog2e;
+            // online variant  max_j y_ij + log2(l_i)
+            const float l2 = kFixed ? uf * kLog2e + fast_log2(lt) : mrun[qt] + fast_log2(lt);
             lse2[head + query] = l2;
             lse[head + query] = l2 * kLn2;
         }
@@ -361,7 +397,9 @@ void fwd_bf16_kernel(
 
 // ---------------------------------------------------------------------------
 // fp32 path: plain VALU arithmetic, one thread per query, 64 queries (one
-// pruning row) per workgroup; K/V tiles staged in LDS; online maximum.
+// pruning row) per workgroup; K/V tiles staged in LDS; online maximum.  The
+// decay is split at R = c of the block's first query off the diagonal and
+// formed per entry on it, as in the bf16 path.
 // ---------------------------------------------------------------------------
 template <int D>
 __global__ __launch_bounds__(64) void fwd_f32_kernel(
@@ -371,11 +409,13 @@ __global__ __launch_bounds__(64) void fwd_f32_kernel(
     float* __restrict__ lse2, int L, int M, float kscale) {
     __shared__ float ks[64 * D];
     __shared__ float vs[64 * D];
-    __shared__ float nc[64];
+    __shared__ float nc[64];   // (R - c_j) log2(e), or c_j on the diagonal tile
     const int bh = blockIdx.x / M, m = blockIdx.x % M, t = threadIdx.x;
     const size_t head = (size_t)bh * L;
     const int query = 64 * m + t;
-    const float cref = cg[head + 64 * m];
+    const float rref = cg[head + 64 * m];
+    const float ci = cg[head + query];
+    const float row = (ci - rref) * kLog2e;
     float q[D], acc[D];
 #pragma unroll
     for (int k = 0; k < D; ++k) { q[k] = Q[(head + query) * D + k]; acc[k] = 0.f; }
@@ -387,14 +427,16 @@ __global__ __launch_bounds__(64) void fwd_f32_kernel(
             ks[i] = K[(head + 64 * n) * D + i];
             vs[i] = V[(head + 64 * n) * D + i];
         }
-        nc[t] = -((cg[head + 64 * n + t] - cref) * kLog2e);
+        const float cj = cg[head + 64 * n + t];
+        nc[t] = n == m ? cj : (rref - cj) * kLog2e;
         __syncthreads();
         const int jmax = (n == m) ? t : 63;
         for (int j = 0; j <= jmax; ++j) {
             float s = 0.f;
 #pragma unroll
             for (int k = 0; k < D; ++k) s = __builtin_fmaf(q[k], ks[j * D + k], s);
-            const float y = __builtin_fmaf(s, kscale, nc[j]);
+            const float y = n == m ? __builtin_fmaf(s, kscale, (ci - nc[j]) * kLog2e)
+                                   : __builtin_fmaf(s, kscale, nc[j]) + row;
             if (y > mrun) {
                 const float alpha = fast_exp2(mrun - y);
                 lrun *= alpha;
@@ -414,7 +456,7 @@ __global__ __launch_bounds__(64) void fwd_f32_kernel(
         const float o = acc[k] * inv;
         O[(head + query) * D + k] = o;
     }
-    const float l2 = mrun + fast_log2(lrun) + (cg[head + query] - cref) * kLog2e;
+    const float l2 = mrun + fast_log2(lrun);
     lse2[head + query] = l2;
     lse[head + query] = l2 * kLn2;
 }

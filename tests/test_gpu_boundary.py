@@ -122,6 +122,31 @@ def test_boundary_flags_bad_gates():
     assert orc.cumsum_span_bits(lf[0, 0].numpy()) <= 52
 
 
+def test_inexact_cumsum_flag_at_53_bits_and_c_overflow():
+    """Flag bit 2 against the oracle's rule on hand-built gates whose partial sums
+    span 52, 53 and 54 bits (63 gates of -6 and one full-significand gate of ulp
+    2^(E - span)); c bit-identical where the span keeps it exact.  A fourth head
+    whose cumulative sum leaves the float32 range (finite gates of -3e38) carries
+    flag bit 1."""
+    w = workloads.custom("span", 1, 4, 64, 64, "f32", 8, mu=(2.0,))
+    x = workloads.generate(w, with_grad=False)
+    lf = torch.full((1, 4, 64), -6.0, dtype=torch.float32)
+    for h, span in enumerate((52, 53, 54)):
+        lf[0, h, -1] = -(1.0 + 2.0 ** -23) * 2.0 ** (9 + 23 - span)
+        assert orc.cumsum_span_bits(lf[0, h].numpy()) == span
+    lf[0, 3, :2] = -3.0e38
+    x["log_f"] = lf
+    print("case: span flags 52/53/54, c overflow", flush=True)
+    got = _gpu_plan(x, EPS)
+    for h in range(3):
+        want = acp.FLAG_INEXACT_CUMSUM if orc.cumsum_inexact_flag(lf[0, h].numpy()) else 0
+        assert got["flags"][0, h] == want, (h, got["flags"][0, h])
+        if not want:
+            np.testing.assert_array_equal(got["c"][0, h], orc.cumsum_log_gates(lf[0, h].numpy()))
+    assert got["flags"][0, 3] & acp.FLAG_NONFINITE_GATE
+    assert not np.all(np.isfinite(orc.cumsum_log_gates(lf[0, 3].numpy())))
+
+
 def test_boundary_is_deterministic():
     w = workloads.WORKLOADS["125m"]
     x = workloads.generate(w, with_grad=False)

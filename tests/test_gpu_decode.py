@@ -1,4 +1,4 @@
-"""Decoding with ACP on the GPU (Sec. 5, inference) against the oracle: after a
+"""Decoding with ACP on the GPU (App. F, inference-time ACP) against the oracle: after a
 prompt, each step's output, log-sum-exp and boundary pointer must match the
 oracle's single-row decoding, with the threshold sized for L_max and the bound
 from QK-norm scales; a ring cache too small for the kept window must report it
