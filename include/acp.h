@@ -158,6 +158,23 @@ acp_status fox_attn_fwd_qknorm(const void* Q, const void* K, const void* V, cons
                                int B, int H, int L, int d, double eps, void* O, float* lse,
                                void* ws, size_t ws_bytes, void* stream);
 
+/* fox_attn_fwd for callers that cannot allocate device memory (code under HIP
+ * graph capture, serving loops, harnesses that forbid hipMalloc): it takes no
+ * workspace and allocates nothing.  Its workspace is a fixed array of
+ * acp_noalloc_scratch_bytes() bytes (32 MiB) that the library holds on every GPU
+ * it runs on until the process ends; shapes whose acp_workspace_size() exceeds it
+ * (B*H*L beyond about 1.5 million positions) are rejected with ACP_EWORKSPACE
+ * before anything is launched.  Same inputs and outputs as fox_attn_fwd, and the
+ * same results bit for bit.  Every call on one GPU shares that GPU's array and
+ * leaves its plan there until the next call overwrites it, so calls that overlap
+ * on one GPU (other host threads, or other streams without ordering between them)
+ * race; the plan is not kept for fox_attn_bwd, which needs a workspace of its own
+ * (use fox_attn_fwd for training). */
+size_t acp_noalloc_scratch_bytes(void);
+acp_status fox_attn_fwd_noalloc(const void* Q, const void* K, const void* V,
+                                const float* log_f, acp_dtype dt, int B, int H, int L,
+                                int d, double eps, void* O, float* lse, void* stream);
+
 /* Backward of fox_attn_fwd (the paper states only that it mirrors the forward,
  * Sec. 2; the gradients follow from eq. 2 by the chain rule, with the pruning
  * mask held constant).  With x_ij = q_i.k_j/sqrt(d) + c_i - c_j, P = softmax(x),

@@ -68,6 +68,8 @@ _SIGS = {
     "fox_attn_fwd_qknorm": [_p, _p, _p, _p, _p, _p, _i, _i, _i, _i, _i, _d, _p, _p, _p, _sz,
                             _p],
     "fox_attn_bwd": [_p, _p, _p, _p, _p, _i, _i, _i, _i, _i, _p, _p, _p, _p, _p, _sz, _p],
+    "fox_attn_fwd_noalloc": [_p, _p, _p, _p, _i, _i, _i, _i, _i, _d, _p, _p, _p],
+    "acp_noalloc_scratch_bytes": [],
     "acp_qk_project": [_p, _p, _p, _i, _i, _i, _i, _i, _i, _p, _p, _p, _sz, _p],
     "fox_attn_fwd_projected": [_p, _p, _p, _p, _i, _i, _i, _i, _i, _d, _p, _p, _p, _sz, _p],
     "acp_decode_state_size": [_i, _i, _i, _i, _i, ctypes.POINTER(_sz)],
@@ -93,7 +95,8 @@ def lib() -> ctypes.CDLL:
         for name, args in _SIGS.items():
             fn = getattr(L, name)
             fn.argtypes = args
-            fn.restype = ctypes.c_char_p if name in ("acp_status_string", "acp_last_error") else _i
+            fn.restype = (ctypes.c_char_p if name in ("acp_status_string", "acp_last_error")
+                          else _sz if name == "acp_noalloc_scratch_bytes" else _i)
         _lib = L
     return _lib
 
@@ -147,6 +150,14 @@ def acp_boundary_qknorm(log_f, gamma_q, gamma_k, dt, B, H, L, d, eps, c, bound_u
 
 def fox_attn_fwd(Q, K, V, log_f, dt, B, H, L, d, eps, O, lse, ws, ws_bytes, stream) -> int:
     return lib().fox_attn_fwd(Q, K, V, log_f, dt, B, H, L, d, eps, O, lse, ws, ws_bytes, stream)
+
+
+def fox_attn_fwd_noalloc(Q, K, V, log_f, dt, B, H, L, d, eps, O, lse, stream) -> int:
+    return lib().fox_attn_fwd_noalloc(Q, K, V, log_f, dt, B, H, L, d, eps, O, lse, stream)
+
+
+def acp_noalloc_scratch_bytes() -> int:
+    return lib().acp_noalloc_scratch_bytes()
 
 
 def fox_attn_fwd_qknorm(Q, K, V, log_f, gamma_q, gamma_k, dt, B, H, L, d, eps, O, lse, ws,

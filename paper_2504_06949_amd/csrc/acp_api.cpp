@@ -161,6 +161,16 @@ hipEvent_t trace_event() {
 }  // namespace
 
 namespace acp {
+acp_status set_error(acp_status s, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof(buf), fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return s;
+}
+
 void trace_begin(int kernel, hipStream_t s) {
     if (!g_trace.on) return;
     hipEvent_t e = trace_event();

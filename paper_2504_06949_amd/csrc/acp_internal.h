@@ -118,6 +118,9 @@ struct DecodeArgs {
     float* lse;               // [B*H]
 };
 
+// Records the message that acp_last_error() returns and passes the status on.
+acp_status set_error(acp_status s, const char* fmt, ...);
+
 // Tracing hooks: no-ops unless acp_timing_enable(1) was called.
 void trace_begin(int kernel, hipStream_t s);
 void trace_end(int kernel, hipStream_t s);

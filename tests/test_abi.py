@@ -22,7 +22,8 @@ def test_every_declared_symbol_is_exported():
                           "acp_decode_state_size", "acp_decode_offsets",
                           "acp_decode_init", "fox_attn_decode",
                           "acp_timing_enable", "acp_timing_reset",
-                          "acp_timing_read", "acp_status_string", "acp_last_error"}
+                          "acp_timing_read", "acp_status_string", "acp_last_error",
+                          "acp_noalloc_scratch_bytes", "fox_attn_fwd_noalloc"}
     lib = ctypes.CDLL(acp.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
@@ -207,3 +208,17 @@ def test_projection_rejects_before_launch():
     st = acp.fox_attn_fwd_projected(16, 16, 16, 16, acp.ACP_BF16, 1, 1, 64, 64, 0.5, 16, 16, 16,
                                     8, None)
     assert st == acp.ACP_EWORKSPACE
+
+
+def test_noalloc_forward_rejects_shapes_beyond_its_fixed_scratch():
+    """fox_attn_fwd_noalloc checks the shapes against its fixed scratch array
+    (32 MiB) before it touches the GPU or any pointer."""
+    size = acp.acp_noalloc_scratch_bytes()
+    assert size == 32 << 20
+    B, H, L, d = 1, 64, 32768, 64
+    assert acp.acp_workspace_size(B, H, L, d, acp.ACP_BF16) > size
+    st = acp.fox_attn_fwd_noalloc(16, 16, 16, 16, acp.ACP_BF16, B, H, L, d, 1e-4, 16, 16, None)
+    assert st == acp.ACP_EWORKSPACE
+    assert "fox_attn_fwd_noalloc" in acp.acp_last_error()
+    st = acp.fox_attn_fwd_noalloc(16, 16, 16, 16, acp.ACP_BF16, 1, 1, 100, 64, 1e-4, 16, 16, None)
+    assert st == acp.ACP_EUNSUPPORTED
