@@ -60,9 +60,9 @@ def test_traffic_follows_the_kernel_source(tmp_path, monkeypatch):
 def test_roofline_takes_the_longest_attention_kernel():
     w = workloads.custom("acct", 2, 3, 256, 64, "bf16", 1)
     kept = 17
-    r = {"kept": kept, "per_kernel_ms": {"fwd": 0.01, "dq": 0.02, "dkdv": 0.03, "rownorm": 0.5}}
+    r = {"kept": kept, "per_kernel_ms": {"fwd": 1e-5, "dq": 2e-5, "dkdv": 3e-5, "rownorm": 0.5}}
     got = bench.roofline(w, r)
     assert got["kernel"] == "dkdv"          # stage-1 kernels are not candidates
-    want = kept * 8 * 64 * 64 * 64 / 0.03e-3 / 1e12
+    want = kept * 8 * 64 * 64 * 64 / 3e-8 / 1e12
     assert got["achieved"] == pytest.approx(want, rel=1e-3)
     assert got["frac"] == pytest.approx(want / bench.PEAK_BF16_TFLOPS, rel=1e-3)
