@@ -49,7 +49,7 @@ BLOCK = 64
 
 __all__ = [
     "BLOCK", "cumsum_log_gates", "cumsum_exact_fraction", "cumsum_span_bits",
-    "cumsum_inexact_flag",
+    "cumsum_inexact_flag", "gate_logits", "log_sigmoid", "gate_log_forget",
     "row_norm_sq_max", "logit_bound", "logit_bound_qknorm", "log_len_over_eps", "threshold",
     "entry_keep", "block_keep_bruteforce", "block_keep_topright", "boundary_from_block_keep",
     "boundary_alg1", "col_end_from_row_start", "kept_tiles", "causal_tiles",
@@ -76,6 +76,39 @@ def cumsum_log_gates(log_f) -> np.ndarray:
         acc = acc + x[..., i]
         out[..., i] = acc
     return out.astype(np.float32)
+
+
+def gate_logits(x, w_f, b_f) -> np.ndarray:
+    """Forget-gate logits a_t = w_f^T x_t + b_f of every head (Sec. 2: each head's
+    gate is f_t = sigmoid(w_f^T x_t + b_f) of the layer input x_t).
+
+    x [T, d_model] and w_f [d_model, H] are bfloat16 values, b_f [H] float32.
+    Reading (the paper does not fix the precision): the dot product is summed in
+    float32 in ascending feature order, each step one rounding (a product of two
+    bfloat16 values is exact in float32), and b_f is added last, in float32.
+    Returns [T, H] float32.
+    """
+    x32 = np.asarray(x, dtype=np.float32)
+    w32 = np.asarray(w_f, dtype=np.float32)
+    acc = np.zeros((x32.shape[0], w32.shape[1]), dtype=np.float32)
+    for k in range(x32.shape[1]):
+        acc = acc + x32[:, k:k + 1] * w32[k:k + 1, :]
+    return acc + np.asarray(b_f, dtype=np.float32)[None, :]
+
+
+def log_sigmoid(a) -> np.ndarray:
+    """log f = log sigmoid(a) = -softplus(-a) (Sec. 2 gate), in float64 as
+    -(max(-a, 0) + log1p(exp(-|a|))), rounded once to float32."""
+    a64 = np.asarray(a, dtype=np.float32).astype(np.float64)
+    return (-(np.maximum(-a64, 0.0) + np.log1p(np.exp(-np.abs(a64))))).astype(np.float32)
+
+
+def gate_log_forget(x, w_f, b_f, B: int) -> np.ndarray:
+    """log f [B, H, L] of a layer input x [B*L, d_model] (token l of sequence b is
+    row b*L + l): log_sigmoid(gate_logits(x, w_f, b_f))."""
+    lf = log_sigmoid(gate_logits(x, w_f, b_f))
+    T, H = lf.shape
+    return np.ascontiguousarray(lf.reshape(B, T // B, H).transpose(0, 2, 1))
 
 
 def cumsum_exact_fraction(log_f_1d) -> np.ndarray:

@@ -154,3 +154,19 @@ def projection_inputs(B: int, L: int, d_model: int, H: int, d: int, seed: int) -
     wk = torch.randn((d_model, H * d), generator=g, dtype=torch.float32) * 0.02
     return {"x": x.bfloat16().contiguous(), "wq": wq.bfloat16().contiguous(),
             "wk": wk.bfloat16().contiguous()}
+
+
+def gate_inputs(B: int, L: int, d_model: int, H: int, seed: int, mu=None) -> dict:
+    """Seeded inputs of the forget-gate projection (Sec. 2, f = sigmoid(w_f^T x + b_f)
+    per head): layer inputs X [B*L, d_model] ~ N(0, 1) and weights w_f [d_model, H]
+    ~ N(0, 0.02^2), both rounded to bfloat16, and float32 biases b_f [H] ~ U[1, 10]
+    (or the given per-head values), so that the gate logits spread like the
+    workloads' a ~ N(mu_h, 0.5).  CPU tensors."""
+    g = torch.Generator(device="cpu")
+    g.manual_seed(seed)
+    x = torch.randn((B * L, d_model), generator=g, dtype=torch.float32)
+    w = torch.randn((d_model, H), generator=g, dtype=torch.float32) * 0.02
+    b = torch.rand(H, generator=g, dtype=torch.float32) * 9.0 + 1.0
+    if mu is not None:
+        b = torch.tensor([float(mu[h % len(mu)]) for h in range(H)], dtype=torch.float32)
+    return {"x": x.bfloat16().contiguous(), "w_f": w.bfloat16().contiguous(), "b_f": b}

@@ -576,3 +576,60 @@ def test_qk_projection_by_a_permutation_moves_columns():
     for b in range(B):
         for h in range(H):
             np.testing.assert_array_equal(q[b, h], x[b * L:(b + 1) * L][:, perm[h * d:(h + 1) * d]])
+
+
+# --------------------------------------------------------------------------
+# Gate projection (Sec. 2, f = sigmoid(w_f^T x + b_f)): float32 dot products in
+# ascending feature order, log sigmoid in float64
+# --------------------------------------------------------------------------
+
+def test_gate_logits_dyadic_closed_form():
+    # dyadic x and w whose partial sums all stay exact in float32: the logit is
+    # the exact dot product plus the bias
+    from fractions import Fraction
+    rng = _rng(11)
+    T, Dm, H = 5, 64, 3
+    x = rng.integers(-8, 9, size=(T, Dm)) / 8.0
+    w = rng.integers(-8, 9, size=(Dm, H)) / 16.0
+    b = np.array([1.5, -2.25, 0.0], dtype=np.float32)
+    a = orc.gate_logits(x, w, b)
+    for t in range(T):
+        for h in range(H):
+            exact = sum(Fraction(float(x[t, k])) * Fraction(float(w[k, h])) for k in range(Dm))
+            assert Fraction(float(a[t, h])) == exact + Fraction(float(b[h]))
+
+
+def test_gate_logits_sum_in_ascending_feature_order():
+    # 1 followed by 2^-25 terms: each float32 step rounds 1 + 2^-25 back to 1, so
+    # the ascending sum is exactly 1; a float64 or reversed sum would not be
+    Dm = 64
+    x = np.full((1, Dm), 2.0 ** -25, dtype=np.float32)
+    x[0, 0] = 1.0
+    w = np.ones((Dm, 1), dtype=np.float32)
+    a = orc.gate_logits(x, w, np.zeros(1, dtype=np.float32))
+    assert a[0, 0] == np.float32(1.0)
+    assert float(np.sum(x.astype(np.float64))) != 1.0
+
+
+def test_log_sigmoid_special_values():
+    lf = orc.log_sigmoid(np.array([0.0, 3.0, 30.0, -30.0, -200.0], dtype=np.float32))
+    assert lf[0] == np.float32(math.log(0.5))
+    assert lf[1] == np.float32(math.log(1.0 / (1.0 + math.exp(-3.0))))
+    # large a: log sigmoid(a) = -e^-a (1 - e^-a / 2 + ...); float32 keeps it nonzero
+    assert lf[2] == np.float32(-math.exp(-30.0) * (1.0 - math.exp(-30.0) / 2.0))
+    assert lf[2] < 0.0
+    assert lf[3] == np.float32(-30.0 - math.log1p(math.exp(-30.0)))
+    assert lf[4] == np.float32(-200.0)
+    assert np.all(lf <= 0.0)
+
+
+def test_gate_log_forget_layout_and_head_permutation():
+    p = workloads.gate_inputs(2, 128, 64, 3, seed=12)
+    x, w, b = (p[n].float().numpy() for n in ("x", "w_f", "b_f"))
+    lf = orc.gate_log_forget(x, w, b, 2)
+    assert lf.shape == (2, 3, 128) and lf.dtype == np.float32
+    a = orc.gate_logits(x, w, b)
+    np.testing.assert_array_equal(lf[1, 2, 5], orc.log_sigmoid(a[128 + 5, 2]))
+    perm = [2, 0, 1]
+    lf2 = orc.gate_log_forget(x, w[:, perm], b[perm], 2)
+    np.testing.assert_array_equal(lf2, lf[:, perm])
