@@ -266,6 +266,80 @@ def run_projection(reps: int = 20, d_model: int = 768):
             "torch_matmul_us": round(mm_us, 2)}
 
 
+def run_gate_fusion(reps: int = 20, d_model: int = 768):
+    """The forget-gate producer with c in its epilogue on the 125M-shaped layer
+    (X [B*L, d_model] bf16, d_model = 768 as in the paper's 125M model): its own
+    time, the stage-1 plan kernel after it (no scan) against the plan kernel that
+    scans log f, and the unfused sequence a model would otherwise run (torch's
+    bf16 matmul for the gate logits, a log-sigmoid, and stage 1 with its scan)."""
+    import torch
+    from paper_2504_06949_amd import acp, workloads
+
+    w = workloads.WORKLOADS["125m"]
+    B, L, H, d = w.B, w.L, w.H, w.d
+    p = workloads.gate_inputs(B, L, d_model, H, seed=9)
+    dev = torch.device("cuda:0")
+    x, wf, bf = (p[n].to(dev) for n in ("x", "w_f", "b_f"))
+    g = {k: v.to(dev) for k, v in workloads.generate(w).items() if torch.is_tensor(v)}
+    ws = acp.workspace(g["q"])
+    lf = torch.empty((B, H, L), dtype=torch.float32, device=dev)
+    o = torch.empty_like(g["q"])
+    lse = torch.empty((B, H, L), dtype=torch.float32, device=dev)
+    grads = (torch.empty_like(g["q"]), torch.empty_like(g["k"]), torch.empty_like(g["v"]),
+             torch.empty((B, H, L), dtype=torch.float32, device=dev))
+
+    def timed(fn, n=reps):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(n):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / n
+
+    def gated_step():
+        acp.gate_project(x, wf, bf, B, H, d, ws=ws, log_f=lf)
+        acp.forward_gated(g["q"], g["k"], g["v"], w.eps, ws, out=(o, lse))
+        acp.backward(g["q"], g["k"], g["v"], o, g["do"], ws, out=grads)
+
+    def plain_step():
+        acp.forward(g["q"], g["k"], g["v"], lf, w.eps, ws=ws, out=(o, lse))
+        acp.backward(g["q"], g["k"], g["v"], o, g["do"], ws, out=grads)
+
+    gate_us = timed(lambda: acp.gate_project(x, wf, bf, B, H, d, ws=ws, log_f=lf))
+    step_us = timed(gated_step)
+    acp.acp_timing_enable(True)
+    for label, fn in (("gated", gated_step), ("plain", plain_step)):
+        acp.acp_timing_reset()
+        for _ in range(reps):
+            fn()
+        torch.cuda.synchronize()
+        kt = acp.acp_timing_read()
+        pk = {k: (v[1] / v[0] * 1e3 if v[0] else 0.0) for k, v in kt.items()}
+        if label == "gated":
+            pk_g = pk
+        else:
+            pk_p = pk
+    acp.acp_timing_enable(False)
+    mm_us = timed(lambda: torch.nn.functional.logsigmoid(
+        torch.matmul(x, wf).float() + bf).view(B, L, H).permute(0, 2, 1).contiguous())
+    stage1_g = pk_g["rownorm"] + pk_g["plan"] + pk_g["schedule"]
+    return {"workload": f"X [{B * L}, {d_model}] bf16, w_f [{d_model}, {H}] -> log f, c "
+                        f"[{B}, {H}, {L}]; then fwd + bwd of the 125m layer",
+            "gate_us": round(gate_us, 2),
+            "plan_after_gate_us": round(pk_g["plan"], 2),
+            "plan_with_scan_us": round(pk_p["plan"], 2),
+            "fused_us": round(gate_us + pk_g["plan"], 2),
+            "unfused_us": round(mm_us + pk_p["plan"], 2),
+            "torch_gate_logits_us": round(mm_us, 2),
+            "step_ms": round(step_us / 1e3, 4),
+            "stage1_share": round(stage1_g * 1e-3 / (step_us / 1e3), 4),
+            "gate_share": round(gate_us / step_us, 4)}
+
+
 def cpu_baseline(res, budget_s: float = 15.0):
     """The oracle, untuned, on whole heads of the same workload until the budget is spent."""
     import numpy as np
@@ -406,6 +480,7 @@ def main():
             "per_kernel_ms")
         prj["norm_pass_us_saved"] = round(pk125["rownorm"] * 1e3, 2) if pk125 else None
         out["projection"] = prj
+        out["gate_fusion"] = run_gate_fusion()
     out["paper_context"] = PAPER_CONTEXT
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(res)

@@ -46,7 +46,7 @@ class DecodeLayout(ctypes.Structure):
 
 
 K_NAMES = ("rownorm", "plan", "fwd", "dsum", "dq", "dkdv", "dlogf", "decode_init", "decode",
-           "project", "schedule")
+           "project", "schedule", "gate")
 
 
 class KernelTimes(ctypes.Structure):
@@ -69,6 +69,8 @@ _SIGS = {
                             _p],
     "fox_attn_bwd": [_p, _p, _p, _p, _p, _i, _i, _i, _i, _i, _p, _p, _p, _p, _p, _sz, _p],
     "fox_attn_fwd_noalloc": [_p, _p, _p, _p, _i, _i, _i, _i, _i, _d, _p, _p, _p],
+    "acp_gate_project": [_p, _p, _p, _i, _i, _i, _i, _i, _p, _p, _sz, _p],
+    "fox_attn_fwd_gated": [_p, _p, _p, _i, _i, _i, _i, _i, _d, _p, _p, _p, _sz, _p],
     "acp_noalloc_scratch_bytes": [],
     "acp_qk_project": [_p, _p, _p, _i, _i, _i, _i, _i, _i, _p, _p, _p, _sz, _p],
     "fox_attn_fwd_projected": [_p, _p, _p, _p, _i, _i, _i, _i, _i, _d, _p, _p, _p, _sz, _p],
@@ -154,6 +156,14 @@ def fox_attn_fwd(Q, K, V, log_f, dt, B, H, L, d, eps, O, lse, ws, ws_bytes, stre
 
 def fox_attn_fwd_noalloc(Q, K, V, log_f, dt, B, H, L, d, eps, O, lse, stream) -> int:
     return lib().fox_attn_fwd_noalloc(Q, K, V, log_f, dt, B, H, L, d, eps, O, lse, stream)
+
+
+def acp_gate_project(X, w_f, b_f, B, L, d_model, H, d, log_f, ws, ws_bytes, stream) -> int:
+    return lib().acp_gate_project(X, w_f, b_f, B, L, d_model, H, d, log_f, ws, ws_bytes, stream)
+
+
+def fox_attn_fwd_gated(Q, K, V, dt, B, H, L, d, eps, O, lse, ws, ws_bytes, stream) -> int:
+    return lib().fox_attn_fwd_gated(Q, K, V, dt, B, H, L, d, eps, O, lse, ws, ws_bytes, stream)
 
 
 def acp_noalloc_scratch_bytes() -> int:
@@ -399,6 +409,54 @@ def forward(q, k, v, log_f, eps: float, ws: torch.Tensor | None = None, out=None
                         B, H, L, d, eps, o.data_ptr(), lse.data_ptr(), ws.data_ptr(), ws.numel(),
                         _stream(dev)))
     return o, lse, ws
+
+
+def gate_project(x, w_f, b_f, B: int, H: int, d: int, ws: torch.Tensor | None = None,
+                 log_f: torch.Tensor | None = None, dtype=torch.bfloat16):
+    """log f [B, H, L] of the gate projection of X [B*L, d_model] (bf16) with w_f
+    [d_model, H] (bf16) and b_f [H] (float32); the workspace receives c and the
+    gate checks that forward_gated() then uses.  Returns (log_f, ws)."""
+    dev = _dev(x, w_f, b_f)
+    if x.dim() != 2 or w_f.dim() != 2 or w_f.shape[0] != x.shape[1] or w_f.shape[1] != H:
+        raise ValueError("X must be [B*L, d_model] and w_f [d_model, H]")
+    if x.dtype != torch.bfloat16 or w_f.dtype != torch.bfloat16 or b_f.dtype != torch.float32:
+        raise TypeError("X and w_f must be bfloat16, b_f float32")
+    if tuple(b_f.shape) != (H,):
+        raise ValueError("b_f must be [H]")
+    M, Dm = (int(t) for t in x.shape)
+    if M % B != 0:
+        raise ValueError("shape mismatch")
+    L = M // B
+    if ws is None:
+        ws = torch.empty(acp_workspace_size(B, H, L, d, _dt_of(dtype)), dtype=torch.uint8,
+                         device=dev)
+    if log_f is None:
+        log_f = torch.empty((B, H, L), dtype=torch.float32, device=dev)
+    _check(acp_gate_project(x.data_ptr(), w_f.data_ptr(), b_f.data_ptr(), B, L, Dm, H, d,
+                            log_f.data_ptr(), ws.data_ptr(), ws.numel(), _stream(dev)))
+    return log_f, ws
+
+
+def forward_gated(q, k, v, eps: float, ws: torch.Tensor, out=None):
+    """forward() for the gates gate_project() left in `ws`: stage 1 reads c from
+    there instead of scanning log f.  Returns (O, lse, ws)."""
+    dev = _dev(q, k, v)
+    B, H, L, d = _shape(q)
+    if k.shape != q.shape or v.shape != q.shape or k.dtype != q.dtype or v.dtype != q.dtype:
+        raise ValueError("Q, K, V must share shape and dtype")
+    if out is None:
+        o = torch.empty_like(q)
+        lse = torch.empty((B, H, L), dtype=torch.float32, device=dev)
+    else:
+        o, lse = out
+    _check(fox_attn_fwd_gated(q.data_ptr(), k.data_ptr(), v.data_ptr(), _dt(q), B, H, L, d, eps,
+                              o.data_ptr(), lse.data_ptr(), ws.data_ptr(), ws.numel(),
+                              _stream(dev)))
+    return o, lse, ws
+
+
+def _dt_of(dtype) -> int:
+    return ACP_F32 if dtype == torch.float32 else ACP_BF16
 
 
 def backward(q, k, v, o, do, ws: torch.Tensor, out=None):

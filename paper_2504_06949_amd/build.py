@@ -21,7 +21,7 @@ LIB = os.path.join(PKG, "libacp.so")
 BUILD_DIR = os.path.join(PKG, "_build")
 
 SOURCES = ["acp_api.cpp", "acp_plan.hip", "fox_fwd.hip", "fox_bwd.hip", "fox_bwd_mfma.hip",
-           "acp_decode.hip", "acp_project.hip", "acp_noalloc.hip"]
+           "acp_decode.hip", "acp_project.hip", "acp_noalloc.hip", "acp_gate.hip"]
 
 COMMON = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",

@@ -32,7 +32,7 @@ acp_status ok() {
 
 struct Layout {
     size_t c, u, delta, rs, ce, kept, flags, part, lse2, dsum, rowsum, colsum, sched_q, sched_k,
-        total;
+        gate_agg, gate_incl, gate_stats, total;
     int nchunk;
 };
 
@@ -61,6 +61,9 @@ Layout layout(int B, int H, int L, int d) {
     const size_t nb = ((size_t)L + 127) / 128;   // 128-row blocks of the attention kernels
     y.sched_q = take(BH * nb * 4);
     y.sched_k = take(BH * nb * 4);
+    y.gate_agg = take(BH * M * 8);      // gate producer's chained scan (acp_gate_project)
+    y.gate_incl = take(BH * M * 8);
+    y.gate_stats = take(BH * M * sizeof(acp::GateStats));
     y.total = off;
     return y;
 }
@@ -313,13 +316,14 @@ acp_status acp_boundary_qknorm(const float* log_f, const float* gamma_q, const f
 static acp_status fwd_common(const void* Q, const void* K, const void* V, const float* log_f,
                              const float* gamma_q, const float* gamma_k, acp_dtype dt, int B,
                              int H, int L, int d, double eps, void* O, float* lse, void* ws,
-                             size_t ws_bytes, void* stream, bool norms_ready = false) {
+                             size_t ws_bytes, void* stream, bool norms_ready = false,
+                             bool gated = false) {
     ACP_TRY(check_shape(B, H, L, d, dt));
     ACP_TRY(check_eps(eps));
     ACP_TRY(check_ptr(Q, "Q"));
     ACP_TRY(check_ptr(K, "K"));
     ACP_TRY(check_ptr(V, "V"));
-    ACP_TRY(check_ptr(log_f, "log_f"));
+    if (!gated) ACP_TRY(check_ptr(log_f, "log_f"));
     ACP_TRY(check_ptr(O, "O"));
     ACP_TRY(check_ptr(lse, "lse"));
     const Layout y = layout(B, H, L, d);
@@ -329,6 +333,7 @@ static acp_status fwd_common(const void* Q, const void* K, const void* V, const 
     p.gamma_q = gamma_q;
     p.gamma_k = gamma_k;
     p.norms_ready = norms_ready;
+    if (gated) p.gate = (const acp::GateStats*)(w + y.gate_stats);
     hipError_t e = acp::launch_plan(p, (hipStream_t)stream);
     if (e != hipSuccess) return hip_status(e, "fox_attn_fwd boundary launch");
     if (dt == ACP_BF16) {
@@ -372,6 +377,45 @@ acp_status fox_attn_fwd_projected(const void* Q, const void* K, const void* V, c
                                   float* lse, void* ws, size_t ws_bytes, void* stream) {
     return fwd_common(Q, K, V, log_f, nullptr, nullptr, dt, B, H, L, d, eps, O, lse, ws,
                       ws_bytes, stream, true);
+}
+
+acp_status acp_gate_project(const void* X, const void* w_f, const float* b_f, int B, int L,
+                            int d_model, int H, int d, float* log_f, void* ws, size_t ws_bytes,
+                            void* stream) {
+    ACP_TRY(check_shape(B, H, L, d, ACP_BF16));
+    if (d_model <= 0 || d_model % 64 != 0 || d_model > 8192)
+        return fail(ACP_EUNSUPPORTED, "d_model=%d is not a multiple of 64 in [64, 8192]", d_model);
+    if (H > 64) return fail(ACP_EUNSUPPORTED, "H=%d: the gate projection takes at most 64 heads", H);
+    ACP_TRY(check_ptr(X, "X"));
+    ACP_TRY(check_ptr(w_f, "w_f"));
+    if (b_f == nullptr) return fail(ACP_EINVAL, "b_f is NULL");
+    ACP_TRY(check_ptr(log_f, "log_f"));
+    const Layout y = layout(B, H, L, d);
+    ACP_TRY(check_ws(ws, ws_bytes, y));
+    char* w = (char*)ws;
+    acp::GateArgs a{};
+    a.X = X; a.W = w_f; a.bias = b_f;
+    a.B = B; a.L = L; a.Dm = d_model; a.H = H;
+    a.log_f = log_f;
+    a.c = (float*)(w + y.c);
+    a.agg = (unsigned long long*)(w + y.gate_agg);
+    a.incl = (unsigned long long*)(w + y.gate_incl);
+    a.stats = (acp::GateStats*)(w + y.gate_stats);
+    // the float32 copy of the weights goes where the backward keeps Delta' (free
+    // until a backward runs on this workspace)
+    const size_t wq_bytes = (size_t)((H + 3) / 4) * d_model * 16;
+    if (wq_bytes > (size_t)B * H * L * 4)
+        return fail(ACP_EUNSUPPORTED, "d_model=%d too large for these shapes (%zu bytes of "
+                    "float32 weights, %zu available)", d_model, wq_bytes, (size_t)B * H * L * 4);
+    a.wq = w + y.dsum;
+    return hip_status(acp::launch_gate(a, (hipStream_t)stream), "acp_gate_project launch");
+}
+
+acp_status fox_attn_fwd_gated(const void* Q, const void* K, const void* V, acp_dtype dt, int B,
+                              int H, int L, int d, double eps, void* O, float* lse, void* ws,
+                              size_t ws_bytes, void* stream) {
+    return fwd_common(Q, K, V, nullptr, nullptr, nullptr, dt, B, H, L, d, eps, O, lse, ws,
+                      ws_bytes, stream, false, true);
 }
 
 acp_status acp_qk_project(const void* X, const void* Wq, const void* Wk, acp_dtype dt, int B,

@@ -9,6 +9,14 @@
 
 namespace acp {
 
+// Per-block statistics of the gate producer (one entry per 64 gates of a head)
+// that stage 1's checks need in place of its own pass over log f.
+struct GateStats {
+    double abs_sum;           // float64 sum of |log f|
+    int min_lsb;              // smallest float32 ulp exponent of a nonzero gate
+    int flags;                // bit 1: a non-finite gate; bit 5: the chained scan timed out
+};
+
 struct PlanArgs {
     const void* Q;
     const void* K;
@@ -20,6 +28,8 @@ struct PlanArgs {
     const float* gamma_q;     // [H] QK-norm scale bounds, or null: U from the row norms
     const float* gamma_k;     // [H]
     bool norms_ready;         // part already holds the chunk maxima (the projection's epilogue)
+    const GateStats* gate;    // non-null: c is already in place (the gate producer's
+                              // epilogue) and these are its per-head statistics
     double* part;             // [B*H, 2, nchunk]
     float* c;                 // [B*H, L]
     double* u;                // [B*H]
@@ -28,6 +38,19 @@ struct PlanArgs {
     int* col_end;             // [B*H, M]
     long long* kept;          // [B*H]
     int* flags;               // [B*H]
+};
+
+struct GateArgs {
+    const void* X;            // [B*L, Dm] bf16 layer inputs
+    const void* W;            // [Dm, H] bf16 gate weights
+    const float* bias;        // [H]
+    int B, L, Dm, H;
+    float* log_f;             // [B*H, L]
+    float* c;                 // [B*H, L]
+    unsigned long long* agg;  // [B*H, L/64] block totals (float64 bits)
+    unsigned long long* incl; // [B*H, L/64] inclusive prefixes (float64 bits)
+    GateStats* stats;         // [B*H, L/64]
+    void* wq;                 // [ceil(H/4), Dm] float4: the weights by group of 4 heads
 };
 
 struct FwdArgs {
@@ -132,6 +155,7 @@ int norm_chunks(int L);
 hipError_t launch_schedule(const long long* kept, const int* row_start, const int* col_end,
                            int BH, int M, int nb, int* sched_q, int* sched_k, hipStream_t s);
 hipError_t launch_plan(const PlanArgs& a, hipStream_t s);
+hipError_t launch_gate(const GateArgs& a, hipStream_t s);
 hipError_t launch_fwd(const FwdArgs& a, hipStream_t s);
 hipError_t launch_bwd(const BwdArgs& a, hipStream_t s);
 hipError_t launch_dq_bf16(const BwdArgs& a, hipStream_t s);

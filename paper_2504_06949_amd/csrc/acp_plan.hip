@@ -10,7 +10,9 @@
 //                         log f into c, then find every row's first kept block
 //                         and every column's last kept block.
 // With QK-norm scale bounds (App. E: U = gamma_q gamma_k sqrt(d)) the first
-// launch is skipped and the plan kernel takes U from the scales.
+// launch is skipped and the plan kernel takes U from the scales.  After the
+// gate producer (acp_gate.hip), which leaves c and the gates' statistics in
+// place, the plan kernel reads the block corners of c instead of scanning log f.
 #include "acp_device.h"
 #include "acp_internal.h"
 #include "acp_scan.h"
@@ -118,8 +120,8 @@ constexpr int kPlanHeld = 16;   // log f values a thread keeps in registers (L <
 
 __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
     const float* __restrict__ log_f, const double* __restrict__ part, int nchunk,
-    const float* __restrict__ gamma_q, const float* __restrict__ gamma_k, int H,
-    int L, int d, double log_l_over_eps,
+    const float* __restrict__ gamma_q, const float* __restrict__ gamma_k,
+    const GateStats* __restrict__ gate, int H, int L, int d, double log_l_over_eps,
     float* __restrict__ c_out,
     double* __restrict__ u_out, double* __restrict__ delta_out,
     int* __restrict__ row_start, int* __restrict__ col_end,
@@ -137,7 +139,8 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
     const float* x = log_f + (size_t)bh * L;
     float* cw = c_out + (size_t)bh * L;
     const int per = (L + kPlanThreads - 1) / kPlanThreads;
-    const int beg = min(t * per, L), n = min(beg + per, L) - beg;
+    const bool gated = gate != nullptr;   // c in place: no gates to read or scan
+    const int beg = min(t * per, L), n = gated ? 0 : min(beg + per, L) - beg;
     const bool held = per <= kPlanHeld;
     const bool vec = held && (per & 3) == 0;   // then n is per or 0
     float xv[kPlanHeld];
@@ -174,7 +177,18 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
         local += (double)v;
         local_abs += __builtin_fabs((double)v);
     };
-    if (held) {
+    int gate_flags = 0;
+    if (gated) {
+        // the producer's per-block statistics (sum of |log f|, smallest ulp
+        // exponent, flags) take the place of the gates themselves
+        const int M0 = L / kBlock;
+        for (int m = t; m < M0; m += kPlanThreads) {
+            const GateStats g = gate[(size_t)bh * M0 + m];
+            local_abs += g.abs_sum;
+            min_lsb = min(min_lsb, g.min_lsb);
+            gate_flags |= g.flags;
+        }
+    } else if (held) {
 #pragma unroll
         for (int i = 0; i < kPlanHeld; ++i)
             if (i < n) take(xv[i]);
@@ -195,7 +209,9 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
         min_lsb = min(min(__builtin_amdgcn_readlane(rl, 0), __builtin_amdgcn_readlane(rl, 16)),
                       min(__builtin_amdgcn_readlane(rl, 32), __builtin_amdgcn_readlane(rl, 48)));
     }
-    const int wflags = (__ballot(positive) != 0ull ? 1 : 0) | (__ballot(nonfinite) != 0ull ? 2 : 0);
+    const int wflags = (__ballot(positive) != 0ull ? 1 : 0) |
+                       (__ballot(nonfinite || (gate_flags & 2)) != 0ull ? 2 : 0) |
+                       (__ballot(gate_flags & 32) != 0ull ? 32 : 0);
     if (norms && wid * 64 < nchunk) {   // only waves that loaded partials
         const auto mx = [](double a, double b) { return nan_max(a, b); };
         const double rq = row16_reduce(mq, mx), rk = row16_reduce(mk, mx);
@@ -291,7 +307,12 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
         if ((j & (kBlock - 1)) == 0) s_first[j / kBlock] = cf;
         if ((j & (kBlock - 1)) == kBlock - 1) s_last[j / kBlock] = cf;
     };
-    if (vec) {
+    if (gated) {
+        for (int m = t; m < M; m += kPlanThreads) {
+            s_first[m] = cw[kBlock * m];
+            s_last[m] = cw[kBlock * m + kBlock - 1];
+        }
+    } else if (vec) {
 #pragma unroll
         for (int i = 0; i < kPlanHeld; i += 4) {
             if (i < n) {
@@ -529,7 +550,7 @@ hipError_t launch_plan(const PlanArgs& a, hipStream_t s) {
     }
     trace_begin(ACP_K_PLAN, s);
     hipLaunchKernelGGL(plan_kernel, dim3(BH), dim3(kPlanThreads), 0, s,
-                       a.log_f, a.part, a.nchunk, a.gamma_q, a.gamma_k, a.H, a.L, a.d,
+                       a.log_f, a.part, a.nchunk, a.gamma_q, a.gamma_k, a.gate, a.H, a.L, a.d,
                        a.log_l_over_eps,
                        a.c, a.u, a.delta, a.row_start, a.col_end, a.kept, a.flags);
     e = hipGetLastError();

@@ -23,7 +23,8 @@ def test_every_declared_symbol_is_exported():
                           "acp_decode_init", "fox_attn_decode",
                           "acp_timing_enable", "acp_timing_reset",
                           "acp_timing_read", "acp_status_string", "acp_last_error",
-                          "acp_noalloc_scratch_bytes", "fox_attn_fwd_noalloc"}
+                          "acp_noalloc_scratch_bytes", "fox_attn_fwd_noalloc",
+                          "acp_gate_project", "fox_attn_fwd_gated"}
     lib = ctypes.CDLL(acp.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
@@ -222,3 +223,20 @@ def test_noalloc_forward_rejects_shapes_beyond_its_fixed_scratch():
     assert "fox_attn_fwd_noalloc" in acp.acp_last_error()
     st = acp.fox_attn_fwd_noalloc(16, 16, 16, 16, acp.ACP_BF16, 1, 1, 100, 64, 1e-4, 16, 16, None)
     assert st == acp.ACP_EUNSUPPORTED
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(X=0), acp.ACP_EINVAL),
+    (dict(w_f=8), acp.ACP_EINVAL),                 # misaligned
+    (dict(b_f=0), acp.ACP_EINVAL),
+    (dict(d_model=96), acp.ACP_EUNSUPPORTED),
+    (dict(H=65), acp.ACP_EUNSUPPORTED),
+    (dict(d_model=8200), acp.ACP_EUNSUPPORTED),
+    (dict(L=100), acp.ACP_EUNSUPPORTED),
+    (dict(ws_bytes=16), acp.ACP_EWORKSPACE),
+])
+def test_gate_project_rejects_bad_arguments(kw, status):
+    a = dict(X=16, w_f=16, b_f=16, B=1, L=64, d_model=64, H=2, d=64, log_f=16, ws=16,
+             ws_bytes=1 << 40, stream=None)
+    a.update(kw)
+    assert acp.acp_gate_project(*a.values()) == status
