@@ -175,10 +175,15 @@ def run_decode(steps: int = 64, warmup: int = 16, L0: int = 4096, C: int = 8192)
     w0 = workloads.WORKLOADS["125m"]
     n_tok = warmup + 2 * steps
     L = L0 + 64 * ((n_tok + 63) // 64)
-    w = workloads.custom("125m_decode", w0.B, w0.H, L, w0.d, "bf16", w0.seed, qk_norm=True)
-    x = workloads.generate(w, with_grad=False)
     dev = torch.device("cuda:0")
-    g = {n: x[n].to(dev) for n in ("q", "k", "v", "log_f", "gamma_q", "gamma_k")}
+    if L0 <= 4096:
+        w = workloads.custom("125m_decode", w0.B, w0.H, L, w0.d, "bf16", w0.seed, qk_norm=True)
+        x = workloads.generate(w, with_grad=False)
+        g = {n: x[n].to(dev) for n in ("q", "k", "v", "log_f", "gamma_q", "gamma_k")}
+    else:
+        # long prompts: drawn on the GPU (timing only)
+        w = workloads.custom("125m_decode", w0.B, w0.H, L, w0.d, "bf16", w0.seed, qk_norm=True)
+        g = workloads.long_decode_inputs(w0.B, w0.H, L, w0.d, w0.seed, dev)
     prompt = {n: g[n][:, :, :L0].contiguous() for n in ("k", "v", "log_f")}
     toks = [{n: g[n][:, :, t].contiguous() for n in ("q", "k", "v", "log_f")}
             for t in range(L0, L0 + n_tok)]
@@ -474,6 +479,9 @@ def main():
         out["other_workloads"] = extra
     if not args.no_decode:
         out["decode"] = run_decode()
+        # the regime App. F reports on: long prompts (the ring holds the whole
+        # context, so every kept key is attended)
+        out["decode_long"] = {str(n): run_decode(L0=n, C=n + 256) for n in (16384, 65536)}
         prj = run_projection()
         # the norm pass the fused epilogue replaces, as timed on the 125m layer
         pk125 = pk if w.name == "125m" else out.get("other_workloads", {}).get("125m", {}).get(

@@ -406,18 +406,19 @@ __global__ __launch_bounds__(kDecChunk) void decode_step_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// The partial sums of one head merged into O and lse: one workgroup of 256
-// threads per head.  Thread i requests dim i mod D of splits i / D, i / D + 256 / D,
-// ... (up to kHeld of them) and the (max, sum) of split i before it waits.
-template <typename T, int D>
-__global__ __launch_bounds__(kDecChunk) void decode_combine_kernel(
+// The partial sums of one head merged into O and lse: one workgroup per head,
+// of 256 threads, or 1024 when a long context leaves more than 256 splits (up to
+// 512).  Thread i takes the (max, sum) of split i, and dim i mod D of splits
+// i / D, i / D + THREADS / D, ..., whose loads it issues kBatch at a time before
+// it waits for any of them.
+template <typename T, int D, int THREADS>
+__global__ __launch_bounds__(THREADS) void decode_combine_kernel(
     int nsplit, const float* __restrict__ part, T* __restrict__ O, float* __restrict__ lse) {
-    constexpr int kWaves = kDecChunk / 64;
-    constexpr int kGroups = kDecChunk / D;
-    constexpr int kMaxSplit = 64 * 2048 / kDecChunk;
-    constexpr int kHeld = 8;
-    __shared__ float w_s[kMaxSplit];
-    __shared__ float o_s[kDecChunk];
+    constexpr int kWaves = THREADS / 64;
+    constexpr int kGroups = THREADS / D;
+    constexpr int kBatch = 8;
+    __shared__ float w_s[THREADS];   // nsplit <= THREADS
+    __shared__ float o_s[THREADS];
     __shared__ float s_m[kWaves], s_l[kWaves];
     const int bh = blockIdx.x, BH = gridDim.x, tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
     const float* pml = part + (size_t)bh * nsplit * 2;
@@ -426,21 +427,9 @@ __global__ __launch_bounds__(kDecChunk) void decode_combine_kernel(
 
     const int sm = min(tid, nsplit - 1);
     float ms = pml[2 * sm], ls = pml[2 * sm + 1];
-    float ov[kHeld];
-#pragma unroll
-    for (int r = 0; r < kHeld; ++r) ov[r] = po[(size_t)min(grp + kGroups * r, nsplit - 1) * D + dim];
     if (tid >= nsplit) {
         ms = -INFINITY;
         ls = 0.f;
-    }
-    const float m0 = ms;
-    for (int s2 = tid + kDecChunk; s2 < nsplit; s2 += kDecChunk) {   // more than 256 splits
-        const float m2 = pml[2 * s2], l2 = pml[2 * s2 + 1];
-        const float mx = fmaxf(ms, m2);
-        if (mx != -INFINITY) {
-            ls = ls * fast_exp2(ms - mx) + l2 * fast_exp2(m2 - mx);
-            ms = mx;
-        }
     }
     float M = ms;
 #pragma unroll
@@ -454,26 +443,26 @@ __global__ __launch_bounds__(kDecChunk) void decode_combine_kernel(
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) L += __shfl_xor(L, off);
     if (lane == 0) s_l[wid] = L;
-    if (tid < nsplit) w_s[tid] = fast_exp2(m0 - M);
-    for (int s2 = tid + kDecChunk; s2 < nsplit; s2 += kDecChunk) w_s[s2] = fast_exp2(pml[2 * s2] - M);
+    if (tid < nsplit) w_s[tid] = fast_exp2(ms - M);
     __syncthreads();
     L = s_l[0];
 #pragma unroll
     for (int w = 1; w < kWaves; ++w) L += s_l[w];
     // splits without a kept key (weight 0) hold no O: selected away, not multiplied
     float o = 0.f;
+    for (int s0 = grp; s0 < nsplit; s0 += kGroups * kBatch) {
+        float pv[kBatch];
 #pragma unroll
-    for (int r = 0; r < kHeld; ++r) {
-        const int s2 = grp + kGroups * r;
-        if (s2 < nsplit) {
-            const float w = w_s[s2];
-            o += w != 0.f ? w * ov[r] : 0.f;
+        for (int r = 0; r < kBatch; ++r)
+            pv[r] = po[(size_t)min(s0 + kGroups * r, nsplit - 1) * D + dim];
+#pragma unroll
+        for (int r = 0; r < kBatch; ++r) {
+            const int s2 = s0 + kGroups * r;
+            if (s2 < nsplit) {
+                const float w = w_s[s2];
+                o += w != 0.f ? w * pv[r] : 0.f;
+            }
         }
-    }
-    for (int s2 = grp + kGroups * kHeld; s2 < nsplit; s2 += kGroups) {
-        const float w = w_s[s2];
-        const float pv = po[(size_t)s2 * D + dim];
-        o += w != 0.f ? w * pv : 0.f;
     }
     o_s[tid] = o;
     __syncthreads();
@@ -519,8 +508,13 @@ static hipError_t step_t(const DecodeArgs& a, hipStream_t s) {
                        kLog2e / sqrtf((float)D));
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((decode_combine_kernel<T, D>), dim3(a.B * a.H), dim3(kDecChunk), 0, s,
-                       nsplit, a.part, (T*)a.O, a.lse);
+    static_assert(64 * 2048 / kDecChunk <= 1024, "one split per combine thread");
+    if (nsplit <= 256)
+        hipLaunchKernelGGL((decode_combine_kernel<T, D, 256>), dim3(a.B * a.H), dim3(256), 0, s,
+                           nsplit, a.part, (T*)a.O, a.lse);
+    else
+        hipLaunchKernelGGL((decode_combine_kernel<T, D, 1024>), dim3(a.B * a.H), dim3(1024), 0, s,
+                           nsplit, a.part, (T*)a.O, a.lse);
     return hipGetLastError();
 }
 

@@ -170,3 +170,30 @@ def gate_inputs(B: int, L: int, d_model: int, H: int, seed: int, mu=None) -> dic
     if mu is not None:
         b = torch.tensor([float(mu[h % len(mu)]) for h in range(H)], dtype=torch.float32)
     return {"x": x.bfloat16().contiguous(), "w_f": w.bfloat16().contiguous(), "b_f": b}
+
+
+def long_decode_inputs(B: int, H: int, L: int, d: int, seed: int, device) -> dict:
+    """Seeded inputs for timing decoding after a long prompt (16k-64k tokens),
+    drawn on `device` so that tens of millions of rows need no host round trip:
+    q, k, v [B, H, L, d] bf16 with q and k RMS-normalised and scaled by per-head
+    weights from U[0.5, 1.5]^d (the QK-norm setting of App. E, shrunk by 1 - 2^-7
+    as in generate()), gates a ~ N(mu_h, 0.5) with mu_h ~ U[1, 10] (drawn on the
+    CPU, log f = -softplus(-a) in float64 rounded to float32), and the scale
+    bounds gamma_q, gamma_k [H]."""
+    g = torch.Generator(device="cpu")
+    g.manual_seed(seed)
+    mu = torch.rand(H, generator=g, dtype=torch.float64) * 9.0 + 1.0
+    z = torch.randn((B, H, L), generator=g, dtype=torch.float32)
+    a = mu.numpy().reshape(1, H, 1) + 0.5 * z.numpy().astype(np.float64)
+    out = {"log_f": torch.from_numpy(log_sigmoid_f32(a)).to(device)}
+    gd = torch.Generator(device=device)
+    gd.manual_seed(seed)
+    for name in ("q", "k", "v"):
+        x = torch.randn((B, H, L, d), generator=gd, dtype=torch.float32, device=device)
+        if name != "v":
+            wt = torch.rand((H, d), generator=g, dtype=torch.float32) + 0.5
+            x = x / torch.sqrt((x * x).mean(dim=-1, keepdim=True)) * (1.0 - 2.0 ** -7)
+            x = x * wt.to(device).view(1, H, 1, d)
+            out["gamma_" + name] = wt.abs().amax(dim=-1).contiguous().to(device)
+        out[name] = x.to(torch.bfloat16).contiguous()
+    return out
