@@ -129,7 +129,13 @@ acp_status acp_boundary(const void* Q, const void* K, const float* log_f, acp_dt
  * When q and k are RMS-normalised (mean square 1 over the d features) and then
  * scaled elementwise by weights of magnitude at most gamma_q[h], gamma_k[h],
  * |q.k| / sqrt(d) <= U = gamma_q[h] gamma_k[h] sqrt(d), so the pruning stays safe
- * without reading Q and K.  The caller vouches for that premise.
+ * without reading Q and K.  The caller vouches for that premise, and it must hold
+ * for the values the attention kernels read: every stored row needs
+ * |q| <= gamma_q sqrt(d) and |k| <= gamma_k sqrt(d).  Rounding a normalised row to
+ * bfloat16 can lengthen it by up to 2^-8 relative, so with bf16 inputs either
+ * scale the rows by 1 - 2^-8 (or less) before rounding, or pass gammas enlarged
+ * by (1 + 2^-8); otherwise U can fall short by that much and the pruned mass of
+ * a row can exceed eps (by a factor up to e^(4 U 2^-8)).
  *   in : log_f [B,H,L] float; gamma_q, gamma_k [H] float (>= 0, finite; shared over
  *        the batch); dt and d fix the workspace shape only.
  *   out: as acp_boundary; U = (gamma_q gamma_k) sqrt(d) in float64.  Flag bit 3
