@@ -43,7 +43,7 @@ struct alignas(1024) DqSmem {
 };
 
 template <int D>
-__global__ __launch_bounds__(kBwdThreads) __attribute__((amdgpu_waves_per_eu(D == 64 ? 3 : 1)))
+__global__ __launch_bounds__(kBwdThreads) __attribute__((amdgpu_waves_per_eu(D == 64 ? 3 : 2)))
 void dq_bf16_kernel(
     const __bf16* __restrict__ Q, const __bf16* __restrict__ K, const __bf16* __restrict__ V,
     const __bf16* __restrict__ O, const __bf16* __restrict__ dO, const float* __restrict__ cg,
@@ -157,12 +157,10 @@ void dq_bf16_kernel(
 
     // Each key tile is taken in two halves of 32 keys, each in three phases: A
     // forms S^T and dP^T (MFMA; key rows from LDS), B the softmax terms (VALU),
-    // C accumulates dQ (MFMA; key columns from LDS).  At d = 64 each phase reads
-    // its own LDS operands, so that the kernel fits 168 VGPRs: three waves per
-    // SIMD, whose interleaving hides the LDS latency.  At d = 128 (one wave per
-    // SIMD) each LDS operand is read one phase before it is used, as in the
-    // dK/dV pass, and the barrier that publishes the next tile sits before the
-    // second half's phase C.
+    // C accumulates dQ (MFMA; key columns from LDS).  Each phase reads its own
+    // LDS operands, so that the kernel fits 168 VGPRs at d = 64 (three waves per
+    // SIMD) and 256 at d = 128 (two): the other waves' interleaving hides the LDS
+    // latency.
     struct OpA {
         bf16x8 a[2][NDS], b[2][NDS];
         float4 lo, hi;                 // key biases (diagonal tiles: gates c_j) of the lane's 8 keys
@@ -255,13 +253,6 @@ void dq_bf16_kernel(
         }
         return DsH{{dsf[0], dsf[1]}};
     };
-    auto phase_c_part = [&](const OpC& rc, const DsH& y, int part) __attribute__((always_inline)) {
-#pragma unroll
-        for (int dt = part * NDT / 2; dt < (part + 1) * NDT / 2; ++dt) {
-            acc[0][dt] = mfma16(rc.ak[dt], y.d[0], acc[0][dt]);
-            acc[1][dt] = mfma16(rc.ak[dt], y.d[1], acc[1][dt]);
-        }
-    };
     // dQ^T += K^T dS^T over the half's 32 keys
     auto phase_c = [&](const OpC& rc, const DsH& y) __attribute__((always_inline)) {
 #pragma unroll
@@ -309,44 +300,108 @@ void dq_bf16_kernel(
     for (; n < n_mask; ++n) step(std::false_type{}, n);
     for (; n <= n_hi; ++n) step(std::true_type{}, n);
     } else {
-    // The diagonal tiles (m0 for waves 0-1, m0 + 1 = n_hi for waves 2-3) are the
-    // last two and go through the masking variant.
-    const int n_mask = max(n_lo, n_hi - 1);
-    // (read whether or not this wave takes the tile: no path keeps an older set
-    // of them live through the loop)
-    OpA ra = load_a(n_lo >= n_mask, 0, 0);
-    auto step = [&](auto mask_tag, int n) __attribute__((always_inline)) {
+    // d = 128: phase A is split in two, S^T with the key rows and dP^T with the
+    // value rows, each read just before its MFMAs, so that no more than one
+    // operand set is live next to the wave's Q and dO fragments and dQ.
+    struct OpS {
+        bf16x8 a[2][NDS];
+        float4 lo, hi;
+    };
+    struct OpD {
+        bf16x8 b[2][NDS];
+    };
+    auto load_s = [&](bool diag, int buf, int h) __attribute__((always_inline)) {
+        const float* nkrow = diag ? sm.kc[buf] : sm.kb[buf][w >> 1];
+        OpS r;
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+            const int rstep = 128 * (32 * h + 4 * t);
+#pragma unroll
+            for (int ds = 0; ds < NDS; ++ds)
+                r.a[t][ds] = *reinterpret_cast<const bf16x8*>(sm.k[buf] + roff[ds] + rstep);
+        }
+        r.lo = *reinterpret_cast<const float4*>(&nkrow[32 * h + 8 * g]);
+        r.hi = *reinterpret_cast<const float4*>(&nkrow[32 * h + 8 * g + 4]);
+        return r;
+    };
+    auto load_d = [&](int buf, int h) __attribute__((always_inline)) {
+        OpD r;
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+            const int rstep = 128 * (32 * h + 4 * t);
+#pragma unroll
+            for (int ds = 0; ds < NDS; ++ds)
+                r.b[t][ds] = *reinterpret_cast<const bf16x8*>(sm.v[buf] + roff[ds] + rstep);
+        }
+        return r;
+    };
+    auto phase_s = [&](auto mask_tag, const OpS& rs, SdP& x) __attribute__((always_inline)) {
         constexpr bool kMask = decltype(mask_tag)::value;
+        f32x4 init[2];
+#pragma unroll
+        for (int qt = 0; qt < 2; ++qt) {
+            if constexpr (kMask) {
+                float a = sdiag[qt];
+                asm volatile("" : "+v"(a));
+                init[qt] = f32x4{a, a, a, a};
+            } else {
+                init[qt] = sinit[qt];
+            }
+        }
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+            for (int ds = 0; ds < NDS; ++ds)
+#pragma unroll
+                for (int qt = 0; qt < 2; ++qt)
+                    x.s[t][qt] = mfma16(rs.a[t][ds], qf[qt][ds], ds == 0 ? init[qt] : x.s[t][qt]);
+    };
+    auto phase_d = [&](const OpD& rd, SdP& x) __attribute__((always_inline)) {
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+            for (int ds = 0; ds < NDS; ++ds)
+#pragma unroll
+                for (int qt = 0; qt < 2; ++qt)
+                    x.dp[t][qt] = mfma16(rd.b[t][ds], dof[qt][ds], ds == 0 ? dinit[qt] : x.dp[t][qt]);
+    };
+    auto step = [&](auto mask_tag, int n) __attribute__((always_inline)) {
         const bool act = n >= w_lo && n <= mw;
         const int qk0 = 32 * (w & 1) + r16 - 8 * g + (n == mw ? 0 : 4096);
-        OpC rc;
-        DsH y;
         if (act) {
-            rc = load_c(buf, 0);
-            SdP x = phase_a(mask_tag, ra);
-            y = phase_b(mask_tag, x, ra, 0, qk0);
-            ra = load_a(kMask, buf, 1);
-            phase_c(rc, y);
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                __builtin_amdgcn_sched_barrier(0);
+                SdP x;
+                const OpS rs = load_s(decltype(mask_tag)::value, buf, h);
+                phase_s(mask_tag, rs, x);
+                __builtin_amdgcn_sched_barrier(0);
+                {
+                    const OpD rd = load_d(buf, h);
+                    phase_d(rd, x);
+                }
+                __builtin_amdgcn_sched_barrier(0);
+                OpA ra;
+                ra.lo = rs.lo;
+                ra.hi = rs.hi;
+                const DsH y = phase_b(mask_tag, x, ra, h, qk0);
+                __builtin_amdgcn_sched_barrier(0);
+                const OpC rc = load_c(buf, h);
+                phase_c(rc, y);
+            }
             __builtin_amdgcn_sched_barrier(0);
-            rc = load_c(buf, 1);
-            x = phase_a(mask_tag, ra);
-            y = phase_b(mask_tag, x, ra, 1, qk0);
         }
         if (n < n_hi) put_kb(cnext, buf ^ 1);
         // tile n + 1 has landed and every wave's reads of tile n are complete
         wait_vmcnt0_lgkmcnt0();
         __syncthreads();
-        // the next tile's loads, spread over this tile's last MFMAs (see the dK/dV
-        // pass)
         const bool more = n + 1 < n_hi;
         if (more && tid < 16) cnext = *reinterpret_cast<const float4*>(cg + head + 64 * (n + 2) + 4 * tid);
-        if (n < n_hi) ra = load_a(n + 1 >= n_mask, buf ^ 1, 0);
-        if (act) phase_c_part(rc, y, 0);
         if (more) dma.issue(sm.k[buf], K + (head + (size_t)64 * (n + 2)) * D, w);
-        if (act) phase_c_part(rc, y, 1);
         if (more) dma.issue(sm.v[buf], V + (head + (size_t)64 * (n + 2)) * D, w);
         buf ^= 1;
     };
+    const int n_mask = max(n_lo, n_hi - 1);
     int n = n_lo;
     for (; n < n_mask; ++n) step(std::false_type{}, n);
     for (; n <= n_hi; ++n) step(std::true_type{}, n);
@@ -382,27 +437,40 @@ void dq_bf16_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// dK/dV pass: one workgroup per 128 keys (wave w's 32 keys lie in one pruning
-// column), looping over query blocks m = first column .. col_end[last column].
+// dK/dV pass: one workgroup per 128 keys, looping over query blocks
+// m = first key block .. col_end[last key block].  Each wave owns 32 keys that
+// lie in one pruning column.  At d = 64 four waves each take both 32-query
+// halves of every tile.  At d = 128 eight waves run, two per key group: each
+// takes one half of every tile, so that its dK and dV accumulators (32 keys x
+// 128 columns, twice) fit two waves per SIMD, and the pair's partial sums are
+// added through LDS at the end.
 // S = Q K^T and dP = dO V^T are formed queries x keys so that P and dS land in
 // the B-operand layout of dV^T = dO^T P and dK^T = Q^T dS.  The A-operand rows
 // (queries) are read in the order qrow = 32 h + 8 (r / 4) + 4 t + r % 4.
 // ---------------------------------------------------------------------------
 template <int D>
+struct DkvShape {
+    static constexpr int QSPLIT = D == 64 ? 1 : 2;    // waves sharing a key group
+    static constexpr int NW = 4 * QSPLIT;             // waves per workgroup
+    static constexpr bool kVinLds = D == 128;         // V rows from LDS (else registers)
+};
+
+template <int D>
 struct alignas(1024) DkvSmem {
     unsigned char q[2][128 * D];   // 64 x D bf16 tiles (see tile_off)
     unsigned char o[2][128 * D];   // dO
+    unsigned char k[2][128 * D];   // the workgroup's 128 keys (two tiles)
+    // d = 128: their values (the B operand of dP)
+    unsigned char v[DkvShape<D>::kVinLds ? 2 : 1][DkvShape<D>::kVinLds ? 128 * D : 16];
     float la[2][2][64];            // a_i / k',  a_i = (c_i - R) log2(e) - L_i, per key block
     float ll[2][64];               // -L_i / k' (diagonal tiles)
     float lc[2][64];               // c_i (diagonal tiles)
     float dl[2][64];               // -Delta'_i
     float kc[128];                 // c_j of the workgroup's keys (diagonal tiles)
-    // d = 64: the workgroup's 128 keys (two tiles), read as the B operand of S
-    unsigned char k[D == 64 ? 2 : 1][D == 64 ? 128 * D : 16];
 };
 
 template <int D>
-__global__ __launch_bounds__(kBwdThreads) __attribute__((amdgpu_waves_per_eu(D == 64 ? 3 : 1)))
+__global__ __launch_bounds__(64 * DkvShape<D>::NW) __attribute__((amdgpu_waves_per_eu(D == 64 ? 3 : 2)))
 void dkdv_bf16_kernel(
     const __bf16* __restrict__ Q, const __bf16* __restrict__ K, const __bf16* __restrict__ V,
     const __bf16* __restrict__ dO, const float* __restrict__ cg,
@@ -412,6 +480,8 @@ void dkdv_bf16_kernel(
     int nblocks, float kscale, float qscale) {
     constexpr int NDS = D / 32;
     constexpr int NDT = D / 16;
+    constexpr int QSPLIT = DkvShape<D>::QSPLIT, NW = DkvShape<D>::NW;
+    constexpr bool kVinLds = DkvShape<D>::kVinLds;
     __shared__ DkvSmem<D> sm;
 
     const int item = sched[xcd_logical_id(blockIdx.x, nblocks)];   // bh * nkb + key block
@@ -419,9 +489,12 @@ void dkdv_bf16_kernel(
     const int kb = item % nkb;
     const int tid = threadIdx.x, lane = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int kg = w & 3;                   // the wave's key group
+    const int qh = w >> 2;                  // its query half (d = 128)
+    const int wb = kg >> 1;                 // the key group's block in the workgroup
     const int g = lane >> 4, r16 = lane & 15;
     const int k0 = kb * kBwdRows;
-    const int wk0 = k0 + 32 * w;
+    const int wk0 = k0 + 32 * kg;
     const bool wave_on = wk0 < L;
     const int nw = wk0 / 64;
     const int n0 = k0 / 64;
@@ -435,21 +508,19 @@ void dkdv_bf16_kernel(
     // wave's block
     const float rb0 = cg[head + k0 + 63];
     const float rb1 = k0 + 64 < L ? cg[head + k0 + 127] : rb0;
-    const float rw = (w >> 1) ? rb1 : rb0;
+    const float rw = wb ? rb1 : rb0;
 
-    constexpr bool kKinLds = D == 64;
-    bf16x8 kf[2][NDS], vf[2][NDS];   // kf unused at d = 64 (K is in LDS)
-    float nk[2] = {0.f, 0.f};   // (R - c_j) log2(e) of the lane's keys
+    bf16x8 vf[2][kVinLds ? 1 : NDS];   // d = 64: the wave's V rows
+    float nk[2] = {0.f, 0.f};          // (R - c_j) log2(e) of the lane's keys
     if (tid < 128) sm.kc[tid] = k0 + tid < L ? cg[head + k0 + tid] : 0.f;
     if (wave_on) {
 #pragma unroll
         for (int kt = 0; kt < 2; ++kt) {
             const size_t row = head + wk0 + 16 * kt + r16;
+            if constexpr (!kVinLds) {
 #pragma unroll
-            for (int ds = 0; ds < NDS; ++ds) {
-                if constexpr (!kKinLds)
-                    kf[kt][ds] = *reinterpret_cast<const bf16x8*>(K + row * D + 32 * ds + 8 * g);
-                vf[kt][ds] = *reinterpret_cast<const bf16x8*>(V + row * D + 32 * ds + 8 * g);
+                for (int ds = 0; ds < NDS; ++ds)
+                    vf[kt][ds] = *reinterpret_cast<const bf16x8*>(V + row * D + 32 * ds + 8 * g);
             }
             nk[kt] = (rw - cg[row]) * kLog2e;
         }
@@ -457,7 +528,7 @@ void dkdv_bf16_kernel(
 
     // The small per-row loads go first and are combined only after the tile's
     // compute: vmcnt retires in order, so using them does not wait for the DMA.
-    TileDma<D, 4> dma;
+    TileDma<D, NW> dma;
     dma.init(w, lane);
     auto issue = [&](int m, int buf) __attribute__((always_inline)) {
         float3 r = make_float3(0.f, 0.f, 0.f);
@@ -494,19 +565,21 @@ void dkdv_bf16_kernel(
         }
     float csum[2] = {0.f, 0.f};
 
-    // Each query tile is taken in two halves of 32 queries, each in three
-    // phases: A forms S and dP (MFMA; query rows and the accumulator starts from
-    // LDS), B the softmax terms (VALU), C accumulates dV and dK (MFMA; query
-    // columns from LDS).  At d = 64 (three waves per SIMD, below) each phase reads
-    // its own operands.  At d = 128 (one wave per SIMD) every LDS operand is read
-    // one phase before it is used, so its latency passes under other work: the
-    // columns of a half during its phase A, the rows of the second half during
-    // the first half's phase C, and the rows of the next tile's first half during
-    // the second half's phase C, which runs after the barrier that publishes that
-    // tile.
-    struct OpA {
-        bf16x8 a[2][NDS], b[2][NDS];
-        f32x4 si[2], di[2];
+    // Each query half of 32 queries is taken in four phases: S (MFMA; query rows,
+    // the accumulator starts and the key rows from LDS), dP (dO rows from LDS, V
+    // from registers at d = 64 and from LDS at d = 128), the softmax terms (VALU),
+    // and dV, dK (MFMA; query columns from LDS).  No operand is held across a
+    // phase, and scheduling barriers keep the compiler from hoisting the next
+    // phase's LDS reads: the other waves on the SIMD (three at d = 64, two at
+    // d = 128) fill the wait, and the kernel stays within their register budget
+    // (168, resp. 256).
+    struct OpS {
+        bf16x8 a[2][NDS];
+        f32x4 si[2];
+    };
+    struct OpD {
+        bf16x8 b[2][NDS];
+        f32x4 di[2];
     };
     struct OpC {
         bf16x8 ao[NDT], aq[NDT];
@@ -518,122 +591,14 @@ void dkdv_bf16_kernel(
         bf16x8 pb[2], db[2];
     };
     // diag: the tile goes through the masking variant (S starts at -L_i / k')
-    auto load_a = [&](bool diag, int buf, int h) __attribute__((always_inline)) {
-        OpA r;
-        const unsigned char* qtile = sm.q[buf];
-        const unsigned char* otile = sm.o[buf];
-        const float* sirow = diag ? sm.ll[buf] : sm.la[buf][w >> 1];
+    auto load_s = [&](bool diag, int buf, int h) __attribute__((always_inline)) {
+        OpS r;
+        const float* sirow = diag ? sm.ll[buf] : sm.la[buf][wb];
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
             // rows 32 h + 4 t + (row of roff); the lane's accumulator rows are the
             // queries 32 h + 8 g + 4 t + u, whose a_i / k' and -Delta'_i start S
             // and dP, so the MFMAs leave the exponent's row term and dP - Delta'
-            r.si[t] = *reinterpret_cast<const f32x4*>(&sirow[32 * h + 8 * g + 4 * t]);
-            r.di[t] = *reinterpret_cast<const f32x4*>(&sm.dl[buf][32 * h + 8 * g + 4 * t]);
-            const int rstep = 128 * (32 * h + 4 * t);
-#pragma unroll
-            for (int ds = 0; ds < NDS; ++ds) {
-                r.a[t][ds] = *reinterpret_cast<const bf16x8*>(qtile + roff[ds] + rstep);
-                r.b[t][ds] = *reinterpret_cast<const bf16x8*>(otile + roff[ds] + rstep);
-            }
-        }
-        return r;
-    };
-    auto load_c = [&](int buf, int h) __attribute__((always_inline)) {
-        OpC r;
-#pragma unroll
-        for (int dt = 0; dt < NDT; ++dt) {
-            r.ao[dt] = tile_col8_at(sm.o[buf] + coff[dt] + 128 * 32 * h);
-            r.aq[dt] = tile_col8_at(sm.q[buf] + coff[dt] + 128 * 32 * h);
-        }
-        return r;
-    };
-    auto phase_a = [&](const OpA& ra) __attribute__((always_inline)) {
-        SdP x;
-#pragma unroll
-        for (int t = 0; t < 2; ++t)
-#pragma unroll
-            for (int ds = 0; ds < NDS; ++ds)
-#pragma unroll
-                for (int kt = 0; kt < 2; ++kt) {
-                    x.s[t][kt] = mfma16(ra.a[t][ds], kf[kt][ds], ds == 0 ? ra.si[t] : x.s[t][kt]);
-                    x.dp[t][kt] = mfma16(ra.b[t][ds], vf[kt][ds], ds == 0 ? ra.di[t] : x.dp[t][kt]);
-                }
-        return x;
-    };
-    // The lane's queries are 32 h + 8 g + j, j = 0..7 (j < 4 from subtile 0).
-    // kMask: the tile may be this wave's diagonal one, where key kloc is dropped
-    // for the queries before it.  The test is kq > 32 h + j with the lane's
-    // kq = kloc - 8 g, lowered out of reach on tiles that are not diagonal, so
-    // that the comparisons take immediate operands.  Such tiles form the decay
-    // c_i - c_j per entry (c_i from LDS).
-    auto phase_b = [&](auto mask_tag, const SdP& x, int buf, int h, int kq0) __attribute__((always_inline)) {
-        constexpr bool kMask = decltype(mask_tag)::value;
-        float ci[8], ck[2];
-        if constexpr (kMask) {
-            const float4 a = *reinterpret_cast<const float4*>(&sm.lc[buf][32 * h + 8 * g]);
-            const float4 b = *reinterpret_cast<const float4*>(&sm.lc[buf][32 * h + 8 * g + 4]);
-            ci[0] = a.x; ci[1] = a.y; ci[2] = a.z; ci[3] = a.w;
-            ci[4] = b.x; ci[5] = b.y; ci[6] = b.z; ci[7] = b.w;
-            ck[0] = sm.kc[32 * w + r16];
-            ck[1] = sm.kc[32 * w + 16 + r16];
-        }
-        PdS y;
-#pragma unroll
-        for (int kt = 0; kt < 2; ++kt) {
-            int kq = kq0 + 16 * kt;
-            if constexpr (kMask) asm volatile("" : "+v"(kq));
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                const int t = j >> 2, u = j & 3;
-                const float bias = kMask ? (ci[j] - ck[kt]) * kLog2e : nk[kt];
-                float p = fast_exp2(__builtin_fmaf(x.s[t][kt][u], kscale, bias));
-                if (kMask && kq > 32 * h + j) p = 0.f;
-                const float dsv = p * x.dp[t][kt][u];
-                csum[kt] += dsv;
-                y.pb[kt][j] = (__bf16)p;
-                y.db[kt][j] = (__bf16)dsv;
-            }
-        }
-        return y;
-    };
-    auto phase_c_part = [&](const OpC& rc, const PdS& y, int part) __attribute__((always_inline)) {
-#pragma unroll
-        for (int dt = part * NDT / 2; dt < (part + 1) * NDT / 2; ++dt)
-#pragma unroll
-            for (int kt = 0; kt < 2; ++kt) {
-                dv[kt][dt] = mfma16(rc.ao[dt], y.pb[kt], dv[kt][dt]);
-                dk[kt][dt] = mfma16(rc.aq[dt], y.db[kt], dk[kt][dt]);
-            }
-    };
-    // dV^T += dO^T P,  dK^T += Q^T dS over the half's 32 queries
-    auto phase_c = [&](const OpC& rc, const PdS& y) __attribute__((always_inline)) {
-#pragma unroll
-        for (int dt = 0; dt < NDT; ++dt)
-#pragma unroll
-            for (int kt = 0; kt < 2; ++kt) {
-                dv[kt][dt] = mfma16(rc.ao[dt], y.pb[kt], dv[kt][dt]);
-                dk[kt][dt] = mfma16(rc.aq[dt], y.db[kt], dk[kt][dt]);
-            }
-    };
-
-    if constexpr (kKinLds) {
-    // d = 64: three waves per SIMD.  No operand is held across a phase, phase A is
-    // split into S (query rows and K from LDS) and dP (dO rows, V in registers),
-    // and the keys' K rows come from LDS, so that the kernel fits 168 VGPRs.
-    struct OpS {
-        bf16x8 a[2][NDS];
-        f32x4 si[2];
-    };
-    struct OpD {
-        bf16x8 b[2][NDS];
-        f32x4 di[2];
-    };
-    auto load_s = [&](bool diag, int buf, int h) __attribute__((always_inline)) {
-        OpS r;
-        const float* sirow = diag ? sm.ll[buf] : sm.la[buf][w >> 1];
-#pragma unroll
-        for (int t = 0; t < 2; ++t) {
             r.si[t] = *reinterpret_cast<const f32x4*>(&sirow[32 * h + 8 * g + 4 * t]);
             const int rstep = 128 * (32 * h + 4 * t);
 #pragma unroll
@@ -654,14 +619,23 @@ void dkdv_bf16_kernel(
         }
         return r;
     };
-    // the wave's keys: rows 32 (w % 2) + 16 kt + (lane % 16) of K tile w / 2
+    auto load_c = [&](int buf, int h) __attribute__((always_inline)) {
+        OpC r;
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt) {
+            r.ao[dt] = tile_col8_at(sm.o[buf] + coff[dt] + 128 * 32 * h);
+            r.aq[dt] = tile_col8_at(sm.q[buf] + coff[dt] + 128 * 32 * h);
+        }
+        return r;
+    };
+    // the wave's keys: rows 32 (kg % 2) + 16 kt + (lane % 16) of K tile kg / 2
+    const int krow = 32 * (kg & 1) + r16;
     auto phase_s = [&](const OpS& rs, SdP& x) __attribute__((always_inline)) {
         bf16x8 kr[2][NDS];
 #pragma unroll
         for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-            for (int ds = 0; ds < NDS; ++ds)
-                kr[kt][ds] = tile_row8(sm.k[w >> 1], 32 * (w & 1) + 16 * kt + r16, 32 * ds + 8 * g);
+            for (int ds = 0; ds < NDS; ++ds) kr[kt][ds] = tile_row8(sm.k[wb], krow + 16 * kt, 32 * ds + 8 * g);
 #pragma unroll
         for (int t = 0; t < 2; ++t)
 #pragma unroll
@@ -671,19 +645,82 @@ void dkdv_bf16_kernel(
                     x.s[t][kt] = mfma16(rs.a[t][ds], kr[kt][ds], ds == 0 ? rs.si[t] : x.s[t][kt]);
     };
     auto phase_d = [&](const OpD& rd, SdP& x) __attribute__((always_inline)) {
+        if constexpr (kVinLds) {
 #pragma unroll
-        for (int t = 0; t < 2; ++t)
+            for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-            for (int ds = 0; ds < NDS; ++ds)
+                for (int ds = 0; ds < NDS; ++ds) {
+                    const bf16x8 vr = tile_row8(sm.v[wb], krow + 16 * kt, 32 * ds + 8 * g);
 #pragma unroll
-                for (int kt = 0; kt < 2; ++kt)
-                    x.dp[t][kt] = mfma16(rd.b[t][ds], vf[kt][ds], ds == 0 ? rd.di[t] : x.dp[t][kt]);
+                    for (int t = 0; t < 2; ++t)
+                        x.dp[t][kt] = mfma16(rd.b[t][ds], vr, ds == 0 ? rd.di[t] : x.dp[t][kt]);
+                }
+        } else {
+#pragma unroll
+            for (int t = 0; t < 2; ++t)
+#pragma unroll
+                for (int ds = 0; ds < NDS; ++ds)
+#pragma unroll
+                    for (int kt = 0; kt < 2; ++kt)
+                        x.dp[t][kt] = mfma16(rd.b[t][ds], vf[kt][ds], ds == 0 ? rd.di[t] : x.dp[t][kt]);
+        }
+    };
+    // The lane's queries are 32 h + 8 g + j, j = 0..7 (j < 4 from subtile 0).
+    // kMask: the tile may be this wave's diagonal one, where key kloc is dropped
+    // for the queries before it.  The test is kq > 32 h + j with the lane's
+    // kq = kloc - 8 g, lowered out of reach on tiles that are not diagonal, so
+    // that the comparisons take immediate operands.  Such tiles form the decay
+    // c_i - c_j per entry (c_i from LDS).
+    auto phase_b = [&](auto mask_tag, const SdP& x, int buf, int h, int kq0) __attribute__((always_inline)) {
+        constexpr bool kMask = decltype(mask_tag)::value;
+        float ci[8], ck[2];
+        if constexpr (kMask) {
+            const float4 a = *reinterpret_cast<const float4*>(&sm.lc[buf][32 * h + 8 * g]);
+            const float4 b = *reinterpret_cast<const float4*>(&sm.lc[buf][32 * h + 8 * g + 4]);
+            ci[0] = a.x; ci[1] = a.y; ci[2] = a.z; ci[3] = a.w;
+            ci[4] = b.x; ci[5] = b.y; ci[6] = b.z; ci[7] = b.w;
+            ck[0] = sm.kc[32 * kg + r16];
+            ck[1] = sm.kc[32 * kg + 16 + r16];
+        }
+        PdS y;
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt) {
+            int kq = kq0 + 16 * kt;
+            if constexpr (kMask) asm volatile("" : "+v"(kq));
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const int t = j >> 2, u = j & 3;
+                const float bias = kMask ? (ci[j] - ck[kt]) * kLog2e : nk[kt];
+                float p = fast_exp2(__builtin_fmaf(x.s[t][kt][u], kscale, bias));
+                if (kMask && kq > 32 * h + j) p = 0.f;
+                const float dsv = p * x.dp[t][kt][u];
+                csum[kt] += dsv;
+                y.pb[kt][j] = (__bf16)p;
+                y.db[kt][j] = (__bf16)dsv;
+            }
+        }
+        return y;
+    };
+    // dV^T += dO^T P,  dK^T += Q^T dS over the half's 32 queries
+    auto phase_c = [&](const OpC& rc, const PdS& y) __attribute__((always_inline)) {
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+            for (int kt = 0; kt < 2; ++kt) {
+                dv[kt][dt] = mfma16(rc.ao[dt], y.pb[kt], dv[kt][dt]);
+                dk[kt][dt] = mfma16(rc.aq[dt], y.db[kt], dk[kt][dt]);
+            }
     };
 
-    // the workgroup's K tiles (when only 64 keys are left, waves 2-3 hold none)
+    // The workgroup's K (and at d = 128 V) tiles; when only 64 keys are left, the
+    // second block's waves hold none
     dma.issue(sm.k[0], K + (head + k0) * D, w);
     if (k0 + 64 < L) dma.issue(sm.k[1], K + (head + k0 + 64) * D, w);
-    // tile m_lo in LDS and published (with K); tile m_lo + 1 on its way
+    if constexpr (kVinLds) {
+        dma.issue(sm.v[0], V + (head + k0) * D, w);
+        if (k0 + 64 < L) dma.issue(sm.v[1], V + (head + k0 + 64) * D, w);
+    }
+    // tile m_lo in LDS and published; tile m_lo + 1 on its way
     put_rows(issue(m_lo, 0), 0);
     wait_vmcnt0();
     __syncthreads();
@@ -692,12 +729,11 @@ void dkdv_bf16_kernel(
     int buf = 0;
     auto step = [&](auto mask_tag, int m) __attribute__((always_inline)) {
         const bool act = m >= nw && m <= w_hi;
-        const int kq0 = 32 * (w & 1) + r16 - 8 * g - (m == nw ? 0 : 4096);
+        const int kq0 = 32 * (kg & 1) + r16 - 8 * g - (m == nw ? 0 : 4096);
         if (act) {
 #pragma unroll
-            for (int h = 0; h < 2; ++h) {
-                // (scheduling barriers keep each phase's LDS reads from being
-                // hoisted into the phase before, which would not fit 168 VGPRs)
+            for (int hh = 0; hh < 2 / QSPLIT; ++hh) {
+                const int h = QSPLIT == 1 ? hh : qh;
                 __builtin_amdgcn_sched_barrier(0);
                 SdP x;
                 {
@@ -730,70 +766,52 @@ void dkdv_bf16_kernel(
         if (more) dma.issue(sm.o[buf], dO + (head + (size_t)64 * (m + 2)) * D, w);
         buf ^= 1;
     };
+    // The first block's waves meet their diagonal tile at m_lo, the second
+    // block's at m_lo + 1; those two tiles go through the masking variant.
     const int m_diag = min(m_lo + 1, m_hi);
     int m = m_lo;
     for (; m <= m_diag; ++m) step(std::true_type{}, m);
     for (; m <= m_hi; ++m) step(std::false_type{}, m);
-    } else {
-    // tile m_lo in LDS and published; tile m_lo + 1 on its way
-    put_rows(issue(m_lo, 0), 0);
-    wait_vmcnt0();
-    __syncthreads();
-    float3 rnext = make_float3(0.f, 0.f, 0.f);
-    if (m_lo < m_hi) rnext = issue(m_lo + 1, 1);
-    // One query tile.  Waves 0-1 meet their diagonal tile at m_lo, waves 2-3 at
-    // m_lo + 1; those two tiles go through the masking variant.
-    const int m_diag = min(m_lo + 1, m_hi);
-    // (the rows are read whether or not this wave takes the tile, so that no
-    // path keeps an older set of them live through the loop)
-    OpA ra = load_a(true, 0, 0);
-    int buf = 0;
-    auto step = [&](auto mask_tag, int m) __attribute__((always_inline)) {
-        constexpr bool kMask = decltype(mask_tag)::value;
-        const bool act = m >= nw && m <= w_hi;
-        const int kq0 = 32 * (w & 1) + r16 - 8 * g - (m == nw ? 0 : 4096);
-        OpC rc;
-        PdS y;
-        if (act) {
-            // first half
-            rc = load_c(buf, 0);
-            SdP x = phase_a(ra);
-            y = phase_b(mask_tag, x, buf, 0, kq0);
-            ra = load_a(kMask, buf, 1);
-            phase_c(rc, y);
-            // (not merged with the second half's phase A: both hold four operand
-            // sets and would not fit the registers of two waves per SIMD)
-            __builtin_amdgcn_sched_barrier(0);
-            // second half up to its softmax terms
-            rc = load_c(buf, 1);
-            x = phase_a(ra);
-            y = phase_b(mask_tag, x, buf, 1, kq0);
+
+    if constexpr (QSPLIT == 2) {
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt) {
+            csum[kt] += __shfl_xor(csum[kt], 16);
+            csum[kt] += __shfl_xor(csum[kt], 32);
         }
-        if (m < m_hi) put_rows(rnext, buf ^ 1);
-        // tile m + 1 has landed and every wave's reads of tile m are complete
-        wait_vmcnt0_lgkmcnt0();
+        // The second half's waves hand their partial sums to the first half's
+        // through LDS, whose tiles are no longer read (the last step ended with
+        // a barrier): dK in the Q and dO tiles, dV in the K and V tiles, lane-major
+        // so that the 16-byte accesses do not conflict.
+        static_assert(sizeof(sm.q) + sizeof(sm.o) >= 4 * 2 * NDT * 64 * sizeof(f32x4), "dK staging");
+        static_assert(sizeof(sm.k) + sizeof(sm.v) >= 4 * 2 * NDT * 64 * sizeof(f32x4), "dV staging");
+        f32x4* sdk = reinterpret_cast<f32x4*>(&sm.q[0][0]);
+        f32x4* sdv = reinterpret_cast<f32x4*>(&sm.k[0][0]);
+        if (qh == 1) {
+#pragma unroll
+            for (int kt = 0; kt < 2; ++kt) {
+#pragma unroll
+                for (int dt = 0; dt < NDT; ++dt) {
+                    const int e = ((kg * 2 + kt) * NDT + dt) * 64 + lane;
+                    sdk[e] = dk[kt][dt];
+                    sdv[e] = dv[kt][dt];
+                }
+                if (g == 0) sm.kc[32 * kg + 16 * kt + r16] = csum[kt];
+            }
+        }
         __syncthreads();
-        // The next tile's loads are spread over this tile's last MFMAs: issued in
-        // one clump right after the barrier, the four waves' DMA instructions
-        // queue for the CU's address unit and stall the waves' issue.
-        const bool more = m + 1 < m_hi;
-        if (more && tid < 64) {
-            const size_t row = head + 64 * (m + 2) + tid;
-            rnext = make_float3(cg[row], lse2[row], dsum[row]);
+        if (qh == 1) return;
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt) {
+#pragma unroll
+            for (int dt = 0; dt < NDT; ++dt) {
+                const int e = ((kg * 2 + kt) * NDT + dt) * 64 + lane;
+                dk[kt][dt] += sdk[e];
+                dv[kt][dt] += sdv[e];
+            }
+            csum[kt] += sm.kc[32 * kg + 16 * kt + r16];
         }
-        if (m < m_hi) ra = load_a(m + 1 <= m_diag, buf ^ 1, 0);
-        if (act) phase_c_part(rc, y, 0);
-        if (more) dma.issue(sm.q[buf], Q + (head + (size_t)64 * (m + 2)) * D, w);
-        if (act) phase_c_part(rc, y, 1);
-        if (more) dma.issue(sm.o[buf], dO + (head + (size_t)64 * (m + 2)) * D, w);
-        buf ^= 1;
-    };
-    int m = m_lo;
-    for (; m <= m_diag; ++m) step(std::true_type{}, m);
-    for (; m <= m_hi; ++m) step(std::false_type{}, m);
-
     }
-
     if (!wave_on) return;
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt) {
@@ -810,8 +828,10 @@ void dkdv_bf16_kernel(
             *reinterpret_cast<bf16x4*>(dV + off) = bb;
         }
         float c = csum[kt];
-        c += __shfl_xor(c, 16);
-        c += __shfl_xor(c, 32);
+        if constexpr (QSPLIT == 1) {
+            c += __shfl_xor(c, 16);
+            c += __shfl_xor(c, 32);
+        }
         if (g == 0) colsum[head + key] = c;
     }
 }
@@ -845,13 +865,13 @@ hipError_t launch_dkdv_bf16(const BwdArgs& a, hipStream_t s) {
     const int nkb = (a.L + kBwdRows - 1) / kBwdRows;
     const int nblocks = BH * nkb;
     if (a.d == 64)
-        hipLaunchKernelGGL(dkdv_bf16_kernel<64>, dim3(nblocks), dim3(kBwdThreads), 0, s,
+        hipLaunchKernelGGL(dkdv_bf16_kernel<64>, dim3(nblocks), dim3(64 * DkvShape<64>::NW), 0, s,
                            (const __bf16*)a.Q, (const __bf16*)a.K, (const __bf16*)a.V,
                            (const __bf16*)a.dO, a.c, a.col_end, a.lse2, a.dsum,
                            (__bf16*)a.dK, (__bf16*)a.dV, a.colsum, a.sched_k, a.L, M, nkb,
                            nblocks, kscale, qscale);
     else
-        hipLaunchKernelGGL(dkdv_bf16_kernel<128>, dim3(nblocks), dim3(kBwdThreads), 0, s,
+        hipLaunchKernelGGL(dkdv_bf16_kernel<128>, dim3(nblocks), dim3(64 * DkvShape<128>::NW), 0, s,
                            (const __bf16*)a.Q, (const __bf16*)a.K, (const __bf16*)a.V,
                            (const __bf16*)a.dO, a.c, a.col_end, a.lse2, a.dsum,
                            (__bf16*)a.dK, (__bf16*)a.dV, a.colsum, a.sched_k, a.L, M, nkb,
