@@ -202,3 +202,36 @@ def test_decode_at_the_bench_shape_sampled():
         for t, o, lse, _ in steps:
             o_ref, lse_ref, _ = orc.decode_row(q[t], k, v, c_ref[b, h], t, delta)
             assert float(np.max(np.abs(o[b, h] - o_ref))) <= 2e-2 and abs(lse[b, h] - lse_ref) <= 1e-3
+
+
+def test_decode_long_ring_sampled():
+    """A ring of 66048 positions after a 66000-token prompt: each step launches
+    258 key chunks per head, more than 256, so their partial sums go through the
+    1024-thread variant of the merge kernel.  Three steps, every head's pointer
+    and output against the oracle."""
+    w = workloads.custom("declong", 1, 4, 66003, 64, "bf16", 5, qk_norm=True, mu=(1.0, 3.0, 6.0, 9.0))
+    print(f"case: decode long ring {w.describe()}", flush=True)
+    x = workloads.generate(w, with_grad=False)
+    g = to_gpu(x)
+    L0, C, L_max = 66000, 66048, 131072
+    dec = acp.Decoder(w.B, w.H, C, w.d).init(g["k"][:, :, :L0].contiguous(),
+                                              g["v"][:, :, :L0].contiguous(),
+                                              g["log_f"][:, :, :L0].contiguous(),
+                                              g["gamma_q"], g["gamma_k"], EPS, L_max)
+    steps = []
+    for t in range(L0, L0 + 3):
+        o, lse = dec.step(_token(g, "q", t), _token(g, "k", t), _token(g, "v", t),
+                          _token(g, "log_f", t))
+        steps.append((t, o.double().cpu().numpy(), lse.double().cpu().numpy(),
+                      dec.current_pointer().cpu().numpy()))
+    assert dec.views()["flags"].cpu().numpy().max() == 0
+    c_ref = orc.cumsum_log_gates(x["log_f"].numpy())
+    for h in range(w.H):
+        q, k, v, _, _ = head_inputs(x, 0, h)
+        U = orc.logit_bound_qknorm(float(x["gamma_q"][h]), float(x["gamma_k"][h]), w.d)
+        delta = orc.threshold(U, L_max, EPS)
+        for t, o, lse, ptr in steps:
+            assert int(ptr[0, h]) == orc.decode_pointer(c_ref[0, h], t, delta), (h, t)
+            o_ref, lse_ref, _ = orc.decode_row(q[t], k, v, c_ref[0, h], t, delta)
+            assert float(np.max(np.abs(o[0, h] - o_ref))) <= 2e-2, (h, t)
+            assert abs(lse[0, h] - lse_ref) <= 1e-3, (h, t)
