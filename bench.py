@@ -38,6 +38,7 @@ PAPER_CONTEXT = {
                "L = 4k/8k/16k",
 }
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+NOMINAL_CLOCK_GHZ = 2.4     # the shader clock the dense peak is quoted at
 PEAK_HBM_GBS = 8000.0
 
 
@@ -61,29 +62,45 @@ def roofline(w, r):
     pk = r["per_kernel_ms"]
     dom = max(("fwd", "dq", "dkdv"), key=lambda k: pk[k])
     achieved = fl[dom] / (pk[dom] * 1e-3) / 1e12
-    return {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 2),
-            "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-            "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-            "traffic": measured_traffic(dom, w.name)}
+    out = {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 2),
+           "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+           "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+           "traffic": measured_traffic(dom, w.name)}
+    # The same rate against the shader clock the kernel sustains under this load
+    # (from the counter profile; the nominal peak assumes 2.4 GHz), or None.
+    clk = _profile_value("clock", dom, w.name)
+    out["clock_ghz"] = clk
+    out["frac_at_clock"] = (round(achieved / (PEAK_BF16_TFLOPS * clk / NOMINAL_CLOCK_GHZ), 4)
+                            if clk else None)
+    return out
+
+
+def _profile_value(kind: str, kernel: str, workload: str):
+    """A machine-read line `kind kernel workload value src:digest` of the committed
+    rocprofv3 summaries, as a number, or None when none exists or the kernel's
+    source changed since the counters were taken."""
+    import glob
+    import hashlib
+    for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*.md"))):
+        for line in open(path):
+            f = line.split()
+            if len(f) == 5 and f[0] == kind and f[1] == kernel and f[2] == workload:
+                src, digest = f[4].split(":")
+                src_path = os.path.join(ROOT, "paper_2504_06949_amd", "csrc", src)
+                if not os.path.exists(src_path):
+                    return None
+                now = hashlib.sha1(open(src_path, "rb").read()).hexdigest()[:12]
+                if now != digest:
+                    return None
+                return int(f[3]) if kind == "traffic" else float(f[3])
+    return None
 
 
 def measured_traffic(kernel: str, workload: str):
     """HBM bytes per launch of `kernel` on `workload` from the committed rocprofv3
     summaries (FETCH_SIZE + WRITE_SIZE, copy-calibrated), or None when none exists
     or the kernel's source changed since the counters were taken."""
-    import glob
-    import hashlib
-    for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*.md"))):
-        for line in open(path):
-            f = line.split()
-            if len(f) == 5 and f[0] == "traffic" and f[1] == kernel and f[2] == workload:
-                src, digest = f[4].split(":")
-                src_path = os.path.join(ROOT, "paper_2504_06949_amd", "csrc", src)
-                if not os.path.exists(src_path):
-                    return None
-                now = hashlib.sha1(open(src_path, "rb").read()).hexdigest()[:12]
-                return int(f[3]) if now == digest else None
-    return None
+    return _profile_value("traffic", kernel, workload)
 
 
 def _stage1_ms(pk: dict) -> float:

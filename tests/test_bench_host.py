@@ -66,3 +66,26 @@ def test_roofline_takes_the_longest_attention_kernel():
     want = kept * 8 * 64 * 64 * 64 / 3e-8 / 1e12
     assert got["achieved"] == pytest.approx(want, rel=1e-3)
     assert got["frac"] == pytest.approx(want / bench.PEAK_BF16_TFLOPS, rel=1e-3)
+
+
+def test_roofline_against_the_measured_clock(tmp_path, monkeypatch):
+    """With a clock line for the dominant kernel, the same rate is also reported
+    against the peak scaled to that clock; without one (or after the kernel's
+    source changed) both fields are None."""
+    src_dir = tmp_path / "paper_2504_06949_amd" / "csrc"
+    src_dir.mkdir(parents=True)
+    (tmp_path / "profiles").mkdir()
+    src = src_dir / "fox_bwd_mfma.hip"
+    src.write_bytes(b"// kernel v1\n")
+    digest = hashlib.sha1(src.read_bytes()).hexdigest()[:12]
+    (tmp_path / "profiles" / "c.md").write_text(
+        "    clock dkdv acct 1.800 fox_bwd_mfma.hip:%s\n" % digest)
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    w = workloads.custom("acct", 2, 3, 256, 64, "bf16", 1)
+    r = {"kept": 17, "per_kernel_ms": {"fwd": 1e-5, "dq": 2e-5, "dkdv": 3e-5}}
+    got = bench.roofline(w, r)
+    assert got["clock_ghz"] == pytest.approx(1.8)
+    assert got["frac_at_clock"] == pytest.approx(got["frac"] * 2.4 / 1.8, rel=1e-3)
+    src.write_bytes(b"// kernel v2\n")
+    got = bench.roofline(w, r)
+    assert got["clock_ghz"] is None and got["frac_at_clock"] is None
