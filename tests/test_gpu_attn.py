@@ -90,7 +90,10 @@ def test_tiny_f32_pruning_changes_output_by_at_most_2eps():
 @pytest.mark.parametrize("B,H,L,d,mu,seed", [
     (2, 3, 320, 64, (0.5, 2.0, 8.0), 21),     # ragged: L % 128 == 64
     (1, 2, 384, 128, (1.0, 6.0), 22),
+    (2, 2, 320, 128, (0.5, 3.0), 27),         # d = 128 ragged: the last workgroup's second
+                                              # block of keys is past L (its waves idle)
     (1, 2, 64, 64, (1.0, 3.0), 23),           # a single block
+    (1, 3, 64, 128, (0.0, 1.0, 6.0), 28),     # a single block at d = 128
     (1, 1, 1024, 64, (0.0,), 24),             # mu = 0: strongly local
 ])
 def test_small_bf16_full(B, H, L, d, mu, seed):
