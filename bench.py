@@ -75,6 +75,18 @@ def roofline(w, r):
     return out
 
 
+def frac_at_step_clock(w, pk: dict, executed_tflops: float):
+    """The step's executed MFMA rate against the peak at the clock its attention
+    kernels sustain: their profiled clocks weighted by their share of the step's
+    attention time; None unless all three have a current clock line."""
+    ks = ("fwd", "dq", "dkdv")
+    clocks = [_profile_value("clock", k, w.name) for k in ks]
+    if any(c is None for c in clocks) or sum(pk[k] for k in ks) <= 0:
+        return None
+    clk = sum(pk[k] * c for k, c in zip(ks, clocks)) / sum(pk[k] for k in ks)
+    return round(executed_tflops / (PEAK_BF16_TFLOPS * clk / NOMINAL_CLOCK_GHZ), 4)
+
+
 def _profile_value(kind: str, kernel: str, workload: str):
     """A machine-read line `kind kernel workload value src:digest` of the committed
     rocprofv3 summaries, as a number, or None when none exists or the kernel's
@@ -455,6 +467,8 @@ def main():
         "executed_tflops": round(fl["executed"] / (res["ms"] * 1e-3) / 1e12, 2),
         "mfma_frac_executed": round(fl["executed"] / (res["ms"] * 1e-3) / 1e12
                                     / PEAK_BF16_TFLOPS, 4),
+        "mfma_frac_executed_at_clock": frac_at_step_clock(
+            w, pk, fl["executed"] / (res["ms"] * 1e-3) / 1e12),
         "ms_unpruned": None if args.skip_unpruned else round(res["ms_dense"], 4),
         "speedup_vs_unpruned": None if args.skip_unpruned else round(res["ms_dense"] / res["ms"], 3),
         "per_kernel_ms": {k: round(v, 4) for k, v in pk.items()},
@@ -475,6 +489,7 @@ def main():
                            "effective_tflops": round(f["effective"] / (r["ms"] * 1e-3) / 1e12, 1),
                            "executed_tflops": round(ex, 1),
                            "mfma_frac_executed": round(ex / PEAK_BF16_TFLOPS, 4),
+                           "mfma_frac_executed_at_clock": frac_at_step_clock(r["w"], r["per_kernel_ms"], ex),
                            "pruned_fraction": round(1 - r["kept"] / r["causal"], 4),
                            "boundary_share": round(_stage1_ms(r["per_kernel_ms"]) / r["ms"], 4),
                            "roofline": roofline(r["w"], r),

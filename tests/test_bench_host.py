@@ -89,3 +89,28 @@ def test_roofline_against_the_measured_clock(tmp_path, monkeypatch):
     src.write_bytes(b"// kernel v2\n")
     got = bench.roofline(w, r)
     assert got["clock_ghz"] is None and got["frac_at_clock"] is None
+
+
+def test_step_fraction_at_the_kernels_clock(tmp_path, monkeypatch):
+    """The step's executed rate is scaled by the attention kernels' clocks weighted
+    by their times; a missing clock line gives None."""
+    src_dir = tmp_path / "paper_2504_06949_amd" / "csrc"
+    src_dir.mkdir(parents=True)
+    (tmp_path / "profiles").mkdir()
+    lines = []
+    for name in ("fox_fwd.hip", "fox_bwd_mfma.hip"):
+        (src_dir / name).write_bytes(b"// " + name.encode() + b"\n")
+    dg = {n: hashlib.sha1((src_dir / n).read_bytes()).hexdigest()[:12]
+          for n in ("fox_fwd.hip", "fox_bwd_mfma.hip")}
+    lines.append("    clock fwd acct 2.000 fox_fwd.hip:%s" % dg["fox_fwd.hip"])
+    lines.append("    clock dq acct 1.800 fox_bwd_mfma.hip:%s" % dg["fox_bwd_mfma.hip"])
+    (tmp_path / "profiles" / "c.md").write_text("\n".join(lines) + "\n")
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    w = workloads.custom("acct", 2, 3, 256, 64, "bf16", 1)
+    pk = {"fwd": 1.0, "dq": 1.0, "dkdv": 2.0}
+    assert bench.frac_at_step_clock(w, pk, 1000.0) is None          # no dK/dV clock yet
+    with open(tmp_path / "profiles" / "c.md", "a") as f:
+        f.write("    clock dkdv acct 1.600 fox_bwd_mfma.hip:%s\n" % dg["fox_bwd_mfma.hip"])
+    clk = (1.0 * 2.0 + 1.0 * 1.8 + 2.0 * 1.6) / 4.0
+    assert bench.frac_at_step_clock(w, pk, 1000.0) == pytest.approx(
+        1000.0 / (bench.PEAK_BF16_TFLOPS * clk / 2.4), rel=1e-3)
