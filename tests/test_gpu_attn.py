@@ -102,6 +102,34 @@ def test_small_bf16_full(B, H, L, d, mu, seed):
     _full_parity(w)
 
 
+def _random_cases(n=8, seed=2025):
+    """Seeded random shapes: ragged lengths (any multiple of 64 up to 768), odd head
+    counts, both head dims, per-head gate means from strong to no forgetting, and
+    pruning from light to heavy (eps up to 0.5)."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for i in range(n):
+        B = int(rng.integers(1, 3))
+        H = int(rng.integers(1, 6 if B == 1 else 4))
+        L = 64 * int(rng.integers(1, 13))
+        d = int(rng.choice([64, 128]))
+        mu = tuple(float(m) for m in rng.uniform(-1.0, 12.0, size=H))
+        eps = float(rng.choice([math.exp(-10), math.exp(-3), 0.5]))
+        out.append((B, H, L, d, mu, eps, 100 + i))
+    return out
+
+
+_RANDOM = _random_cases()
+
+
+@pytest.mark.parametrize("B,H,L,d,mu,eps,seed", _RANDOM,
+                         ids=[f"B{c[0]}H{c[1]}L{c[2]}d{c[3]}eps{c[5]:.3g}" for c in _RANDOM])
+def test_random_shapes_full(B, H, L, d, mu, eps, seed):
+    w = workloads.custom(f"rand{seed}", B, H, L, d, "bf16", seed, mu=mu)
+    print(f"case: fwd/bwd {w.describe()} eps={eps:g}", flush=True)
+    _full_parity(w, eps=eps)
+
+
 def test_small_f32_d128_full():
     w = workloads.custom("f32d128", 1, 2, 192, 128, "f32", 25, mu=(0.5, 4.0))
     print(f"case: fwd/bwd {w.describe()}", flush=True)
