@@ -410,7 +410,7 @@ __global__ __launch_bounds__(kDecChunk) void decode_step_kernel(
 // of 256 threads, or 1024 when a long context leaves more than 256 splits (up to
 // 512).  Thread i takes the (max, sum) of split i, and dim i mod D of splits
 // i / D, i / D + THREADS / D, ..., whose loads it issues kBatch at a time before
-// it waits for any of them.
+// it waits for any of them (the first batch together with the (max, sum) loads).
 template <typename T, int D, int THREADS>
 __global__ __launch_bounds__(THREADS) void decode_combine_kernel(
     int nsplit, const float* __restrict__ part, T* __restrict__ O, float* __restrict__ lse) {
@@ -426,6 +426,12 @@ __global__ __launch_bounds__(THREADS) void decode_combine_kernel(
     const int dim = tid % D, grp = tid / D;
 
     const int sm = min(tid, nsplit - 1);
+    // The first batch of partial outputs is requested with the (max, sum) pairs:
+    // it does not depend on them (a split without a kept key is selected away
+    // below), so small merges make one round trip to memory instead of two.
+    float pv0[kBatch];
+#pragma unroll
+    for (int r = 0; r < kBatch; ++r) pv0[r] = po[(size_t)min(grp + kGroups * r, nsplit - 1) * D + dim];
     float ms = pml[2 * sm], ls = pml[2 * sm + 1];
     if (tid >= nsplit) {
         ms = -INFINITY;
@@ -450,7 +456,15 @@ __global__ __launch_bounds__(THREADS) void decode_combine_kernel(
     for (int w = 1; w < kWaves; ++w) L += s_l[w];
     // splits without a kept key (weight 0) hold no O: selected away, not multiplied
     float o = 0.f;
-    for (int s0 = grp; s0 < nsplit; s0 += kGroups * kBatch) {
+#pragma unroll
+    for (int r = 0; r < kBatch; ++r) {
+        const int s2 = grp + kGroups * r;
+        if (s2 < nsplit) {
+            const float w = w_s[s2];
+            o += w != 0.f ? w * pv0[r] : 0.f;
+        }
+    }
+    for (int s0 = grp + kGroups * kBatch; s0 < nsplit; s0 += kGroups * kBatch) {
         float pv[kBatch];
 #pragma unroll
         for (int r = 0; r < kBatch; ++r)
