@@ -48,8 +48,9 @@ def test_boundary_qknorm_bit_exact():
     assert pruned > 0
 
 
-def test_forward_backward_qknorm_matches_oracle():
-    w = workloads.custom("qk", 1, 3, 320, 64, "bf16", 32, mu=(1.0, 3.0, 8.0), qk_norm=True)
+@pytest.mark.parametrize("d", [64, 128])
+def test_forward_backward_qknorm_matches_oracle(d):
+    w = workloads.custom("qk", 1, 3, 320, d, "bf16", 32, mu=(1.0, 3.0, 8.0), qk_norm=True)
     print(f"case: fwd/bwd qknorm {w.describe()}", flush=True)
     x = workloads.generate(w)
     g = to_gpu(x)
@@ -67,8 +68,14 @@ def test_forward_backward_qknorm_matches_oracle():
         q, k, v, do, lf = head_inputs(x, 0, h)
         ref = orc.run_head(q, k, v, lf, EPS, do=do, U=_u(x, h, w.d))
         errs = {n: float(np.max(np.abs(f64(got[n][0, h]) - ref[n]))) for n in got}
-        print(f"  head {h}: kept {ref['kept']} of {orc.causal_tiles(w.M)}, errors {errs}", flush=True)
-        assert max(errs.values()) <= 2e-2, (h, errs)
+        # bf16 outputs carry a relative rounding of 2^-9: where O or a gradient
+        # exceeds 1 in size (dQ of QK-normed rows at d = 128) its bound is relative
+        # to it, as in the attention tests; LSE and dlog f keep the absolute bound
+        bound = {n: 2e-2 * (max(1.0, float(np.max(np.abs(ref[n])))) if n in ("o", "dq", "dk", "dv")
+                            else 1.0) for n in got}
+        print(f"  head {h}: kept {ref['kept']} of {orc.causal_tiles(w.M)}, errors {errs}, "
+              f"bounds {bound}", flush=True)
+        assert all(errs[n] <= bound[n] for n in got), (h, errs, bound)
 
 
 def test_qknorm_bad_scale_is_flagged():
