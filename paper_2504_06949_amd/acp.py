@@ -477,6 +477,32 @@ def backward(q, k, v, o, do, ws: torch.Tensor, out=None):
     return dq, dk, dv, dlf
 
 
+class _FoxAttention(torch.autograd.Function):
+    """Autograd node over forward() and backward(): the forward's workspace (its
+    plan, and the state the backward reads) is saved with Q, K, V and O."""
+
+    @staticmethod
+    def forward(ctx, q, k, v, log_f, eps):
+        q, k, v, log_f = (t.contiguous() for t in (q, k, v, log_f))
+        o, lse, ws = forward(q, k, v, log_f, eps)
+        ctx.save_for_backward(q, k, v, o, ws)
+        ctx.mark_non_differentiable(lse)
+        return o, lse
+
+    @staticmethod
+    def backward(ctx, do, _dlse):
+        q, k, v, o, ws = ctx.saved_tensors
+        dq, dk, dv, dlf = backward(q, k, v, o, do.to(q.dtype).contiguous(), ws)
+        return dq, dk, dv, dlf, None
+
+
+def fox_attention(q, k, v, log_f, eps: float):
+    """Differentiable FoX attention with ACP: (O, lse) of forward(), with gradients
+    for Q, K, V and log f from backward() when autograd asks for them.  lse carries
+    no gradient.  Inputs need not be contiguous (they are copied if not)."""
+    return _FoxAttention.apply(q, k, v, log_f, eps)
+
+
 def plan_views(ws: torch.Tensor, B: int, H: int, L: int, d: int, dtype) -> dict:
     """Views into a workspace of the plan that fox_attn_fwd wrote."""
     dt = ACP_F32 if dtype == torch.float32 else ACP_BF16

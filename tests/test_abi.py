@@ -134,6 +134,8 @@ def test_tensor_helpers_refuse_cpu_tensors():
     q = torch.zeros(1, 1, 64, 64)
     with pytest.raises(ValueError):
         acp.forward(q, q, q, torch.zeros(1, 1, 64), 1e-4)
+    with pytest.raises(ValueError):
+        acp.fox_attention(q.requires_grad_(True), q, q, torch.zeros(1, 1, 64), 1e-4)
 
 
 def test_timing_state_without_launches():
