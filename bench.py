@@ -87,22 +87,37 @@ def frac_at_step_clock(w, pk: dict, executed_tflops: float):
     return round(executed_tflops / (PEAK_BF16_TFLOPS * clk / NOMINAL_CLOCK_GHZ), 4)
 
 
+# device headers that every kernel file includes: a change there changes the kernels
+SHARED_HEADERS = ("acp_device.h", "acp_internal.h")
+
+
+def source_digest(src: str):
+    """First 12 hex digits of the SHA-1 of a kernel source file followed by the
+    shared device headers, or None when the file does not exist."""
+    import hashlib
+    d = os.path.join(ROOT, "paper_2504_06949_amd", "csrc")
+    path = os.path.join(d, src)
+    if not os.path.exists(path):
+        return None
+    h = hashlib.sha1(open(path, "rb").read())
+    for name in SHARED_HEADERS:
+        hp = os.path.join(d, name)
+        if os.path.exists(hp):
+            h.update(open(hp, "rb").read())
+    return h.hexdigest()[:12]
+
+
 def _profile_value(kind: str, kernel: str, workload: str):
     """A machine-read line `kind kernel workload value src:digest` of the committed
     rocprofv3 summaries, as a number, or None when none exists or the kernel's
     source changed since the counters were taken."""
     import glob
-    import hashlib
     for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*.md"))):
         for line in open(path):
             f = line.split()
             if len(f) == 5 and f[0] == kind and f[1] == kernel and f[2] == workload:
                 src, digest = f[4].split(":")
-                src_path = os.path.join(ROOT, "paper_2504_06949_amd", "csrc", src)
-                if not os.path.exists(src_path):
-                    return None
-                now = hashlib.sha1(open(src_path, "rb").read()).hexdigest()[:12]
-                if now != digest:
+                if source_digest(src) != digest:
                     return None
                 return int(f[3]) if kind == "traffic" else float(f[3])
     return None

@@ -146,8 +146,14 @@ struct TileDma {
             const int i = wave + NWAVES * k;
             const unsigned lds = __builtin_amdgcn_readfirstlane(
                 (unsigned)(unsigned long long)(const lds_u8*)(tile + 1024 * i));
+            // One wait state between the SALU write of M0 and the LDS DMA that
+            // reads it (a gfx9-family hazard that the compiler's hazard check
+            // cannot see inside this statement).  Nothing in these kernels keeps
+            // a value in M0 across it (DS instructions do not read M0 on gfx9 and
+            // later), so the clobber costs nothing.
             asm volatile(
                 "s_mov_b32 m0, %0\n\t"
+                "s_nop 0\n\t"
                 "global_load_lds_dwordx4 %1, %2"
                 :
                 : "s"(lds), "v"(off[k]), "s"(base)

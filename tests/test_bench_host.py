@@ -46,13 +46,20 @@ def test_traffic_follows_the_kernel_source(tmp_path, monkeypatch):
     (tmp_path / "profiles").mkdir()
     src = src_dir / "kern.hip"
     src.write_bytes(b"// kernel v1\n")
-    digest = hashlib.sha1(src.read_bytes()).hexdigest()[:12]
+    hdr = src_dir / "acp_device.h"
+    hdr.write_bytes(b"// device header v1\n")
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    digest = bench.source_digest("kern.hip")
+    assert digest == hashlib.sha1(src.read_bytes() + hdr.read_bytes()).hexdigest()[:12]
     (tmp_path / "profiles" / "k.md").write_text(
         "# summary\n\n    traffic kern 125m 123456 kern.hip:%s\n" % digest)
-    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
     assert bench.measured_traffic("kern", "125m") == 123456
     assert bench.measured_traffic("kern", "360m") is None      # no line for this workload
     assert bench.measured_traffic("other", "125m") is None
+    hdr.write_bytes(b"// device header v2\n")                  # a shared header changed
+    assert bench.measured_traffic("kern", "125m") is None
+    hdr.write_bytes(b"// device header v1\n")
+    assert bench.measured_traffic("kern", "125m") == 123456
     src.write_bytes(b"// kernel v2\n")                          # the kernel changed since
     assert bench.measured_traffic("kern", "125m") is None
 
