@@ -82,7 +82,9 @@ __device__ __forceinline__ double wave_reduce_sum_f64(double v) {
 // wave w computes the groups of 4 heads w, w + 4, ...  The block's token rows
 // and the groups' weights stream through LDS 64 features at a time
 // (double-buffered, each tile loaded once, coalesced, by the whole workgroup);
-// each lane reads its token's features from its LDS row.
+// each lane reads its token's features from its LDS row.  The tile's next
+// global loads are held in named registers (an indexed array of them was
+// placed in scratch memory, whose stores waited for the loads).
 constexpr int kGateThreads = 256;
 constexpr int kGateTile = 64;          // features per tile (d_model % 64 == 0)
 constexpr int kGateRow = 72;           // bf16 per LDS row (rows padded to 144 bytes)
@@ -106,31 +108,29 @@ __global__ __launch_bounds__(kGateThreads) void gate_kernel(
     // tile t: 512 pieces of 16 bytes of X (row p / 8, part p % 8) and nquad * 64
     // float4 of weights; thread tid takes pieces tid, tid + 256, ...
     const int nw4 = nquad * kGateTile;
-    uint4 xr[2];
-    float4 wr[4];
+    uint4 xr0, xr1;
+    float4 wr0, wr1, wr2, wr3;
     auto fetch = [&](int t) __attribute__((always_inline)) {
-#pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            const int p = tid + kGateThreads * i;
-            xr[i] = *reinterpret_cast<const uint4*>(xsrc + (size_t)(p >> 3) * Dm + kGateTile * t + 8 * (p & 7));
-        }
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int p = tid + kGateThreads * i;
-            if (p < nw4) wr[i] = wq[(size_t)(p / kGateTile) * Dm + kGateTile * t + p % kGateTile];
-        }
+        const int p0 = tid, p1 = tid + kGateThreads;
+        xr0 = *reinterpret_cast<const uint4*>(xsrc + (size_t)(p0 >> 3) * Dm + kGateTile * t + 8 * (p0 & 7));
+        xr1 = *reinterpret_cast<const uint4*>(xsrc + (size_t)(p1 >> 3) * Dm + kGateTile * t + 8 * (p1 & 7));
+        auto wload = [&](int p) __attribute__((always_inline)) {
+            return p < nw4 ? wq[(size_t)(p / kGateTile) * Dm + kGateTile * t + p % kGateTile]
+                           : make_float4(0.f, 0.f, 0.f, 0.f);
+        };
+        wr0 = wload(tid);
+        wr1 = wload(tid + kGateThreads);
+        wr2 = wload(tid + 2 * kGateThreads);
+        wr3 = wload(tid + 3 * kGateThreads);
     };
     auto stash = [&](int buf) __attribute__((always_inline)) {
-#pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            const int p = tid + kGateThreads * i;
-            *reinterpret_cast<uint4*>(xt + (buf * 64 + (p >> 3)) * kGateRow + 8 * (p & 7)) = xr[i];
-        }
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int p = tid + kGateThreads * i;
-            if (p < nw4) wt[buf * nw4 + p] = wr[i];
-        }
+        const int p0 = tid, p1 = tid + kGateThreads;
+        *reinterpret_cast<uint4*>(xt + (buf * 64 + (p0 >> 3)) * kGateRow + 8 * (p0 & 7)) = xr0;
+        *reinterpret_cast<uint4*>(xt + (buf * 64 + (p1 >> 3)) * kGateRow + 8 * (p1 & 7)) = xr1;
+        if (tid < nw4) wt[buf * nw4 + tid] = wr0;
+        if (tid + kGateThreads < nw4) wt[buf * nw4 + tid + kGateThreads] = wr1;
+        if (tid + 2 * kGateThreads < nw4) wt[buf * nw4 + tid + 2 * kGateThreads] = wr2;
+        if (tid + 3 * kGateThreads < nw4) wt[buf * nw4 + tid + 3 * kGateThreads] = wr3;
     };
 
     // ---- logits: float32, ascending feature order -----------------------------
@@ -142,26 +142,45 @@ __global__ __launch_bounds__(kGateThreads) void gate_kernel(
     fetch(0);
     stash(0);
     __syncthreads();
+    // Each group's 64 features of a tile are taken in steps of 8, the LDS reads
+    // of step g + 1 (the lane's 8 features, the group's 8 weight vectors) issued
+    // before the 32 FMAs of step g, so that their latency is covered.
     for (int t = 0; t < ntile; ++t) {
         const int buf = t & 1;
         if (t + 1 < ntile) fetch(t + 1);
-#pragma unroll 2
-        for (int g = 0; g < kGateTile / 8; ++g) {
-            // the lane's 8 features, shared by its wave's groups of heads
-            const bf16x8 xv = *reinterpret_cast<const bf16x8*>(xt + (buf * 64 + lane) * kGateRow + 8 * g);
+        const __bf16* xrow = xt + (buf * 64 + lane) * kGateRow;
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int q = w + 4 * r;
-                if (q >= nquad) break;
-                const float4* wq_t = wt + buf * nw4 + q * kGateTile + 8 * g;
+        for (int r = 0; r < 4; ++r) {
+            const int q = w + 4 * r;
+            if (q >= nquad) break;
+            const float4* wq_t = wt + buf * nw4 + q * kGateTile;
+            bf16x8 xa = *reinterpret_cast<const bf16x8*>(xrow);
+            float4 wa[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) wa[e] = wq_t[e];
+#pragma unroll
+            for (int g = 0; g < kGateTile / 8; ++g) {
+                bf16x8 xb;
+                float4 wb[8];
+                if (g + 1 < kGateTile / 8) {
+                    xb = *reinterpret_cast<const bf16x8*>(xrow + 8 * (g + 1));
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) wb[e] = wq_t[8 * (g + 1) + e];
+                }
+                __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
                 for (int e = 0; e < 8; ++e) {
-                    const float xe = (float)xv[e];
-                    const float4 w4 = wq_t[e];   // the same address on every lane
-                    acc[r][0] = __builtin_fmaf(xe, w4.x, acc[r][0]);
-                    acc[r][1] = __builtin_fmaf(xe, w4.y, acc[r][1]);
-                    acc[r][2] = __builtin_fmaf(xe, w4.z, acc[r][2]);
-                    acc[r][3] = __builtin_fmaf(xe, w4.w, acc[r][3]);
+                    const float xe = (float)xa[e];
+                    acc[r][0] = __builtin_fmaf(xe, wa[e].x, acc[r][0]);
+                    acc[r][1] = __builtin_fmaf(xe, wa[e].y, acc[r][1]);
+                    acc[r][2] = __builtin_fmaf(xe, wa[e].z, acc[r][2]);
+                    acc[r][3] = __builtin_fmaf(xe, wa[e].w, acc[r][3]);
+                }
+                __builtin_amdgcn_sched_barrier(0);
+                if (g + 1 < kGateTile / 8) {
+                    xa = xb;
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) wa[e] = wb[e];
                 }
             }
         }
