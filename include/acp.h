@@ -244,7 +244,9 @@ acp_status fox_attn_fwd_projected(const void* Q, const void* K, const void* V, c
  * (float64 prefix sums across the sequence by a chained scan, exact whenever flag
  * bit 2 stays clear), with the per-head statistics of stage 1's checks.
  *   Supported: d_model a multiple of 64 up to 8192; H <= 64; L, d as for the
- *   attention.
+ *   attention; and ceil(H / 4) * d_model * 16 <= B * H * L * 4 (a float32 copy of
+ *   the weights is kept in the workspace's backward area, which the forward
+ *   leaves free), else ACP_EUNSUPPORTED.
  *   ws: a workspace of acp_workspace_size(B, H, L, d, dt) bytes.
  *
  * fox_attn_fwd_gated:  fox_attn_fwd for the gates acp_gate_project left in this

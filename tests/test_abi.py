@@ -236,9 +236,12 @@ def test_noalloc_forward_rejects_shapes_beyond_its_fixed_scratch():
     (dict(d_model=8200), acp.ACP_EUNSUPPORTED),
     (dict(L=100), acp.ACP_EUNSUPPORTED),
     (dict(ws_bytes=16), acp.ACP_EWORKSPACE),
+    (dict(d_model=4096), acp.ACP_EUNSUPPORTED),     # weight copy beyond B*H*L*4 bytes
 ])
 def test_gate_project_rejects_bad_arguments(kw, status):
     a = dict(X=16, w_f=16, b_f=16, B=1, L=64, d_model=64, H=2, d=64, log_f=16, ws=16,
              ws_bytes=1 << 40, stream=None)
     a.update(kw)
     assert acp.acp_gate_project(*a.values()) == status
+    if kw.get("d_model") == 4096:
+        assert "too large for these shapes" in acp.acp_last_error()
