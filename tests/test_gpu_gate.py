@@ -28,6 +28,8 @@ def _plan(ws, B, H, L, d, dtype):
     (2, 320, 64, 3, 64, 81),        # a partial group of heads, ragged block count
     (4, 1024, 1024, 16, 128, 82),
     (1, 16384, 768, 12, 64, 83),    # 256 blocks chained per head
+    (2, 192, 128, 5, 64, 85),       # groups of two heads, the last one partial
+    (1, 256, 64, 20, 64, 86),       # more groups than waves
 ])
 def test_gate_projection_and_gated_forward(B, L, Dm, H, d, seed):
     print(f"case: gate projection B={B} L={L} d_model={Dm} H={H} d={d}", flush=True)
