@@ -130,6 +130,33 @@ def test_random_shapes_full(B, H, L, d, mu, eps, seed):
     _full_parity(w, eps=eps)
 
 
+def _random_long_cases(n=6, seed=2026):
+    """Longer seeded shapes (1024 to 2560 positions, ragged multiples of 64), so
+    that every key block's loop over query tiles runs long and the d = 128 dK/dV
+    pass adds its wave pairs' partial sums after many tiles, compared in full."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for i in range(n):
+        H = int(rng.integers(1, 4))
+        L = 64 * int(rng.integers(16, 41))
+        d = 128 if i % 2 == 0 else 64
+        mu = tuple(float(m) for m in rng.uniform(-1.0, 12.0, size=H))
+        eps = float(rng.choice([math.exp(-10), math.exp(-3)]))
+        out.append((1, H, L, d, mu, eps, 200 + i))
+    return out
+
+
+_RANDOM_LONG = _random_long_cases()
+
+
+@pytest.mark.parametrize("B,H,L,d,mu,eps,seed", _RANDOM_LONG,
+                         ids=[f"B{c[0]}H{c[1]}L{c[2]}d{c[3]}eps{c[5]:.3g}" for c in _RANDOM_LONG])
+def test_random_long_shapes_full(B, H, L, d, mu, eps, seed):
+    w = workloads.custom(f"rlong{seed}", B, H, L, d, "bf16", seed, mu=mu)
+    print(f"case: fwd/bwd {w.describe()} eps={eps:g}", flush=True)
+    _full_parity(w, eps=eps)
+
+
 def test_small_f32_d128_full():
     w = workloads.custom("f32d128", 1, 2, 192, 128, "f32", 25, mu=(0.5, 4.0))
     print(f"case: fwd/bwd {w.describe()}", flush=True)
