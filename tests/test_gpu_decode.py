@@ -24,7 +24,9 @@ def _lib():
 
 
 def _token(g, name, t):
-    return g[name][:, :, t].contiguous()
+    # a fresh allocation: a slice that is already contiguous (B = H = 1) would
+    # keep the offset of position t and miss the ABI's 16-byte alignment
+    return g[name][:, :, t].clone(memory_format=torch.contiguous_format)
 
 
 def _run(w, L0, C, eps, L_max, poke=None):
@@ -103,6 +105,38 @@ def test_decode_matches_oracle(dtype, d):
     steps = _check(w, 333, 512, EPS, 4096, expect_lost=False)
     # strongly decaying heads move their pointer while the step runs
     assert int(steps[-1][3][0, 0]) > int(steps[0][3][0, 0]) > 0
+
+
+def _random_decode_cases(n=6, seed=2027):
+    """Seeded random decoding set-ups: head counts, head dims, dtypes, prompt
+    lengths from 1 token up (not multiples of 64), rings from smaller than the
+    kept window to larger than the context, eps from none to heavy pruning, and
+    L_max from the final length up to four times it."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for i in range(n):
+        B = int(rng.integers(1, 3))
+        H = int(rng.integers(1, 6))
+        d = int(rng.choice([64, 128]))
+        dtype = "f32" if i == n - 1 else "bf16"
+        L0 = int(rng.integers(1, 600))
+        L = L0 + int(rng.integers(20, 90))
+        C = int(rng.choice([64, 192, 512, 1024]))
+        eps = float(rng.choice([0.0, math.exp(-10), math.exp(-3)]))
+        L_max = L * int(rng.integers(1, 5))
+        mu = tuple(float(m) for m in rng.uniform(-1.0, 20.0, size=H))
+        out.append((B, H, d, dtype, L0, L, C, eps, L_max, mu, 300 + i))
+    return out
+
+
+_RANDOM_DEC = _random_decode_cases()
+
+
+@pytest.mark.parametrize("B,H,d,dtype,L0,L,C,eps,L_max,mu,seed", _RANDOM_DEC,
+                         ids=[f"B{c[0]}H{c[1]}d{c[2]}{c[3]}L0_{c[4]}C{c[6]}" for c in _RANDOM_DEC])
+def test_decode_random_setups(B, H, d, dtype, L0, L, C, eps, L_max, mu, seed):
+    w = workloads.custom("decr", B, H, L, d, dtype, seed, mu=mu, qk_norm=True)
+    _check(w, L0, C, eps, L_max)
 
 
 def test_decode_ring_smaller_than_window():
