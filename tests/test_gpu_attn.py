@@ -38,6 +38,15 @@ def _run_gpu(x, eps, grads=True):
     return out
 
 
+def _bound(tol, name, want):
+    """The bound on one output: absolute for LSE and dlog f (float32 outputs) and
+    for the float32 path; for O, dQ, dK and dV in bfloat16 relative to the largest
+    reference value where that exceeds 1 (see _scaled_tol)."""
+    if tol >= 1e-2 and name in ("o", "dq", "dk", "dv"):
+        return _scaled_tol(tol, want)
+    return tol
+
+
 def _compare_head(got, ref, b, h, tol, names=("o", "lse", "dq", "dk", "dv", "dlog_f")):
     errs = {}
     for n in names:
@@ -45,8 +54,8 @@ def _compare_head(got, ref, b, h, tol, names=("o", "lse", "dq", "dk", "dv", "dlo
         e = float(np.max(np.abs(a - ref[n])))
         errs[n] = e
         assert np.all(np.isfinite(a)), (n, b, h)
-    bad = {n: e for n, e in errs.items() if e > tol}
-    assert not bad, f"head ({b},{h}) errors over {tol}: {errs}"
+    bad = {n: e for n, e in errs.items() if e > _bound(tol, n, ref[n])}
+    assert not bad, f"head ({b},{h}) errors over the bound: {errs}"
     return errs
 
 
@@ -316,9 +325,11 @@ def _head_f64(x, b, h):
 
 
 def _scaled_tol(tol, ref):
-    """bf16 outputs carry a relative rounding of 2^-9, so where rows are scaled
-    up (outputs above 1 in size) the bound is taken relative to the largest
-    reference value."""
+    """bf16 outputs carry a relative rounding of 2^-9 (half an ulp: 2^-6 = 0.016
+    for values in [4, 8)), so where an output exceeds 1 in size (rows scaled
+    beyond norm sqrt(d), or attention concentrated on a few keys by strong
+    forgetting, which makes dV approach dO) the bound is taken relative to the
+    largest reference value."""
     return tol * max(1.0, float(np.max(np.abs(ref))))
 
 
@@ -340,7 +351,7 @@ def _check_whole_heads(w, x, got, heads):
         for n, want in ref.items():
             a = f64(got[n][b, h])
             errs[n] = float(np.max(np.abs(a - want)))
-            assert errs[n] <= _scaled_tol(tol, want), (b, h, n, errs[n])
+            assert errs[n] <= _bound(tol, n, want), (b, h, n, errs[n])
         print(f"  head ({b},{h}) kept {plan['kept']}: {errs}", flush=True)
 
 
