@@ -18,11 +18,24 @@ def _lib():
     ensure_built()
 
 
+def _random_projection_shapes(n=5, seed=2028):
+    """Seeded shapes within the projection's limits: L a multiple of 128, d_model a
+    multiple of 64, H * d a multiple of 128."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for _ in range(n):
+        d = int(rng.choice([64, 128]))
+        H = int(rng.integers(1, 4)) * (1 if d == 128 else 2)
+        out.append((int(rng.integers(1, 4)), 128 * int(rng.integers(1, 7)),
+                    64 * int(rng.integers(1, 13)), H, d))
+    return out
+
+
 @pytest.mark.parametrize("B,L,Dm,H,d", [(2, 256, 192, 2, 64), (1, 384, 128, 3, 128),
-                                        (1, 128, 64, 2, 64)])
+                                        (1, 128, 64, 2, 64)] + _random_projection_shapes())
 def test_projection_and_projected_forward(B, L, Dm, H, d):
     print(f"case: projection B={B} L={L} d_model={Dm} H={H} d={d}", flush=True)
-    p = workloads.projection_inputs(B, L, Dm, H, d, seed=50 + d)
+    p = workloads.projection_inputs(B, L, Dm, H, d, seed=50 + d + Dm + L)
     w = workloads.custom("prj", B, H, L, d, "bf16", 51, mu=(0.5, 2.0, 6.0))
     x = workloads.generate(w, with_grad=True)
     g = to_gpu(x)
