@@ -168,6 +168,38 @@ def test_random_long_shapes_full(B, H, L, d, mu, eps, seed):
     _full_parity(w, eps=eps)
 
 
+def _random_mixed_cases(n=12, seed=2029):
+    """Seeded shapes that also vary what the other families hold fixed: per-head
+    row norms from 0.5 to 16 (logit bounds up to 2048), gate spreads from 0.1 to 2,
+    eps up to 0.9, and the float32 path."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for i in range(n):
+        B = int(rng.integers(1, 3))
+        H = int(rng.integers(1, 5))
+        L = 64 * int(rng.integers(1, 33))
+        d = int(rng.choice([64, 128]))
+        mu = tuple(float(m) for m in rng.uniform(-2.0, 25.0, size=H))
+        eps = float(rng.choice([0.0, math.exp(-20), math.exp(-10), math.exp(-3), 0.3, 0.9]))
+        dtype = "f32" if i % 4 == 3 else "bf16"
+        rn = tuple(float(r) for r in rng.choice([0.5, 1.0, 4.0, 8.0, 16.0], size=H))
+        sig = float(rng.choice([0.1, 0.5, 2.0]))
+        out.append((B, H, L, d, dtype, mu, rn, sig, eps, 400 + i))
+    return out
+
+
+_RANDOM_MIXED = _random_mixed_cases()
+
+
+@pytest.mark.parametrize("B,H,L,d,dtype,mu,rn,sig,eps,seed", _RANDOM_MIXED,
+                         ids=[f"B{c[0]}H{c[1]}L{c[2]}d{c[3]}{c[4]}eps{c[8]:.3g}" for c in _RANDOM_MIXED])
+def test_random_mixed_shapes_full(B, H, L, d, dtype, mu, rn, sig, eps, seed):
+    w = workloads.custom(f"rmix{seed}", B, H, L, d, dtype, seed, mu=mu, row_norms=rn,
+                         gate_sigma=sig)
+    print(f"case: fwd/bwd {w.describe()} eps={eps:g}", flush=True)
+    _full_parity(w, eps=eps)
+
+
 def test_small_f32_d128_full():
     w = workloads.custom("f32d128", 1, 2, 192, 128, "f32", 25, mu=(0.5, 4.0))
     print(f"case: fwd/bwd {w.describe()}", flush=True)
