@@ -154,3 +154,42 @@ def test_boundary_is_deterministic():
     b = _gpu_plan(x, w.eps)
     for n in a:
         np.testing.assert_array_equal(a[n], b[n])
+
+
+def test_wide_gate_spreads_flag_inexact_sums():
+    """Gates with a wide spread (logits N(mu, 3): log f from about -15 to -1e-17 in
+    one head) give cumulative sums spanning more than 53 bits on many heads.  Flag
+    bit 2 must be set exactly on those (the device rule: from 53 bits on); their c
+    stays within one float32 ulp of the sequential float64 definition, U and delta
+    stay exact, and every other head is bit-exact throughout."""
+    w = workloads.custom("wide", 2, 8, 4096, 64, "bf16", 91,
+                         mu=(-2.0, 0.0, 3.0, 6.0, 10.0, 15.0, 20.0, 28.0), gate_sigma=3.0)
+    print(f"case: boundary {w.describe()}", flush=True)
+    x = workloads.generate(w, with_grad=False)
+    got = _gpu_plan(x, w.eps)
+    lf = x["log_f"].numpy()
+    c_ref = orc.cumsum_log_gates(lf)
+    flagged = exact = 0
+    for b in range(w.B):
+        for h in range(w.H):
+            q = x["q"][b, h].float().numpy()
+            k = x["k"][b, h].float().numpy()
+            U = orc.logit_bound(orc.row_norm_sq_max(q), orc.row_norm_sq_max(k), w.d)
+            delta = orc.threshold(U, w.L, w.eps)
+            assert got["bound_u"][b, h] == U and got["delta"][b, h] == delta, (b, h)
+            span = orc.cumsum_span_bits(lf[b, h])
+            fl = int(got["flags"][b, h])
+            assert bool(fl & 4) == (span >= 53) and fl & ~4 == 0, (b, h, span, fl)
+            if span >= 53:
+                flagged += 1
+                ulp = np.spacing(np.abs(c_ref[b, h]).astype(np.float32))
+                assert np.all(np.abs(got["c"][b, h] - c_ref[b, h]) <= ulp), (b, h)
+                continue
+            exact += 1
+            np.testing.assert_array_equal(got["c"][b, h], c_ref[b, h])
+            rs, ce = orc.boundary_from_block_keep(orc.block_keep_topright(c_ref[b, h], delta))
+            np.testing.assert_array_equal(got["row_start"][b, h], rs)
+            np.testing.assert_array_equal(got["col_end"][b, h], ce)
+            assert got["kept"][b, h] == orc.kept_tiles(rs)
+    print(f"  {flagged} heads flagged inexact, {exact} exact", flush=True)
+    assert flagged > 0 and exact > 0
