@@ -35,15 +35,17 @@
  *       bit 0  some log f > 0 (the gate must lie in (0, 1]; monotonicity of D fails)
  *       bit 1  some log f is NaN or infinite, or the cumulative sum c leaves the
  *              float32 range
- *       bit 2  the partial sums of log f span 53 bits or more: E - lsb >= 53, with
+ *       bit 2  the partial sums of log f span 105 bits or more: E - lsb >= 105, with
  *              lsb the exponent of the smallest float32 ulp among the nonzero gates
- *              and 2^E the least power of two above sum |log f|.  Up to 53 bits
- *              every float64 partial sum is exact, so any summation order gives the
- *              sequential definition's c; the flag is raised from 53 on (one bit
- *              early) because the device's own float64 sum of |log f| may round a
- *              total just above a power of two down to it once the span exceeds
- *              53 bits, which would then read one bit short.  Clear bit 2 thus
- *              guarantees c is exact; set, c may differ in its last bit.
+ *              and 2^E the least power of two above sum |log f|.  The device sums
+ *              log f in double-double (pairs of float64 values), which is exact
+ *              in any summation order up to a 105-bit span; the flag is raised
+ *              from 105 on because the device's own sum of |log f| may round a
+ *              total just above a power of two down to it beyond 105 bits, which
+ *              would then read one bit short.  Clear bit 2 thus guarantees that c
+ *              is the float32 rounding of the exact sum; set, c may differ in its
+ *              last bit.  (At L <= 131072 a span of 105 bits needs a ratio of
+ *              2^65 or more between the largest and the smallest nonzero |log f|.)
  *       bit 3  rho_q^2 or rho_k^2 is not finite (Q or K holds NaN/Inf or overflows),
  *              or, in the QK-norm variants, a scale bound is negative or not finite
  *       bit 4  (decoding only) a key that ACP keeps had already left the ring cache,
@@ -54,8 +56,9 @@
  *     With bit 0, 1 or 3 set the boundary and the attention outputs are unspecified.
  *
  * Numerics of the pruning decision (identical on every device and on the host):
- *   c_i   = float32( float64 running sum of log f_0..log f_i )  (exact whenever
- *           flag bit 2 is clear, so any summation order gives the same c)
+ *   c_i   = float32 rounding (to nearest, ties to even) of the exact sum
+ *           log f_0 + ... + log f_i (guaranteed whenever flag bit 2 is clear; it
+ *           depends on no summation order)
  *   rho^2 = max_i float64 sum_{k ascending} x_ik^2      (squares exact in float64)
  *   U     = sqrt(rho_q^2 * rho_k^2 / d), delta = -(2U + (log L - log eps)); float64,
  *           IEEE round-to-nearest; log L - log eps is evaluated on the host.
@@ -241,8 +244,8 @@ acp_status fox_attn_fwd_projected(const void* Q, const void* K, const void* V, c
  *   a = sum_k x_k w_fk summed in float32 in ascending feature order, + b_f
  *   (float32), and log f = -softplus(-a) evaluated in float64 and rounded once;
  * and, into the workspace, c exactly as stage 1 would compute it from this log f
- * (float64 prefix sums across the sequence by a chained scan, exact whenever flag
- * bit 2 stays clear), with the per-head statistics of stage 1's checks.
+ * (double-double prefix sums across the sequence by a chained scan, exact whenever
+ * flag bit 2 stays clear), with the per-head statistics of stage 1's checks.
  *   Supported: d_model a multiple of 64 up to 8192; H <= 64; L, d as for the
  *   attention; and ceil(H / 4) * d_model * 16 <= B * H * L * 4 (a float32 copy of
  *   the weights is kept in the workspace's backward area, which the forward
@@ -272,8 +275,8 @@ acp_status fox_attn_fwd_gated(const void* Q, const void* K, const void* V, acp_d
  *
  * State: one caller-owned device buffer of acp_decode_state_size() bytes holds,
  * per (batch, head), a ring cache of C positions (position j in slot j mod C)
- * for K, V and c, the float64 running sum of log f, delta, the pointer and the
- * flag word.  C is a multiple of 64; with ACP it only needs to cover the kept
+ * for K, V and c, the running sum of log f (a double-double pair), delta, the
+ * pointer and the flag word.  C is a multiple of 64; with ACP it only needs to cover the kept
  * window (positions from 64 pointer to t), which is how ACP frees the cache
  * memory behind the pointer.  If a kept key is overwritten, flag bit 4 is set and
  * the query attends to the kept keys the ring still holds, positions
@@ -291,8 +294,9 @@ typedef struct {
     size_t k_cache;    /* [B,H,C,d] dt     keys, position j in slot j mod C          */
     size_t v_cache;    /* [B,H,C,d] dt     values                                    */
     size_t c;          /* [B,H,C]   float  c_j of the cached positions               */
-    size_t cum;        /* [2,B,H]   double running float64 sum of log f; the value
-                                           after position p is in copy p mod 2          */
+    size_t cum;        /* [2,B,H,2] double running sum of log f as a double-double
+                                           pair (hi, lo); the value after position p
+                                           is in copy p mod 2                           */
     size_t delta;      /* [B,H]     double delta                                     */
     size_t pointer;    /* [2,B,H]   int32  first kept key block of query p, in copy
                                            p mod 2                                      */

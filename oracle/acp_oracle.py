@@ -9,9 +9,11 @@ blocks of BLOCK = 64 rows by 64 columns.
 Every function cites the passage of the paper it follows.  Points where the paper
 is silent or garbled are settled as follows (the same readings bind the HIP path):
 
-* cumulative gates (Sec. 2, "FlashAttention implementation"): c_i is the sum of
-  log f_l for l <= i, accumulated in float64 in index order and rounded once to
-  float32.  c is the canonical float32 quantity both sides compare on.
+* cumulative gates (Sec. 2, "FlashAttention implementation"): c_i is the float32
+  rounding (to nearest, ties to even) of the exact sum of log f_l for l <= i.
+  Being the rounding of an exact value, it does not depend on the order of the
+  additions, so a parallel scan can reproduce it bit for bit; c is the canonical
+  float32 quantity both sides compare on.
 * logit bound (Sec. 3, "Safe pruning"): U = rho_q * rho_k / sqrt(d), with rho the
   largest row L2 norm of the stored Q (resp. K) of the one sequence and head.
   Squared norms are float64 sums in ascending feature order; U = sqrt(rq2*rk2/d)
@@ -67,18 +69,64 @@ __all__ = [
 def cumsum_log_gates(log_f) -> np.ndarray:
     """c_i = sum_{l<=i} log f_l (Sec. 2, FlashAttention paragraph: D = c1^T - 1c^T).
 
-    float64 running sum in index order, rounded once to float32.
+    The float32 rounding of the exact prefix sum of the float32 gates.  Where a
+    row's partial sums span at most 53 bits (cumsum_span_bits) every float64
+    running sum is exact, and one rounding of it gives c; wider rows are summed
+    exactly in integers.  A sum beyond the float32 range rounds to -inf.
     """
-    x = np.asarray(log_f, dtype=np.float32).astype(np.float64)
-    acc = np.zeros(x.shape[:-1], dtype=np.float64)
-    out = np.empty(x.shape, dtype=np.float64)
-    for i in range(x.shape[-1]):
-        acc = acc + x[..., i]
-        out[..., i] = acc
-    # a sum beyond the float32 range rounds to -inf (IEEE round-to-nearest), which
-    # is the value the checks expect; numpy would only warn about it
-    with np.errstate(over="ignore"):
-        return out.astype(np.float32)
+    x = np.asarray(log_f, dtype=np.float32)
+    flat = x.reshape(-1, x.shape[-1]) if x.ndim else x.reshape(1, 1)
+    out = np.empty(flat.shape, dtype=np.float32)
+    for r in range(flat.shape[0]):
+        row = flat[r]
+        if not np.all(np.isfinite(row)) or cumsum_span_bits(row) <= 53:
+            acc = np.cumsum(row.astype(np.float64))
+            # a sum beyond the float32 range rounds to -inf (IEEE round-to-nearest),
+            # which is the value the checks expect; numpy would only warn about it
+            with np.errstate(over="ignore", invalid="ignore"):
+                out[r] = acc.astype(np.float32)
+        else:
+            out[r] = _exact_prefix_f32(row)
+    return out.reshape(x.shape)
+
+
+def _exact_prefix_f32(row) -> np.ndarray:
+    """Prefix sums of finite float32 values, exact in integers (each value is an
+    integer significand times a power of two), each rounded once to float32."""
+    f, e = np.frexp(np.asarray(row, dtype=np.float32).astype(np.float64))
+    m = (f * 2.0 ** 24).astype(np.int64)          # exact: at most 24 significant bits
+    k = e.astype(np.int64) - 24                   # row[i] = m[i] * 2^k[i]
+    nz = m != 0
+    out = np.zeros(len(m), dtype=np.float32)
+    if not nz.any():
+        return out
+    lsb = int(k[nz].min())
+    acc = 0
+    for i in range(len(m)):
+        if m[i]:
+            acc += int(m[i]) << int(k[i] - lsb)
+        out[i] = _int_to_f32(acc, lsb)
+    return out
+
+
+def _int_to_f32(n: int, lsb: int) -> np.float32:
+    """Round n * 2^lsb (n an integer) to the nearest float32, ties to even."""
+    if n == 0:
+        return np.float32(0.0)
+    sign = -1.0 if n < 0 else 1.0
+    a = abs(n)
+    e = max(a.bit_length() - 1 + lsb, -126)       # 2^e <= |value| < 2^(e+1); subnormals at -126
+    shift = (e - 23) - lsb                        # drop bits below 2^(e-23)
+    if shift <= 0:
+        q = a << -shift
+    else:
+        q, rem = a >> shift, a & ((1 << shift) - 1)
+        half = 1 << (shift - 1)
+        if rem > half or (rem == half and q & 1):
+            q += 1
+    if e - 23 > 104 or (e - 23 == 104 and q >= 1 << 24):
+        return np.float32(sign * np.inf)         # beyond the largest float32
+    return np.float32(sign * math.ldexp(float(q), e - 23))
 
 
 def gate_logits(x, w_f, b_f) -> np.ndarray:
@@ -170,11 +218,13 @@ def cumsum_span_bits(log_f_1d) -> int:
 
 def cumsum_inexact_flag(log_f_1d) -> bool:
     """Flag bit 2 of stage 1 (reading of Sec. 2's cumulative sum, whose precision
-    the paper leaves open): raised when the span is 53 bits or more.  A span of
-    53 is still exact; it is flagged because a summation of |x| in float64 that
-    rounds (possible only beyond 53 bits) can place its total one power of two
-    low and so read a span of 54 as 53.  Clear, the flag guarantees exact c."""
-    return cumsum_span_bits(log_f_1d) >= 53
+    the paper leaves open): raised when the span is 105 bits or more.  The device
+    sums in double-double (pairs of float64 values), which is exact for any
+    association while the span is at most 105 bits; its double-double sum of |x|
+    is then exact too, so it reads every span up to 105 exactly and wider ones as
+    at least 105.  Clear, the flag guarantees that c is the rounding of the exact
+    sum."""
+    return cumsum_span_bits(log_f_1d) >= 105
 
 
 def row_norm_sq_max(x) -> float:

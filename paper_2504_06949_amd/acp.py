@@ -585,13 +585,15 @@ class Decoder:
         return self.views()["pointer"][(self.t - 1) % 2]
 
     def current_cum(self) -> torch.Tensor:
-        """[B, H] running float64 sum after the latest position (a view)."""
+        """[B, H, 2] running sum after the latest position as a double-double
+        pair (hi, lo): the value is hi + lo exactly (a view)."""
         return self.views()["cum"][(self.t - 1) % 2]
 
     def views(self) -> dict:
         """Views of the state: k_cache, v_cache [B,H,C,d], c [B,H,C], delta and
-        flags [B,H]; cum and pointer [2,B,H], the values after position p being
-        copy p % 2 (current_pointer() and current_cum() pick the latest)."""
+        flags [B,H]; pointer [2,B,H] and cum [2,B,H,2] (pairs hi, lo), the values
+        after position p being copy p % 2 (current_pointer() and current_cum() pick
+        the latest)."""
         lay = acp_decode_offsets(self.B, self.H, self.C, self.d, self.dt)
         B, H, C, d = self.B, self.H, self.C, self.d
 
@@ -603,7 +605,7 @@ class Decoder:
             "k_cache": view(lay.k_cache, B * H * C * d, self.dtype).view(B, H, C, d),
             "v_cache": view(lay.v_cache, B * H * C * d, self.dtype).view(B, H, C, d),
             "c": view(lay.c, B * H * C, torch.float32).view(B, H, C),
-            "cum": view(lay.cum, 2 * B * H, torch.float64).view(2, B, H),
+            "cum": view(lay.cum, 4 * B * H, torch.float64).view(2, B, H, 2),
             "delta": view(lay.delta, B * H, torch.float64).view(B, H),
             "pointer": view(lay.pointer, 2 * B * H, torch.int32).view(2, B, H),
             "flags": view(lay.flags, B * H, torch.int32).view(B, H),

@@ -61,8 +61,8 @@ Layout layout(int B, int H, int L, int d) {
     const size_t nb = ((size_t)L + 127) / 128;   // 128-row blocks of the attention kernels
     y.sched_q = take(BH * nb * 4);
     y.sched_k = take(BH * nb * 4);
-    y.gate_agg = take(BH * M * 8);      // gate producer's chained scan (acp_gate_project)
-    y.gate_incl = take(BH * M * 8);
+    y.gate_agg = take(BH * M * 16);     // gate producer's chained scan (acp_gate_project):
+    y.gate_incl = take(BH * M * 16);    // a double-double pair per block
     y.gate_stats = take(BH * M * sizeof(acp::GateStats));
     y.total = off;
     return y;
@@ -491,7 +491,7 @@ static DecLayout dec_layout(int B, int H, int C, int d, acp_dtype dt) {
     y.k = take(BH * C * d * es);
     y.v = take(BH * C * d * es);
     y.c = take(BH * C * 4);
-    y.cum = take(2 * BH * 8);
+    y.cum = take(2 * BH * 16);
     y.delta = take(BH * 8);
     y.ptr = take(2 * BH * 4);
     y.flags = take(BH * 4);

@@ -9,7 +9,8 @@
 // slot j mod C), so its memory is what the kept window needs, not the context.
 //
 // Kernels:
-//   decode_init_kernel  prompt of L0 tokens -> delta, the float64 running cumsum,
+//   decode_init_kernel  prompt of L0 tokens -> delta, the running cumsum (a
+//                       double-double pair),
 //                       c of the prompt's last C positions, the pointer of query
 //                       L0 - 1
 //   decode_copy_kernel  the prompt's last K/V rows into the ring
@@ -50,8 +51,8 @@ __global__ __launch_bounds__(kPlanThreads) void decode_init_kernel(
     double log_lmax_over_eps, float* __restrict__ cc,
     double* __restrict__ cs_out, int* __restrict__ ptr_out, double* __restrict__ delta_out,
     int* __restrict__ flags_out) {
-    __shared__ double s_dbl[kPlanWaves];
-    __shared__ double s_dbl2[kPlanWaves];
+    __shared__ double s_dbl[2][kPlanWaves];
+    __shared__ double s_dbl2[2][kPlanWaves];
     __shared__ int s_int[kPlanWaves];
     __shared__ float s_last[kMaxBlocks];   // c at the last row of each full block
     __shared__ double s_delta;
@@ -75,7 +76,7 @@ __global__ __launch_bounds__(kPlanThreads) void decode_init_kernel(
     const float* x = log_f + (size_t)bh * L0;
     const int per = (L0 + kPlanThreads - 1) / kPlanThreads;
     const int beg = min(t * per, L0), end = min(beg + per, L0);
-    double local = 0.0, local_abs = 0.0;
+    DD local{0.0, 0.0}, local_abs{0.0, 0.0};
     int min_lsb = 1 << 30;
     for (int i = beg; i < end; ++i) {
         const float v = x[i];
@@ -84,30 +85,29 @@ __global__ __launch_bounds__(kPlanThreads) void decode_init_kernel(
             if (v > 0.0f) flags |= 1;
             if (v != 0.0f) min_lsb = min(min_lsb, lsb_exp(v));
         }
-        local += (double)v;
-        local_abs += __builtin_fabs((double)v);
+        local = dd_add(local, (double)v);
+        local_abs = dd_add(local_abs, __builtin_fabs((double)v));
     }
-    const double incl = block_inclusive_scan(local, s_dbl);
-    double run = incl - local;
-    auto sum = [](double a, double b) { return a + b; };
+    const DD incl = block_inclusive_scan_dd(local, s_dbl[0], s_dbl[1]);
+    DD run = dd_add(incl, dd_neg(local));
     auto imin = [](int a, int b) { return min(a, b); };
     auto ior = [](int a, int b) { return a | b; };
-    const double total_abs = block_reduce(local_abs, s_dbl2, sum);
+    const DD total_abs = block_sum_dd(local_abs, s_dbl2[0], s_dbl2[1]);
     min_lsb = block_reduce(min_lsb, s_int, imin);
-    if (t == 0 && total_abs > 0.0) {
-        // the rule of the plan kernel: flagged from a span of 53 bits on
-        const int biased = (int)((__double_as_longlong(total_abs) >> 52) & 0x7ff);
-        const int top = (biased > 0 ? biased : 1) - 1023 + 1;
-        if (top - min_lsb >= 53) flags |= 4;
-        if (!__builtin_isfinite((float)total_abs)) flags |= 2;
+    if (t == 0 && total_abs.hi > 0.0) {
+        // the rule of the plan kernel: flagged from a span of 105 bits on
+        if (dd_top_exp(total_abs) - min_lsb >= kExactSpanBits) flags |= 4;
+        if (__builtin_isinf(dd_to_f32(total_abs))) flags |= 2;
     }
     for (int i = beg; i < end; ++i) {
-        run += (double)x[i];
-        const float cf = (float)run;
+        run = dd_add(run, (double)x[i]);
+        const float cf = dd_to_f32(run);
         if (i >= L0 - C) cc[(size_t)bh * C + (i % C)] = cf;
         if ((i & (kBlock - 1)) == kBlock - 1) s_last[i / kBlock] = cf;
         if (i == L0 - 1) {
-            cs_out[(size_t)((L0 - 1) & 1) * gridDim.x + bh] = run;
+            double* cs = cs_out + 2 * ((size_t)((L0 - 1) & 1) * gridDim.x + bh);
+            cs[0] = run.hi;
+            cs[1] = run.lo;
             s_ct = cf;
         }
     }
@@ -212,7 +212,7 @@ __global__ __launch_bounds__(kDecChunk) void decode_step_kernel(
     const int first = gone + 1 > 0 ? gone + 1 : 0;          // oldest position held
     // (clamped to [0, nb], so that even a corrupted state indexes inside the ring)
     const int p_old = min(max(ptr[(size_t)rd * BH + bh], 0), nb);
-    const double cs_old = cum[(size_t)rd * BH + bh];
+    const DD cs_old{cum[2 * ((size_t)rd * BH + bh)], cum[2 * ((size_t)rd * BH + bh) + 1]};
     const float lff = log_f[bh];
     const double dl = delta[bh];
     const int e0 = (lane % G) * kVec;
@@ -262,8 +262,12 @@ __global__ __launch_bounds__(kDecChunk) void decode_step_kernel(
     asm volatile("" : "+v"(cb) : : "memory");
 
     // ---- 2. c_t and the new pointer --------------------------------------------------
-    const double s2 = cs_old + (double)lff;
-    const float ct = (float)s2;
+    // cum + log f_t as a pair: TwoSum of the leading parts, then the remainders
+    // (the one addition that can round; step 4 checks it), then TwoSum again
+    const DD s1 = two_sum(cs_old.hi, (double)lff);
+    const DD lo_sum = two_sum(cs_old.lo, s1.lo);
+    const DD s2 = two_sum(s1.hi, lo_sum.hi);
+    const float ct = dd_to_f32(s2);
     // blocks n .. n + 63 per ballot; the block holding t (n >= nb) is always kept
     int n = n_start;
     unsigned long long bal = __ballot(n + lane >= nb || (double)ct - (double)cb >= dl);
@@ -383,9 +387,9 @@ __global__ __launch_bounds__(kDecChunk) void decode_step_kernel(
             int fl = flags[bh];
             if (!__builtin_isfinite(lff)) fl |= 2;
             else if (lff > 0.0f) fl |= 1;
-            // the running sum stays the exact prefix sum only while no addition rounds
-            const double bb = s2 - cs_old;
-            if ((cs_old - (s2 - bb)) + ((double)lff - bb) != 0.0) fl |= 4;
+            // the running pair stays the exact prefix sum only while the sum of the
+            // remainders does not round
+            if (lo_sum.lo != 0.0) fl |= 4;
             // A kept key is lost iff the block of position t - C is kept (the blocks
             // before it are then kept too); its last key is still in the ring.
             if (gone >= 0) {
@@ -393,7 +397,8 @@ __global__ __launch_bounds__(kDecChunk) void decode_step_kernel(
                 if ((double)ct - (double)crow[ring(kBlock * nx + kBlock - 1, C)] >= dl) fl |= 16;
             }
             flags[bh] = fl;
-            cum[(size_t)(t & 1) * BH + bh] = s2;
+            cum[2 * ((size_t)(t & 1) * BH + bh)] = s2.hi;
+            cum[2 * ((size_t)(t & 1) * BH + bh) + 1] = s2.lo;
             ptr[(size_t)(t & 1) * BH + bh] = n;
             cc[head + ring(t, C)] = ct;
         }

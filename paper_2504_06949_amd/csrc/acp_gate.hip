@@ -10,24 +10,26 @@
 //     two bfloat16 values is exact in float32, so every step rounds once), the
 //     bias added last.  Token rows and weights (a float32 copy made by the
 //     set-up kernel) stream through LDS.  log f = -softplus(-a) in float64, rounded once.
-//   * c: a float64 scan of the block's 64 gates per head, then a chained scan
-//     across the blocks of the sequence (decoupled look-back): each wave first
-//     publishes its block total, then walks back over earlier blocks, adding
-//     their totals until it meets one whose inclusive prefix is published, and
-//     publishes its own.  The whole wave walks: 64 earlier blocks per round.  Whenever the partial sums span at most 53 bits every
-//     float64 sum here is exact, so c = float32(prefix) equals the sequential
-//     definition bit for bit whatever the association (the span is checked
-//     from the statistics below, as stage 1 does).
-//   * Per-block statistics for stage 1's checks: the float64 sum of |log f|,
+//   * c: a double-double scan of the block's 64 gates per head, then a chained
+//     scan across the blocks of the sequence (decoupled look-back): each wave
+//     first publishes its block total, then walks back over earlier blocks,
+//     adding their totals until it meets one whose inclusive prefix is
+//     published, and publishes its own.  The whole wave walks: 64 earlier
+//     blocks per round.  Whenever the partial sums span at most 105 bits every
+//     double-double sum here is exact, so c, the float32 rounding of the pair,
+//     is that of the exact prefix sum whatever the association (the span is
+//     checked from the statistics below, as stage 1 does).
+//   * Per-block statistics for stage 1's checks: the sum of |log f| (a pair),
 //     the smallest float32 ulp exponent, and flags (a non-finite gate, a
 //     time-out below), written by each block to a slot of its own (stage 1
 //     reduces them; same-address atomics from every block of a sequence would
 //     serialise).
-// Descriptors hold raw float64 bits; a signalling-NaN pattern that no
-// arithmetic produces marks "not published yet" (gate_init_kernel sets it
-// before every call).  Publication is a single
-// agent-scope 64-bit store and the look-back an agent-scope load of it, so no
-// fence is needed (the value is the message).  Blocks of one sequence wait
+// A descriptor is a pair of words holding the raw float64 bits of hi and lo; a
+// signalling-NaN pattern that no arithmetic produces marks a word "not
+// published yet" (gate_init_kernel sets it before every call).  Each word is
+// published by an agent-scope 64-bit store and read by an agent-scope load, and
+// a reader takes a descriptor only once both words are published, so no fence
+// is needed (the values are the message).  Blocks of one sequence wait
 // only on blocks with lower workgroup ids, which were dispatched before them;
 // the wait is bounded all the same, and on a time-out the wave sets flag bit 5
 // and goes on, so every wave ends.
@@ -44,12 +46,12 @@ __device__ __forceinline__ float bf16_bits_to_f32(unsigned short b) {
     return __uint_as_float((unsigned)b << 16);
 }
 
-// Set-up before every call: descriptors unpublished, and the weights as float32 in [group of 4 heads][feature][4] order (heads past H
+// Set-up before every call: descriptor words unpublished, and the weights as float32 in [group of 4 heads][feature][4] order (heads past H
 // zero), so that the producer reads a group's four weights of a feature as one
 // uniform 16-byte load.
 __global__ __launch_bounds__(256) void gate_init_kernel(unsigned long long* __restrict__ agg,
                                                         unsigned long long* __restrict__ incl,
-                                                        int ndesc,
+                                                        int nwords,
                                                         const unsigned short* __restrict__ W,
                                                         float4* __restrict__ wq, int Dm, int H,
                                                         int nquad) {
@@ -64,18 +66,24 @@ __global__ __launch_bounds__(256) void gate_init_kernel(unsigned long long* __re
         if (h0 + 3 < H) v.w = bf16_bits_to_f32(wr[3]);
         wq[i] = v;
     }
-    if (i < ndesc) {
+    if (i < nwords) {
         agg[i] = kUnpublished;
         incl[i] = kUnpublished;
     }
 
 }
 
-// Sum over the 64 lanes (the float64 sums here are exact, so the association
-// does not matter)
-__device__ __forceinline__ double wave_reduce_sum_f64(double v) {
-    const double r = row16_reduce(v, [](double a, double b) { return a + b; });
-    return (readlane_f64(r, 0) + readlane_f64(r, 16)) + (readlane_f64(r, 32) + readlane_f64(r, 48));
+__device__ __forceinline__ void publish(unsigned long long* w, DD v) {
+    __hip_atomic_store(w, (unsigned long long)__double_as_longlong(v.hi), __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(w + 1, (unsigned long long)__double_as_longlong(v.lo), __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ unsigned long long peek(const unsigned long long* w) {
+    return __hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ double bits_f64(unsigned long long b) {
+    return __longlong_as_double((long long)b);
 }
 
 // A workgroup of 4 waves takes one (sequence b, 64-token block) for every head:
@@ -199,13 +207,13 @@ __global__ __launch_bounds__(kGateThreads) void gate_kernel(
 #pragma unroll
         for (int j = 0; j < 4; ++j)
             a4[j] = r == 0 ? acc[0][j] : r == 1 ? acc[1][j] : r == 2 ? acc[2][j] : acc[3][j];
-        double excl_mine = 0.0;   // lane j < nh: exclusive prefix of head h0 + j
-        double abs_mine = 0.0;    // lane j < nh: the block's statistics of head h0 + j
+        DD excl_mine{0.0, 0.0};   // lane j < nh: exclusive prefix of head h0 + j
+        DD abs_mine{0.0, 0.0};    // lane j < nh: the block's statistics of head h0 + j
         int lsb_mine = 1 << 30, flags_mine = 0;
-        double scan[4];
+        DD scan[4];
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            scan[j] = 0.0;
+            scan[j] = DD{0.0, 0.0};
             if (j >= nh) continue;
             const double a = (double)(a4[j] + bias[h0 + j]);
             const double sp = fmax(-a, 0.0) + log1p(exp(-fabs(a)));   // softplus(-a)
@@ -215,33 +223,28 @@ __global__ __launch_bounds__(kGateThreads) void gate_kernel(
             // statistics for stage 1's checks
             const bool bad = !__builtin_isfinite(lf32);
             const int lsb = bad || lf32 == 0.f ? (1 << 30) : lsb_exp(lf32);
-            double sabs = bad ? 0.0 : __builtin_fabs((double)lf32);
+            const DD sabs = wave_sum_dd(DD{bad ? 0.0 : __builtin_fabs((double)lf32), 0.0});
             int slsb = lsb;
 #pragma unroll
-            for (int off = 32; off >= 1; off >>= 1) {
-                sabs += __shfl_xor(sabs, off);
-                slsb = min(slsb, __shfl_xor(slsb, off));
-            }
+            for (int off = 32; off >= 1; off >>= 1) slsb = min(slsb, __shfl_xor(slsb, off));
             const bool anybad = __ballot(bad) != 0ull;
             if (lane == j) {
                 abs_mine = sabs;
                 lsb_mine = slsb;
                 flags_mine = anybad ? 2 : 0;
             }
-            scan[j] = wave_inclusive_scan_f64(bad ? 0.0 : (double)lf32);
+            scan[j] = wave_inclusive_scan_dd(DD{bad ? 0.0 : (double)lf32, 0.0});
         }
         // block totals (lane j holds head h0 + j's), published before the look-back
-        double total = 0.0;
+        DD total{0.0, 0.0};
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            const double tj = readlane_f64(scan[j], 63);
+            const DD tj = readlane_dd(scan[j], 63);
             if (lane == j) total = tj;
         }
         if (lane < nh) {
             const size_t d = ((size_t)b * H + h0 + lane) * nblk + blk;
-            const unsigned long long bits = (unsigned long long)__double_as_longlong(total);
-            if (blk == 0) __hip_atomic_store(&incl[d], bits, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            else __hip_atomic_store(&agg[d], bits, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            publish((blk == 0 ? incl : agg) + 2 * d, total);
         }
         // Look-back, one head at a time with the whole wave: lane l reads block
         // i0 - l's descriptors, 64 blocks per round.  The nearest block with its
@@ -251,28 +254,32 @@ __global__ __launch_bounds__(kGateThreads) void gate_kernel(
         for (int j = 0; j < nh; ++j) {
             if (blk == 0) break;
             const size_t d0 = ((size_t)b * H + h0 + j) * nblk;
-            double run = 0.0;
+            DD run{0.0, 0.0};
             int i0 = blk - 1, spins = 0;
             bool timed_out = false;
             while (i0 >= 0) {
                 const int i = i0 - lane;
-                unsigned long long p = kUnpublished, qq = kUnpublished;
+                unsigned long long p = kUnpublished, pl = kUnpublished;
+                unsigned long long qq = kUnpublished, ql = kUnpublished;
                 if (i >= 0) {
-                    p = __hip_atomic_load(&incl[d0 + i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    qq = __hip_atomic_load(&agg[d0 + i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    const size_t w2 = 2 * (d0 + i);
+                    p = peek(&incl[w2]);
+                    pl = peek(&incl[w2 + 1]);
+                    qq = peek(&agg[w2]);
+                    ql = peek(&agg[w2 + 1]);
                 }
                 // lanes whose block lies before the sequence count as published zeros
-                const bool has_p = i >= 0 && p != kUnpublished;
-                const bool has_q = i < 0 || qq != kUnpublished || has_p;
+                const bool has_p = i >= 0 && p != kUnpublished && pl != kUnpublished;
+                const bool has_q = i < 0 || (qq != kUnpublished && ql != kUnpublished) || has_p;
                 const unsigned long long pm = __ballot(has_p);
                 const int stop = pm ? __builtin_ctzll(pm) : 64;      // nearest prefix
                 const unsigned long long need = stop == 64 ? ~0ull : ((1ull << stop) - 1ull);
                 const unsigned long long qm = __ballot(has_q);
                 if ((qm & need) == need) {
-                    double v = 0.0;
-                    if (lane < stop && i >= 0) v = __longlong_as_double((long long)qq);
-                    if (lane == stop) v = __longlong_as_double((long long)p);
-                    run += wave_reduce_sum_f64(v);
+                    DD v{0.0, 0.0};
+                    if (lane < stop && i >= 0) v = DD{bits_f64(qq), bits_f64(ql)};
+                    if (lane == stop) v = DD{bits_f64(p), bits_f64(pl)};
+                    run = dd_add(run, wave_sum_dd(v));
                     if (stop < 64) break;
                     i0 -= 64;
                     spins = 0;
@@ -287,13 +294,13 @@ __global__ __launch_bounds__(kGateThreads) void gate_kernel(
             if (lane == j) {
                 excl_mine = run;
                 if (timed_out) flags_mine |= 32;
-                const unsigned long long ib = (unsigned long long)__double_as_longlong(run + total);
-                __hip_atomic_store(&incl[d0 + blk], ib, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                publish(&incl[2 * (d0 + blk)], dd_add(run, total));
             }
         }
         if (lane < nh) {
             GateStats g;
-            g.abs_sum = abs_mine;
+            g.abs_sum = abs_mine.hi;
+            g.abs_lo = abs_mine.lo;
             g.min_lsb = lsb_mine;
             g.flags = flags_mine;
             st[((size_t)b * H + h0 + lane) * nblk + blk] = g;
@@ -302,8 +309,8 @@ __global__ __launch_bounds__(kGateThreads) void gate_kernel(
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             if (j >= nh) continue;
-            const double ex = readlane_f64(excl_mine, j);
-            c[((size_t)b * H + h0 + j) * L + tok] = (float)(ex + scan[j]);
+            const DD ex = readlane_dd(excl_mine, j);
+            c[((size_t)b * H + h0 + j) * L + tok] = dd_to_f32(dd_add(ex, scan[j]));
         }
     }
 }
@@ -312,9 +319,9 @@ hipError_t launch_gate(const GateArgs& a, hipStream_t s) {
     const int nblk = a.L / 64, nquad = (a.H + 3) / 4;
     const int ndesc = a.B * a.H * nblk;
     trace_begin(ACP_K_GATE, s);
-    const int ninit = max(ndesc, nquad * a.Dm);
+    const int ninit = max(2 * ndesc, nquad * a.Dm);
     hipLaunchKernelGGL(gate_init_kernel, dim3((ninit + 255) / 256), dim3(256), 0, s,
-                       a.agg, a.incl, ndesc, (const unsigned short*)a.W,
+                       a.agg, a.incl, 2 * ndesc, (const unsigned short*)a.W,
                        (float4*)a.wq, a.Dm, a.H, nquad);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;

@@ -12,7 +12,8 @@ namespace acp {
 // Per-block statistics of the gate producer (one entry per 64 gates of a head)
 // that stage 1's checks need in place of its own pass over log f.
 struct GateStats {
-    double abs_sum;           // float64 sum of |log f|
+    double abs_sum;           // sum of |log f| as a double-double pair (abs_sum, abs_lo)
+    double abs_lo;
     int min_lsb;              // smallest float32 ulp exponent of a nonzero gate
     int flags;                // bit 1: a non-finite gate; bit 5: the chained scan timed out
 };
@@ -47,8 +48,8 @@ struct GateArgs {
     int B, L, Dm, H;
     float* log_f;             // [B*H, L]
     float* c;                 // [B*H, L]
-    unsigned long long* agg;  // [B*H, L/64] block totals (float64 bits)
-    unsigned long long* incl; // [B*H, L/64] inclusive prefixes (float64 bits)
+    unsigned long long* agg;  // [B*H, L/64, 2] block totals (float64 bits of hi, lo)
+    unsigned long long* incl; // [B*H, L/64, 2] inclusive prefixes (float64 bits of hi, lo)
     GateStats* stats;         // [B*H, L/64]
     void* wq;                 // [ceil(H/4), Dm] float4: the weights by group of 4 heads
 };
@@ -114,7 +115,7 @@ struct DecodeInitArgs {
     void* Kc;                 // [B*H, C, d] ring caches, position j in slot j mod C
     void* Vc;
     float* cc;                // [B*H, C] c of the cached positions
-    double* cs;               // [2][B*H] float64 running sum of log f (copy p mod 2
+    double* cs;               // [2][B*H][2] running sum of log f, (hi, lo) (copy p mod 2
                               // holds the value after position p)
     int* ptr;                 // [2][B*H] first kept block of query p, likewise
     double* delta;            // [B*H]

@@ -126,7 +126,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
     double* __restrict__ u_out, double* __restrict__ delta_out,
     int* __restrict__ row_start, int* __restrict__ col_end,
     long long* __restrict__ kept_out, int* __restrict__ flags_out) {
-    __shared__ double s_sum[kPlanWaves], s_abs[kPlanWaves], s_mq[kPlanWaves], s_mk[kPlanWaves];
+    __shared__ double s_sum[2][kPlanWaves], s_abs[2][kPlanWaves], s_mq[kPlanWaves], s_mk[kPlanWaves];
     __shared__ int s_lsb[kPlanWaves], s_flg[kPlanWaves];
     __shared__ float s_first[kMaxBlocks];  // c at the first row of each block
     __shared__ float s_last[kMaxBlocks];   // c at the last row of each block
@@ -164,8 +164,8 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
         }
     }
 
-    // ---- this thread's sums and checks --------------------------------------------
-    double local = 0.0, local_abs = 0.0;
+    // ---- this thread's sums and checks (double-double: exact up to a 105-bit span)
+    DD local{0.0, 0.0}, local_abs{0.0, 0.0};
     int min_lsb = 1 << 30;
     bool positive = false, nonfinite = false;
     auto take = [&](float v) __attribute__((always_inline)) {
@@ -174,8 +174,8 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
             if (v > 0.0f) positive = true;
             if (v != 0.0f) min_lsb = min(min_lsb, lsb_exp(v));
         }
-        local += (double)v;
-        local_abs += __builtin_fabs((double)v);
+        local = dd_add(local, (double)v);
+        local_abs = dd_add(local_abs, __builtin_fabs((double)v));
     };
     int gate_flags = 0;
     if (gated) {
@@ -184,7 +184,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
         const int M0 = L / kBlock;
         for (int m = t; m < M0; m += kPlanThreads) {
             const GateStats g = gate[(size_t)bh * M0 + m];
-            local_abs += g.abs_sum;
+            local_abs = dd_add(local_abs, DD{g.abs_sum, g.abs_lo});
             min_lsb = min(min_lsb, g.min_lsb);
             gate_flags |= g.flags;
         }
@@ -199,12 +199,9 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
     // ---- one round through LDS --------------------------------------------------------
     // (cross-lane steps by DPP within rows of 16, then the four rows' results by
     // readlane: lane 0 writes the wave's entries)
-    const double incl = wave_inclusive_scan_f64(local);
+    const DD incl = wave_inclusive_scan_dd(local);
     {
-        const auto add = [](double a, double b) { return a + b; };
-        const double ra = row16_reduce(local_abs, add);
-        local_abs = ((readlane_f64(ra, 0) + readlane_f64(ra, 16)) + readlane_f64(ra, 32)) +
-                    readlane_f64(ra, 48);
+        local_abs = wave_sum_dd(local_abs);
         const int rl = row16_reduce(min_lsb, [](int a, int b) { return min(a, b); });
         min_lsb = min(min(__builtin_amdgcn_readlane(rl, 0), __builtin_amdgcn_readlane(rl, 16)),
                       min(__builtin_amdgcn_readlane(rl, 32), __builtin_amdgcn_readlane(rl, 48)));
@@ -220,9 +217,13 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
         mk = nan_max(nan_max(readlane_f64(rk, 0), readlane_f64(rk, 16)),
                      nan_max(readlane_f64(rk, 32), readlane_f64(rk, 48)));
     }
-    if (lane == 63) s_sum[wid] = incl;
+    if (lane == 63) {
+        s_sum[0][wid] = incl.hi;
+        s_sum[1][wid] = incl.lo;
+    }
     if (lane == 0) {
-        s_abs[wid] = local_abs;
+        s_abs[0][wid] = local_abs.hi;
+        s_abs[1][wid] = local_abs.lo;
         s_lsb[wid] = min_lsb;
         s_flg[wid] = wflags;
         s_mq[wid] = mq;
@@ -231,22 +232,22 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
     lds_barrier();
     // Every wave combines the 16 waves' entries itself, lane l < 16 taking wave l's
     // (one LDS read per quantity, then a reduction over the row of 16 lanes; row 0
-    // is read out).  The float64 sums are exact whenever the span check passes, so
-    // their association does not matter.
-    double before, total_abs;
+    // is read out).  The double-double sums are exact whenever the span check
+    // passes, so their association does not matter.
+    DD before, total_abs;
     int flags;
     {
         const bool in = lane < kPlanWaves;
         const int l = in ? lane : 0;
-        const auto add = [](double a, double b) { return a + b; };
-        double vs = in && lane < wid ? s_sum[l] : 0.0;
-        double va = in ? s_abs[l] : 0.0;
+        const bool lower = in && lane < wid;
+        DD vs{lower ? s_sum[0][l] : 0.0, lower ? s_sum[1][l] : 0.0};
+        DD va{in ? s_abs[0][l] : 0.0, in ? s_abs[1][l] : 0.0};
         int vl = in ? s_lsb[l] : (1 << 30);
         int vf = in ? s_flg[l] : 0;
         double vq = in ? s_mq[l] : 0.0;   // squared norms are >= 0; a NaN wins nan_max
         double vk = in ? s_mk[l] : 0.0;
-        vs = row16_reduce(vs, add);
-        va = row16_reduce(va, add);
+        vs = row16_sum_dd(vs);
+        va = row16_sum_dd(va);
         vl = row16_reduce(vl, [](int a, int b) { return min(a, b); });
         vf = row16_reduce(vf, [](int a, int b) { return a | b; });
         vq = row16_reduce(vq, [](double a, double b) { return nan_max(a, b); });
@@ -257,24 +258,22 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
             const unsigned hi = (unsigned)__builtin_amdgcn_readfirstlane((int)(unsigned)(b >> 32));
             return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
         };
-        before = first(vs);
-        total_abs = first(va);
+        before = DD{first(vs.hi), first(vs.lo)};
+        total_abs = DD{first(va.hi), first(va.lo)};
         min_lsb = __builtin_amdgcn_readfirstlane(vl);
         flags = __builtin_amdgcn_readfirstlane(vf);
         mq = first(vq);
         mk = first(vk);
     }
-    if (total_abs > 0.0) {
+    if (total_abs.hi > 0.0) {
         // Every partial sum is a multiple of 2^min_lsb and below 2^E, the least
-        // power of two above sum |log f| (E = ilogb + 1).  Flag from E - lsb = 53
-        // on: up to 53 bits total_abs itself is exact, so E is right; beyond, its
-        // rounding can lose one power of two, and 54 bits would read as 53.
-        const int biased = (int)((__double_as_longlong(total_abs) >> 52) & 0x7ff);
-        const int top = (biased > 0 ? biased : 1) - 1023 + 1;
-        if (top - min_lsb >= 53) flags |= 4;
+        // power of two above sum |log f|.  Flag from E - lsb = 105 on: up to 105
+        // bits total_abs itself is exact, so E is right; beyond, its rounding can
+        // lose one power of two, and 106 bits would read as 105.
+        if (dd_top_exp(total_abs) - min_lsb >= kExactSpanBits) flags |= 4;
         // c leaves the float32 range (|c| <= sum |log f|, reached at the end when
         // no gate is positive)
-        if (!__builtin_isfinite((float)total_abs)) flags |= 2;
+        if (__builtin_isinf(dd_to_f32(total_abs))) flags |= 2;
     }
 
     // ---- U and delta ---------------------------------------------------------------------
@@ -302,7 +301,9 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
     }
 
     // ---- c = cumsum(log f) and the block corners ----------------------------------------
-    double run = before + (incl - local);   // exclusive prefix: exact when the span check passes
+    // exclusive prefix (exact when the span check passes), then c = float32 of the
+    // running pair
+    DD run = dd_add(before, dd_add(incl, dd_neg(local)));
     auto corner = [&](int j, float cf) __attribute__((always_inline)) {
         if ((j & (kBlock - 1)) == 0) s_first[j / kBlock] = cf;
         if ((j & (kBlock - 1)) == kBlock - 1) s_last[j / kBlock] = cf;
@@ -317,10 +318,10 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
         for (int i = 0; i < kPlanHeld; i += 4) {
             if (i < n) {
                 float4 cv;
-                run += (double)xv[i];     cv.x = (float)run;
-                run += (double)xv[i + 1]; cv.y = (float)run;
-                run += (double)xv[i + 2]; cv.z = (float)run;
-                run += (double)xv[i + 3]; cv.w = (float)run;
+                run = dd_add(run, (double)xv[i]);     cv.x = dd_to_f32(run);
+                run = dd_add(run, (double)xv[i + 1]); cv.y = dd_to_f32(run);
+                run = dd_add(run, (double)xv[i + 2]); cv.z = dd_to_f32(run);
+                run = dd_add(run, (double)xv[i + 3]); cv.w = dd_to_f32(run);
                 *reinterpret_cast<float4*>(cw + beg + i) = cv;
                 corner(beg + i, cv.x);            // beg + i is a multiple of 4
                 corner(beg + i + 3, cv.w);
@@ -330,16 +331,16 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
 #pragma unroll
         for (int i = 0; i < kPlanHeld; ++i) {
             if (i < n) {
-                run += (double)xv[i];
-                const float cf = (float)run;
+                run = dd_add(run, (double)xv[i]);
+                const float cf = dd_to_f32(run);
                 cw[beg + i] = cf;
                 corner(beg + i, cf);
             }
         }
     } else {
         for (int i = 0; i < n; ++i) {
-            run += (double)x[beg + i];
-            const float cf = (float)run;
+            run = dd_add(run, (double)x[beg + i]);
+            const float cf = dd_to_f32(run);
             cw[beg + i] = cf;
             corner(beg + i, cf);
         }

@@ -110,7 +110,7 @@ def test_boundary_flags_bad_gates():
     lf = x["log_f"].clone()
     lf[0, 1, 17] = 0.25           # f > 1
     lf[0, 2, 100] = float("nan")
-    lf[0, 3, 0] = -1e-30          # tiny gate next to ordinary ones: sums not exact
+    lf[0, 3, 0] = -1e-30          # tiny gate next to ordinary ones: a span beyond 105 bits
     x["log_f"] = lf
     got = _gpu_plan(x, EPS)
     assert got["flags"][0, 0] == 0
@@ -118,33 +118,41 @@ def test_boundary_flags_bad_gates():
     assert got["flags"][0, 2] & acp.FLAG_NONFINITE_GATE
     assert got["flags"][0, 3] & acp.FLAG_INEXACT_CUMSUM
     # span check agrees with the oracle's own bound
-    assert orc.cumsum_span_bits(lf[0, 3].numpy()) > 53
-    assert orc.cumsum_span_bits(lf[0, 0].numpy()) <= 52
+    assert orc.cumsum_span_bits(lf[0, 3].numpy()) >= 105
+    assert orc.cumsum_span_bits(lf[0, 0].numpy()) < 105
 
 
-def test_inexact_cumsum_flag_at_53_bits_and_c_overflow():
+SPANS = (52, 53, 54, 104, 105, 106)
+
+
+def test_inexact_cumsum_flag_at_105_bits_and_c_overflow():
     """Flag bit 2 against the oracle's rule on hand-built gates whose partial sums
-    span 52, 53 and 54 bits (63 gates of -6 and one full-significand gate of ulp
-    2^(E - span)); c bit-identical where the span keeps it exact.  A fourth head
-    whose cumulative sum leaves the float32 range (finite gates of -3e38) carries
-    flag bit 1."""
-    w = workloads.custom("span", 1, 4, 64, 64, "f32", 8, mu=(2.0,))
+    span 52, 53, 54, 104, 105 and 106 bits (63 gates of -6 and one full-significand
+    gate of ulp 2^(E - span)); c bit-identical to the rounded exact sum wherever
+    the flag is clear, also past the 53 bits a float64 sum holds.  A head whose
+    cumulative sum leaves the float32 range (finite gates of -3e38) carries flag
+    bit 1."""
+    H = len(SPANS) + 2
+    w = workloads.custom("span", 1, H, 64, 64, "f32", 8, mu=(2.0,))
     x = workloads.generate(w, with_grad=False)
-    lf = torch.full((1, 4, 64), -6.0, dtype=torch.float32)
-    for h, span in enumerate((52, 53, 54)):
+    lf = torch.full((1, H, 64), -6.0, dtype=torch.float32)
+    for h, span in enumerate(SPANS):
         lf[0, h, -1] = -(1.0 + 2.0 ** -23) * 2.0 ** (9 + 23 - span)
         assert orc.cumsum_span_bits(lf[0, h].numpy()) == span
-    lf[0, 3, :2] = -3.0e38
+    lf[0, H - 2, :2] = -3.0e38
     x["log_f"] = lf
-    print("case: span flags 52/53/54, c overflow", flush=True)
+    print("case: span flags " + "/".join(map(str, SPANS)) + ", c overflow", flush=True)
     got = _gpu_plan(x, EPS)
-    for h in range(3):
+    for h, span in enumerate(SPANS):
         want = acp.FLAG_INEXACT_CUMSUM if orc.cumsum_inexact_flag(lf[0, h].numpy()) else 0
+        assert want == (acp.FLAG_INEXACT_CUMSUM if span >= 105 else 0)
         assert got["flags"][0, h] == want, (h, got["flags"][0, h])
         if not want:
             np.testing.assert_array_equal(got["c"][0, h], orc.cumsum_log_gates(lf[0, h].numpy()))
-    assert got["flags"][0, 3] & acp.FLAG_NONFINITE_GATE
-    assert not np.all(np.isfinite(orc.cumsum_log_gates(lf[0, 3].numpy())))
+            np.testing.assert_array_equal(got["c"][0, h], orc.cumsum_exact_fraction(lf[0, h].numpy()))
+    assert got["flags"][0, H - 2] & acp.FLAG_NONFINITE_GATE
+    assert not np.all(np.isfinite(orc.cumsum_log_gates(lf[0, H - 2].numpy())))
+    assert got["flags"][0, H - 1] == 0
 
 
 def test_boundary_is_deterministic():
@@ -156,14 +164,51 @@ def test_boundary_is_deterministic():
         np.testing.assert_array_equal(a[n], b[n])
 
 
-def test_wide_gate_spreads_flag_inexact_sums():
+def test_wide_gate_spreads_stay_exact():
     """Gates with a wide spread (logits N(mu, 3): log f from about -15 to -1e-17 in
-    one head) give cumulative sums spanning more than 53 bits on many heads.  Flag
-    bit 2 must be set exactly on those (the device rule: from 53 bits on); their c
-    stays within one float32 ulp of the sequential float64 definition, U and delta
-    stay exact, and every other head is bit-exact throughout."""
+    one head) give cumulative sums spanning more than the 53 bits of a float64 on
+    many heads, and less than 105 on all.  No flag may be raised, and c, U, delta
+    and the boundary must be bit-exact on every head: c is the float32 rounding of
+    the exact prefix sum."""
     w = workloads.custom("wide", 2, 8, 4096, 64, "bf16", 91,
                          mu=(-2.0, 0.0, 3.0, 6.0, 10.0, 15.0, 20.0, 28.0), gate_sigma=3.0)
+    print(f"case: boundary {w.describe()}", flush=True)
+    x = workloads.generate(w, with_grad=False)
+    got = _gpu_plan(x, w.eps)
+    lf = x["log_f"].numpy()
+    c_ref = orc.cumsum_log_gates(lf)
+    wide = narrow = 0
+    for b in range(w.B):
+        for h in range(w.H):
+            q = x["q"][b, h].float().numpy()
+            k = x["k"][b, h].float().numpy()
+            U = orc.logit_bound(orc.row_norm_sq_max(q), orc.row_norm_sq_max(k), w.d)
+            delta = orc.threshold(U, w.L, w.eps)
+            assert got["bound_u"][b, h] == U and got["delta"][b, h] == delta, (b, h)
+            span = orc.cumsum_span_bits(lf[b, h])
+            fl = int(got["flags"][b, h])
+            assert span < 105 and fl == 0, (b, h, span, fl)
+            if span > 53:
+                wide += 1
+            else:
+                narrow += 1
+            np.testing.assert_array_equal(got["c"][b, h], c_ref[b, h])
+            rs, ce = orc.boundary_from_block_keep(orc.block_keep_topright(c_ref[b, h], delta))
+            np.testing.assert_array_equal(got["row_start"][b, h], rs)
+            np.testing.assert_array_equal(got["col_end"][b, h], ce)
+            assert got["kept"][b, h] == orc.kept_tiles(rs)
+    print(f"  {wide} heads spanning more than 53 bits, {narrow} within 53", flush=True)
+    assert wide > 0 and narrow > 0
+
+
+def test_gate_spreads_near_105_bits():
+    """Logits N(mu, 8) spread the gates of a head over 2^60 and more, so that the
+    spans of the cumulative sums straddle 105 bits (84 to 108 here).  Flag bit 2
+    must be set exactly from 105 bits on; below, c and the boundary are bit-exact
+    (the float32 rounding of the exact sum); flagged heads keep c within one
+    float32 ulp of it, and U and delta stay exact everywhere."""
+    w = workloads.custom("wider", 2, 8, 4096, 64, "bf16", 93,
+                         mu=(0.0, 5.0, 10.0, 15.0, 20.0, 25.0, 30.0, 35.0), gate_sigma=8.0)
     print(f"case: boundary {w.describe()}", flush=True)
     x = workloads.generate(w, with_grad=False)
     got = _gpu_plan(x, w.eps)
@@ -179,8 +224,8 @@ def test_wide_gate_spreads_flag_inexact_sums():
             assert got["bound_u"][b, h] == U and got["delta"][b, h] == delta, (b, h)
             span = orc.cumsum_span_bits(lf[b, h])
             fl = int(got["flags"][b, h])
-            assert bool(fl & 4) == (span >= 53) and fl & ~4 == 0, (b, h, span, fl)
-            if span >= 53:
+            assert fl == (acp.FLAG_INEXACT_CUMSUM if span >= 105 else 0), (b, h, span, fl)
+            if fl:
                 flagged += 1
                 ulp = np.spacing(np.abs(c_ref[b, h]).astype(np.float32))
                 assert np.all(np.abs(got["c"][b, h] - c_ref[b, h]) <= ulp), (b, h)
@@ -190,6 +235,5 @@ def test_wide_gate_spreads_flag_inexact_sums():
             rs, ce = orc.boundary_from_block_keep(orc.block_keep_topright(c_ref[b, h], delta))
             np.testing.assert_array_equal(got["row_start"][b, h], rs)
             np.testing.assert_array_equal(got["col_end"][b, h], ce)
-            assert got["kept"][b, h] == orc.kept_tiles(rs)
-    print(f"  {flagged} heads flagged inexact, {exact} exact", flush=True)
+    print(f"  {flagged} heads flagged, {exact} exact", flush=True)
     assert flagged > 0 and exact > 0

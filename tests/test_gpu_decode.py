@@ -4,6 +4,7 @@ oracle's single-row decoding, with the threshold sized for L_max and the bound
 from QK-norm scales; a ring cache too small for the kept window must report it
 and attend to what it still holds."""
 import math
+from fractions import Fraction
 
 import numpy as np
 import pytest
@@ -88,7 +89,10 @@ def _check(w, L0, C, eps, L_max, expect_lost=None):
             T = w.L
             for pos in range(max(0, T - C), T):
                 assert float(fin["c"][b, h, pos % C]) == float(c_ref[b, h, pos])
-            assert np.float32(float(fin["cum_now"][b, h])) == c_ref[b, h, T - 1]
+            # the pair is the exact sum, its leading part that sum's float64 rounding
+            hi, lo = (float(v) for v in fin["cum_now"][b, h])
+            exact = sum(Fraction(float(v)) for v in x["log_f"][b, h, :T].numpy())
+            assert Fraction(hi) + Fraction(lo) == exact and hi == float(exact), (b, h)
             kc = fin["k_cache"][b, h]
             pos = T - 1
             assert torch.equal(kc[pos % C], x["k"][b, h, pos])

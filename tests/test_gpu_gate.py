@@ -77,3 +77,39 @@ def test_gate_projection_flags_a_nan_input():
     flags = acp.plan_views(ws, B, H, L, d, torch.bfloat16)["flags"].cpu().numpy()
     assert np.all(flags[0] & acp.FLAG_NONFINITE_GATE)
     assert np.all(flags[1] == 0)
+
+
+def test_gate_projection_wide_spans():
+    """Gate weights scaled up 12-fold spread each head's logits over about N(mu, 8),
+    so that the chained scan adds gates 2^60 apart and more: spans of 60 to past
+    105 bits.  log f stays bit-identical; flag bit 2 is set exactly from 105 bits
+    on; below, c is bit-identical to the rounded exact sum, and the gated plan
+    matches stage 1 scanning the same log f (c, flags and boundary)."""
+    B, L, Dm, H, d = 2, 4096, 1024, 8, 64
+    p = workloads.gate_inputs(B, L, Dm, H, 87, mu=(0.0, 5.0, 10.0, 15.0, 20.0, 25.0, 30.0, 35.0))
+    p["w_f"] = (p["w_f"].float() * 12.0).bfloat16()
+    lf_ref = orc.gate_log_forget(p["x"].float().numpy(), p["w_f"].float().numpy(),
+                                 p["b_f"].numpy(), B)
+    c_ref = orc.cumsum_log_gates(lf_ref)
+    spans = np.array([[orc.cumsum_span_bits(lf_ref[b, h]) for h in range(H)] for b in range(B)])
+    print(f"case: gate projection, wide spans {spans.min()}..{spans.max()}", flush=True)
+    dev = torch.device("cuda:0")
+    g = {n: t.to(dev) for n, t in p.items()}
+    a = to_gpu(workloads.generate(workloads.custom("gatewide", B, H, L, d, "bf16", 87),
+                                  with_grad=False))
+    lf, ws = acp.gate_project(g["x"], g["w_f"], g["b_f"], B, H, d)
+    acp.forward_gated(a["q"], a["k"], a["v"], EPS, ws)
+    _, _, ws2 = acp.forward(a["q"], a["k"], a["v"], torch.from_numpy(lf_ref).to(dev), EPS)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(lf.cpu().numpy(), lf_ref)
+    plan_g = {n: t.cpu().numpy() for n, t in _plan(ws, B, H, L, d, torch.bfloat16).items()}
+    plan_s = {n: t.cpu().numpy() for n, t in _plan(ws2, B, H, L, d, torch.bfloat16).items()}
+    flag = np.where(spans >= 105, acp.FLAG_INEXACT_CUMSUM, 0)
+    np.testing.assert_array_equal(plan_g["flags"], flag)
+    np.testing.assert_array_equal(plan_s["flags"], flag)
+    exact = spans < 105
+    assert exact.any() and (spans[exact] > 53).any() and (~exact).any()
+    np.testing.assert_array_equal(plan_g["c"][exact], c_ref[exact])
+    np.testing.assert_array_equal(plan_s["c"][exact], c_ref[exact])
+    for n in ("row_start", "col_end", "kept"):
+        np.testing.assert_array_equal(plan_g[n][exact], plan_s[n][exact])

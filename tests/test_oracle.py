@@ -34,6 +34,21 @@ def test_cumsum_equals_exact_rational(mu):
     np.testing.assert_array_equal(orc.cumsum_log_gates(lf), orc.cumsum_exact_fraction(lf))
 
 
+@pytest.mark.parametrize("seed", [1, 2, 3])
+def test_cumsum_of_wide_rows_is_the_rounded_exact_sum(seed):
+    # strong gates mixed with nearly saturated ones (log f down to about -1e-18):
+    # the partial sums span far more than 53 bits, so float64 running sums round,
+    # yet c is the float32 rounding of the exact sum, whatever the order
+    rng = _rng(seed)
+    a = np.concatenate([3.0 * rng.standard_normal(1500), 40.0 + rng.standard_normal(1500)])
+    rng.shuffle(a)
+    lf = workloads.log_sigmoid_f32(a)
+    assert orc.cumsum_span_bits(lf) > 80
+    c = orc.cumsum_log_gates(lf)
+    np.testing.assert_array_equal(c, orc.cumsum_exact_fraction(lf))
+    np.testing.assert_array_equal(orc.cumsum_log_gates(lf[::-1].copy())[-1], c[-1])
+
+
 def test_cumsum_dyadic_constant_gate_closed_form():
     lam = 2.0 ** -3
     L = 4096
@@ -70,7 +85,7 @@ def _float64_prefix_sums_exact(lf) -> bool:
     return True
 
 
-@pytest.mark.parametrize("span", [52, 53, 54])
+@pytest.mark.parametrize("span", [52, 53, 54, 104, 105, 106])
 def test_cumsum_span_bits_hand_built(span):
     # the count itself (an off-by-one in E or in the ulp exponent fails here)
     lf = _span_gates(span)
@@ -78,8 +93,10 @@ def test_cumsum_span_bits_hand_built(span):
     # what the count promises: up to 53 bits every float64 partial sum is exact;
     # at 54 the last one (bits 2^8 .. 2^-45) is not
     assert _float64_prefix_sums_exact(lf) == (span <= 53)
-    # flag bit 2 is raised from 53 bits on
-    assert orc.cumsum_inexact_flag(lf) == (span >= 53)
+    # c is the rounded exact sum at any span
+    np.testing.assert_array_equal(orc.cumsum_log_gates(lf), orc.cumsum_exact_fraction(lf))
+    # flag bit 2 is raised from 105 bits on (the device's double-double sums)
+    assert orc.cumsum_inexact_flag(lf) == (span >= 105)
 
 
 def test_cumsum_span_bits_power_of_two_total_and_subnormal():
