@@ -76,7 +76,9 @@ __global__ __launch_bounds__(kPlanThreads) void decode_init_kernel(
     const float* x = log_f + (size_t)bh * L0;
     const int per = (L0 + kPlanThreads - 1) / kPlanThreads;
     const int beg = min(t * per, L0), end = min(beg + per, L0);
-    DD local{0.0, 0.0}, local_abs{0.0, 0.0};
+    // float64 first, double-double for a head whose sums span 53 bits or more (the
+    // rule of the plan kernel, which explains it)
+    double local = 0.0, local_abs = 0.0;
     int min_lsb = 1 << 30;
     for (int i = beg; i < end; ++i) {
         const float v = x[i];
@@ -85,31 +87,52 @@ __global__ __launch_bounds__(kPlanThreads) void decode_init_kernel(
             if (v > 0.0f) flags |= 1;
             if (v != 0.0f) min_lsb = min(min_lsb, lsb_exp(v));
         }
-        local = dd_add(local, (double)v);
-        local_abs = dd_add(local_abs, __builtin_fabs((double)v));
+        local += (double)v;
+        local_abs += __builtin_fabs((double)v);
     }
-    const DD incl = block_inclusive_scan_dd(local, s_dbl[0], s_dbl[1]);
-    DD run = dd_add(incl, dd_neg(local));
+    const double incl = block_inclusive_scan(local, s_dbl[0]);
+    auto sum = [](double a, double b) { return a + b; };
     auto imin = [](int a, int b) { return min(a, b); };
     auto ior = [](int a, int b) { return a | b; };
-    const DD total_abs = block_sum_dd(local_abs, s_dbl2[0], s_dbl2[1]);
+    const double total_abs = block_reduce(local_abs, s_dbl2[0], sum);
     min_lsb = block_reduce(min_lsb, s_int, imin);
-    if (t == 0 && total_abs.hi > 0.0) {
-        // the rule of the plan kernel: flagged from a span of 105 bits on
-        if (dd_top_exp(total_abs) - min_lsb >= kExactSpanBits) flags |= 4;
-        if (__builtin_isinf(dd_to_f32(total_abs))) flags |= 2;
+    bool wide = false;   // uniform: every thread holds the same totals
+    if (total_abs > 0.0) {
+        const int biased = (int)((__double_as_longlong(total_abs) >> 52) & 0x7ff);
+        const int top = (biased > 0 ? biased : 1) - 1023 + 1;
+        wide = top - min_lsb >= 53;
     }
-    for (int i = beg; i < end; ++i) {
-        run = dd_add(run, (double)x[i]);
-        const float cf = dd_to_f32(run);
-        if (i >= L0 - C) cc[(size_t)bh * C + (i % C)] = cf;
-        if ((i & (kBlock - 1)) == kBlock - 1) s_last[i / kBlock] = cf;
-        if (i == L0 - 1) {
-            double* cs = cs_out + 2 * ((size_t)((L0 - 1) & 1) * gridDim.x + bh);
-            cs[0] = run.hi;
-            cs[1] = run.lo;
-            s_ct = cf;
+    auto emit = [&](auto run) __attribute__((always_inline)) {
+        for (int i = beg; i < end; ++i) {
+            run = sum_add(run, x[i]);
+            const float cf = sum_f32(run);
+            if (i >= L0 - C) cc[(size_t)bh * C + (i % C)] = cf;
+            if ((i & (kBlock - 1)) == kBlock - 1) s_last[i / kBlock] = cf;
+            if (i == L0 - 1) {
+                double* cs = cs_out + 2 * ((size_t)((L0 - 1) & 1) * gridDim.x + bh);
+                cs[0] = sum_hi(run);
+                cs[1] = sum_lo(run);
+                s_ct = cf;
+            }
         }
+    };
+    if (wide) {
+        DD l{0.0, 0.0}, la{0.0, 0.0};
+        for (int i = beg; i < end; ++i) {
+            const double v = (double)x[i];
+            l = dd_add(l, v);
+            la = dd_add(la, __builtin_fabs(v));
+        }
+        const DD inc = block_inclusive_scan_dd(l, s_dbl[0], s_dbl[1]);
+        const DD total = block_sum_dd(la, s_dbl2[0], s_dbl2[1]);
+        if (t == 0 && total.hi > 0.0) {
+            if (dd_top_exp(total) - min_lsb >= kExactSpanBits) flags |= 4;
+            if (__builtin_isinf(dd_to_f32(total))) flags |= 2;
+        }
+        emit(dd_add(inc, dd_neg(l)));
+    } else {
+        if (t == 0 && total_abs > 0.0 && !__builtin_isfinite((float)total_abs)) flags |= 2;
+        emit(incl - local);
     }
     flags = block_reduce(flags, s_int, ior);   // also orders the LDS writes above
 

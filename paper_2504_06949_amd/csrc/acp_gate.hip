@@ -10,8 +10,9 @@
 //     two bfloat16 values is exact in float32, so every step rounds once), the
 //     bias added last.  Token rows and weights (a float32 copy made by the
 //     set-up kernel) stream through LDS.  log f = -softplus(-a) in float64, rounded once.
-//   * c: a double-double scan of the block's 64 gates per head, then a chained
-//     scan across the blocks of the sequence (decoupled look-back): each wave
+//   * c: a scan of the block's 64 gates per head (float64 while they span under
+//     53 bits, else double-double), then a double-double chained scan across
+//     the blocks of the sequence (decoupled look-back): each wave
 //     first publishes its block total, then walks back over earlier blocks,
 //     adding their totals until it meets one whose inclusive prefix is
 //     published, and publishes its own.  The whole wave walks: 64 earlier
@@ -220,20 +221,35 @@ __global__ __launch_bounds__(kGateThreads) void gate_kernel(
             const float lf32 = (float)(-sp);
             const size_t bh = (size_t)b * H + h0 + j;
             log_f[bh * L + tok] = lf32;
-            // statistics for stage 1's checks
+            // statistics for stage 1's checks, and the block's scan: in float64
+            // while the block's own 64 gates span under 53 bits (then every float64
+            // sum is exact; the read is stage 1's), else in double-double
             const bool bad = !__builtin_isfinite(lf32);
+            const double gv = bad ? 0.0 : (double)lf32;
             const int lsb = bad || lf32 == 0.f ? (1 << 30) : lsb_exp(lf32);
-            const DD sabs = wave_sum_dd(DD{bad ? 0.0 : __builtin_fabs((double)lf32), 0.0});
+            double sabs_f = __builtin_fabs(gv);
             int slsb = lsb;
 #pragma unroll
-            for (int off = 32; off >= 1; off >>= 1) slsb = min(slsb, __shfl_xor(slsb, off));
+            for (int off = 32; off >= 1; off >>= 1) {
+                sabs_f += __shfl_xor(sabs_f, off);
+                slsb = min(slsb, __shfl_xor(slsb, off));
+            }
+            const int biased = (int)((__double_as_longlong(sabs_f) >> 52) & 0x7ff);
+            const bool bwide = __builtin_amdgcn_readfirstlane(
+                sabs_f > 0.0 && (biased > 0 ? biased : 1) - 1023 + 1 - slsb >= 53);
+            DD sabs{sabs_f, 0.0};
+            if (bwide) {
+                sabs = wave_sum_dd(DD{__builtin_fabs(gv), 0.0});
+                scan[j] = wave_inclusive_scan_dd(DD{gv, 0.0});
+            } else {
+                scan[j] = DD{wave_inclusive_scan_f64(gv), 0.0};
+            }
             const bool anybad = __ballot(bad) != 0ull;
             if (lane == j) {
                 abs_mine = sabs;
                 lsb_mine = slsb;
                 flags_mine = anybad ? 2 : 0;
             }
-            scan[j] = wave_inclusive_scan_dd(DD{bad ? 0.0 : (double)lf32, 0.0});
         }
         // block totals (lane j holds head h0 + j's), published before the look-back
         DD total{0.0, 0.0};
@@ -276,6 +292,10 @@ __global__ __launch_bounds__(kGateThreads) void gate_kernel(
                 const unsigned long long need = stop == 64 ? ~0ull : ((1ull << stop) - 1ull);
                 const unsigned long long qm = __ballot(has_q);
                 if ((qm & need) == need) {
+                    if (stop == 0) {   // the previous block's prefix alone: no reduction
+                        run = dd_add(run, DD{readlane_f64(bits_f64(p), 0), readlane_f64(bits_f64(pl), 0)});
+                        break;
+                    }
                     DD v{0.0, 0.0};
                     if (lane < stop && i >= 0) v = DD{bits_f64(qq), bits_f64(ql)};
                     if (lane == stop) v = DD{bits_f64(p), bits_f64(pl)};

@@ -117,6 +117,7 @@ __global__ __launch_bounds__(kNormThreads) void rownorm_max_kernel(
 // the gate flags go through wave ballots, and the norm maxima are reduced only
 // by the waves that hold partials.
 constexpr int kPlanHeld = 16;   // log f values a thread keeps in registers (L <= 16384)
+constexpr int kWideBit = 1 << 16;   // (inside the kernel only) the gated mode needs pairs
 
 __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
     const float* __restrict__ log_f, const double* __restrict__ part, int nchunk,
@@ -126,7 +127,8 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
     double* __restrict__ u_out, double* __restrict__ delta_out,
     int* __restrict__ row_start, int* __restrict__ col_end,
     long long* __restrict__ kept_out, int* __restrict__ flags_out) {
-    __shared__ double s_sum[2][kPlanWaves], s_abs[2][kPlanWaves], s_mq[kPlanWaves], s_mk[kPlanWaves];
+    __shared__ double s_sum[kPlanWaves], s_abs[kPlanWaves], s_mq[kPlanWaves], s_mk[kPlanWaves];
+    __shared__ double s_dsum[2][kPlanWaves], s_dabs[2][kPlanWaves];   // double-double round
     __shared__ int s_lsb[kPlanWaves], s_flg[kPlanWaves];
     __shared__ float s_first[kMaxBlocks];  // c at the first row of each block
     __shared__ float s_last[kMaxBlocks];   // c at the last row of each block
@@ -164,8 +166,11 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
         }
     }
 
-    // ---- this thread's sums and checks (double-double: exact up to a 105-bit span)
-    DD local{0.0, 0.0}, local_abs{0.0, 0.0};
+    // ---- this thread's sums and checks --------------------------------------------
+    // First in float64, which is exact in any association while the partial sums
+    // span at most 53 bits (the read below decides); a head whose sums span more
+    // is summed again in double-double, exact up to 105 bits.
+    double local = 0.0, local_abs = 0.0;
     int min_lsb = 1 << 30;
     bool positive = false, nonfinite = false;
     auto take = [&](float v) __attribute__((always_inline)) {
@@ -174,17 +179,21 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
             if (v > 0.0f) positive = true;
             if (v != 0.0f) min_lsb = min(min_lsb, lsb_exp(v));
         }
-        local = dd_add(local, (double)v);
-        local_abs = dd_add(local_abs, __builtin_fabs((double)v));
+        local += (double)v;
+        local_abs += __builtin_fabs((double)v);
     };
     int gate_flags = 0;
+    DD gate_abs{0.0, 0.0};
+    bool gate_lo = false;   // a block's |log f| sum needed its low part
     if (gated) {
-        // the producer's per-block statistics (sum of |log f|, smallest ulp
-        // exponent, flags) take the place of the gates themselves
+        // the producer's per-block statistics (sum of |log f| as a pair, smallest
+        // ulp exponent, flags) take the place of the gates themselves
         const int M0 = L / kBlock;
         for (int m = t; m < M0; m += kPlanThreads) {
             const GateStats g = gate[(size_t)bh * M0 + m];
-            local_abs = dd_add(local_abs, DD{g.abs_sum, g.abs_lo});
+            local_abs += g.abs_sum;
+            gate_lo = gate_lo || g.abs_lo != 0.0;
+            gate_abs = dd_add(gate_abs, DD{g.abs_sum, g.abs_lo});
             min_lsb = min(min_lsb, g.min_lsb);
             gate_flags |= g.flags;
         }
@@ -199,16 +208,20 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
     // ---- one round through LDS --------------------------------------------------------
     // (cross-lane steps by DPP within rows of 16, then the four rows' results by
     // readlane: lane 0 writes the wave's entries)
-    const DD incl = wave_inclusive_scan_dd(local);
+    const double incl = wave_inclusive_scan_f64(local);
     {
-        local_abs = wave_sum_dd(local_abs);
+        const auto add = [](double a, double b) { return a + b; };
+        const double ra = row16_reduce(local_abs, add);
+        local_abs = ((readlane_f64(ra, 0) + readlane_f64(ra, 16)) + readlane_f64(ra, 32)) +
+                    readlane_f64(ra, 48);
         const int rl = row16_reduce(min_lsb, [](int a, int b) { return min(a, b); });
         min_lsb = min(min(__builtin_amdgcn_readlane(rl, 0), __builtin_amdgcn_readlane(rl, 16)),
                       min(__builtin_amdgcn_readlane(rl, 32), __builtin_amdgcn_readlane(rl, 48)));
     }
     const int wflags = (__ballot(positive) != 0ull ? 1 : 0) |
                        (__ballot(nonfinite || (gate_flags & 2)) != 0ull ? 2 : 0) |
-                       (__ballot(gate_flags & 32) != 0ull ? 32 : 0);
+                       (__ballot(gate_flags & 32) != 0ull ? 32 : 0) |
+                       (__ballot(gate_lo) != 0ull ? kWideBit : 0);
     if (norms && wid * 64 < nchunk) {   // only waves that loaded partials
         const auto mx = [](double a, double b) { return nan_max(a, b); };
         const double rq = row16_reduce(mq, mx), rk = row16_reduce(mk, mx);
@@ -217,13 +230,9 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
         mk = nan_max(nan_max(readlane_f64(rk, 0), readlane_f64(rk, 16)),
                      nan_max(readlane_f64(rk, 32), readlane_f64(rk, 48)));
     }
-    if (lane == 63) {
-        s_sum[0][wid] = incl.hi;
-        s_sum[1][wid] = incl.lo;
-    }
+    if (lane == 63) s_sum[wid] = incl;
     if (lane == 0) {
-        s_abs[0][wid] = local_abs.hi;
-        s_abs[1][wid] = local_abs.lo;
+        s_abs[wid] = local_abs;
         s_lsb[wid] = min_lsb;
         s_flg[wid] = wflags;
         s_mq[wid] = mq;
@@ -232,48 +241,95 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
     lds_barrier();
     // Every wave combines the 16 waves' entries itself, lane l < 16 taking wave l's
     // (one LDS read per quantity, then a reduction over the row of 16 lanes; row 0
-    // is read out).  The double-double sums are exact whenever the span check
-    // passes, so their association does not matter.
-    DD before, total_abs;
+    // is read out).  The float64 sums are exact whenever the span check passes, so
+    // their association does not matter.
+    double before, total_abs;
     int flags;
     {
         const bool in = lane < kPlanWaves;
         const int l = in ? lane : 0;
-        const bool lower = in && lane < wid;
-        DD vs{lower ? s_sum[0][l] : 0.0, lower ? s_sum[1][l] : 0.0};
-        DD va{in ? s_abs[0][l] : 0.0, in ? s_abs[1][l] : 0.0};
+        const auto add = [](double a, double b) { return a + b; };
+        double vs = in && lane < wid ? s_sum[l] : 0.0;
+        double va = in ? s_abs[l] : 0.0;
         int vl = in ? s_lsb[l] : (1 << 30);
         int vf = in ? s_flg[l] : 0;
         double vq = in ? s_mq[l] : 0.0;   // squared norms are >= 0; a NaN wins nan_max
         double vk = in ? s_mk[l] : 0.0;
-        vs = row16_sum_dd(vs);
-        va = row16_sum_dd(va);
+        vs = row16_reduce(vs, add);
+        va = row16_reduce(va, add);
         vl = row16_reduce(vl, [](int a, int b) { return min(a, b); });
         vf = row16_reduce(vf, [](int a, int b) { return a | b; });
         vq = row16_reduce(vq, [](double a, double b) { return nan_max(a, b); });
         vk = row16_reduce(vk, [](double a, double b) { return nan_max(a, b); });
-        auto first = [](double v) {
-            const unsigned long long b = __double_as_longlong(v);
-            const unsigned lo = (unsigned)__builtin_amdgcn_readfirstlane((int)(unsigned)b);
-            const unsigned hi = (unsigned)__builtin_amdgcn_readfirstlane((int)(unsigned)(b >> 32));
-            return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
-        };
-        before = DD{first(vs.hi), first(vs.lo)};
-        total_abs = DD{first(va.hi), first(va.lo)};
+        before = readfirst_f64(vs);
+        total_abs = readfirst_f64(va);
         min_lsb = __builtin_amdgcn_readfirstlane(vl);
         flags = __builtin_amdgcn_readfirstlane(vf);
-        mq = first(vq);
-        mk = first(vk);
+        mq = readfirst_f64(vq);
+        mk = readfirst_f64(vk);
     }
-    if (total_abs.hi > 0.0) {
-        // Every partial sum is a multiple of 2^min_lsb and below 2^E, the least
-        // power of two above sum |log f|.  Flag from E - lsb = 105 on: up to 105
-        // bits total_abs itself is exact, so E is right; beyond, its rounding can
-        // lose one power of two, and 106 bits would read as 105.
-        if (dd_top_exp(total_abs) - min_lsb >= kExactSpanBits) flags |= 4;
-        // c leaves the float32 range (|c| <= sum |log f|, reached at the end when
-        // no gate is positive)
-        if (__builtin_isinf(dd_to_f32(total_abs))) flags |= 2;
+    // ---- the span, and double-double sums where float64 is not enough -------------
+    // Every partial sum is a multiple of 2^min_lsb and below 2^E, the least power
+    // of two above sum |log f|.  Up to 53 bits the float64 total is exact, so E is
+    // right and every float64 sum is exact; beyond, its rounding can lose one power
+    // of two, and 54 bits would read as 53.  So from a read of 53 bits on (or, in
+    // the gated mode, when a block's sum of |log f| has a low part) the head is
+    // summed again in double-double, where the same argument holds up to 105
+    // bits: flag bit 2 from a span of 105 on.  The test is uniform over the
+    // workgroup.
+    bool wide = (flags & kWideBit) != 0;
+    flags &= ~kWideBit;
+    if (total_abs > 0.0) {
+        const int biased = (int)((__double_as_longlong(total_abs) >> 52) & 0x7ff);
+        const int top = (biased > 0 ? biased : 1) - 1023 + 1;
+        wide = wide || top - min_lsb >= 53;
+    }
+    DD run_dd{0.0, 0.0};
+    if (wide) {
+        DD l{0.0, 0.0}, la = gate_abs;
+        if (held) {
+#pragma unroll
+            for (int i = 0; i < kPlanHeld; ++i) {
+                if (i < n) {
+                    l = dd_add(l, (double)xv[i]);
+                    la = dd_add(la, __builtin_fabs((double)xv[i]));
+                }
+            }
+        } else {
+            for (int i = 0; i < n; ++i) {
+                const double v = (double)x[beg + i];
+                l = dd_add(l, v);
+                la = dd_add(la, __builtin_fabs(v));
+            }
+        }
+        const DD inc = wave_inclusive_scan_dd(l);
+        la = wave_sum_dd(la);
+        if (lane == 63) {
+            s_dsum[0][wid] = inc.hi;
+            s_dsum[1][wid] = inc.lo;
+        }
+        if (lane == 0) {
+            s_dabs[0][wid] = la.hi;
+            s_dabs[1][wid] = la.lo;
+        }
+        lds_barrier();
+        const bool in = lane < kPlanWaves;
+        const int li = in ? lane : 0;
+        const bool lower = in && lane < wid;
+        DD vs{lower ? s_dsum[0][li] : 0.0, lower ? s_dsum[1][li] : 0.0};
+        DD va{in ? s_dabs[0][li] : 0.0, in ? s_dabs[1][li] : 0.0};
+        vs = row16_sum_dd(vs);
+        va = row16_sum_dd(va);
+        const DD total{readfirst_f64(va.hi), readfirst_f64(va.lo)};
+        if (total.hi > 0.0) {
+            if (dd_top_exp(total) - min_lsb >= kExactSpanBits) flags |= 4;
+            // c leaves the float32 range (|c| <= sum |log f|, reached at the end
+            // when no gate is positive)
+            if (__builtin_isinf(dd_to_f32(total))) flags |= 2;
+        }
+        run_dd = dd_add(DD{readfirst_f64(vs.hi), readfirst_f64(vs.lo)}, dd_add(inc, dd_neg(l)));
+    } else if (total_abs > 0.0 && !__builtin_isfinite((float)total_abs)) {
+        flags |= 2;   // (the float64 total is exact here)
     }
 
     // ---- U and delta ---------------------------------------------------------------------
@@ -301,49 +357,54 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
     }
 
     // ---- c = cumsum(log f) and the block corners ----------------------------------------
-    // exclusive prefix (exact when the span check passes), then c = float32 of the
-    // running pair
-    DD run = dd_add(before, dd_add(incl, dd_neg(local)));
     auto corner = [&](int j, float cf) __attribute__((always_inline)) {
         if ((j & (kBlock - 1)) == 0) s_first[j / kBlock] = cf;
         if ((j & (kBlock - 1)) == kBlock - 1) s_last[j / kBlock] = cf;
+    };
+    // run: the exclusive prefix (float64 or a pair), exact when the span check passes
+    auto emit = [&](auto run) __attribute__((always_inline)) {
+        if (vec) {
+#pragma unroll
+            for (int i = 0; i < kPlanHeld; i += 4) {
+                if (i < n) {
+                    float4 cv;
+                    run = sum_add(run, xv[i]);     cv.x = sum_f32(run);
+                    run = sum_add(run, xv[i + 1]); cv.y = sum_f32(run);
+                    run = sum_add(run, xv[i + 2]); cv.z = sum_f32(run);
+                    run = sum_add(run, xv[i + 3]); cv.w = sum_f32(run);
+                    *reinterpret_cast<float4*>(cw + beg + i) = cv;
+                    corner(beg + i, cv.x);            // beg + i is a multiple of 4
+                    corner(beg + i + 3, cv.w);
+                }
+            }
+        } else if (held) {
+#pragma unroll
+            for (int i = 0; i < kPlanHeld; ++i) {
+                if (i < n) {
+                    run = sum_add(run, xv[i]);
+                    const float cf = sum_f32(run);
+                    cw[beg + i] = cf;
+                    corner(beg + i, cf);
+                }
+            }
+        } else {
+            for (int i = 0; i < n; ++i) {
+                run = sum_add(run, x[beg + i]);
+                const float cf = sum_f32(run);
+                cw[beg + i] = cf;
+                corner(beg + i, cf);
+            }
+        }
     };
     if (gated) {
         for (int m = t; m < M; m += kPlanThreads) {
             s_first[m] = cw[kBlock * m];
             s_last[m] = cw[kBlock * m + kBlock - 1];
         }
-    } else if (vec) {
-#pragma unroll
-        for (int i = 0; i < kPlanHeld; i += 4) {
-            if (i < n) {
-                float4 cv;
-                run = dd_add(run, (double)xv[i]);     cv.x = dd_to_f32(run);
-                run = dd_add(run, (double)xv[i + 1]); cv.y = dd_to_f32(run);
-                run = dd_add(run, (double)xv[i + 2]); cv.z = dd_to_f32(run);
-                run = dd_add(run, (double)xv[i + 3]); cv.w = dd_to_f32(run);
-                *reinterpret_cast<float4*>(cw + beg + i) = cv;
-                corner(beg + i, cv.x);            // beg + i is a multiple of 4
-                corner(beg + i + 3, cv.w);
-            }
-        }
-    } else if (held) {
-#pragma unroll
-        for (int i = 0; i < kPlanHeld; ++i) {
-            if (i < n) {
-                run = dd_add(run, (double)xv[i]);
-                const float cf = dd_to_f32(run);
-                cw[beg + i] = cf;
-                corner(beg + i, cf);
-            }
-        }
+    } else if (wide) {
+        emit(run_dd);
     } else {
-        for (int i = 0; i < n; ++i) {
-            run = dd_add(run, (double)x[beg + i]);
-            const float cf = dd_to_f32(run);
-            cw[beg + i] = cf;
-            corner(beg + i, cf);
-        }
+        emit(before + (incl - local));
     }
     lds_barrier();
 

@@ -84,6 +84,14 @@ __device__ __forceinline__ double readlane_f64(double v, int l) {
 }
 
 
+// The value of lane 0 (wave-uniform), as a scalar.
+__device__ __forceinline__ double readfirst_f64(double v) {
+    const unsigned long long b = __double_as_longlong(v);
+    const unsigned lo = (unsigned)__builtin_amdgcn_readfirstlane((int)(unsigned)b);
+    const unsigned hi = (unsigned)__builtin_amdgcn_readfirstlane((int)(unsigned)(b >> 32));
+    return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
+}
+
 // Inclusive prefix sum over the workgroup of one double per thread (any
 // association: the callers only add values whose float64 sums are exact).
 __device__ inline double block_inclusive_scan(double v, double* s_wave) {
@@ -156,6 +164,11 @@ __device__ __forceinline__ DD dd_add(DD a, double b) {
 }
 __device__ __forceinline__ DD dd_neg(DD a) { return DD{-a.hi, -a.lo}; }
 
+// Running sums of float32 gates in either precision (float64 where the span
+// allows it, else pairs), and their float32 value.
+__device__ __forceinline__ double sum_add(double r, float x) { return r + (double)x; }
+__device__ __forceinline__ DD sum_add(DD r, float x) { return dd_add(r, (double)x); }
+
 // The float32 rounding (to nearest, ties to even) of hi + lo.  hi is the nearest
 // float64 to the value and every float32 midpoint is a float64, so the rounding
 // of hi is that of the value unless hi is itself a midpoint; then lo decides.
@@ -182,6 +195,13 @@ __device__ __forceinline__ float dd_to_f32(DD a) {
     if (a.hi == 0.5 * (rd + od) && ((a.lo > 0.0) == (od > rd))) r = other;
     return r;
 }
+
+__device__ __forceinline__ float sum_f32(double r) { return (float)r; }
+__device__ __forceinline__ float sum_f32(DD r) { return dd_to_f32(r); }
+__device__ __forceinline__ double sum_hi(double r) { return r; }
+__device__ __forceinline__ double sum_lo(double) { return 0.0; }
+__device__ __forceinline__ double sum_hi(DD r) { return r.hi; }
+__device__ __forceinline__ double sum_lo(DD r) { return r.lo; }
 
 // Least E with |value| < 2^E for a positive pair (the span bound above).
 __device__ __forceinline__ int dd_top_exp(DD a) {

@@ -63,11 +63,15 @@ def test_boundary_bit_exact(name):
         assert frac.min() == 0.0 and frac.max() > 0.9
 
 
-@pytest.mark.parametrize("L", [4160, 32768])
-def test_boundary_lengths_off_the_vector_path(L):
+@pytest.mark.parametrize("L,sigma", [(4160, 0.5), (32768, 0.5), (4160, 6.0), (32768, 6.0)])
+def test_boundary_lengths_off_the_vector_path(L, sigma):
     # L = 4160: runs of 5 gates per thread (scalar path); L = 32768: runs longer
-    # than the registers hold (re-read from memory); both bit-exact.
-    w = workloads.custom("len", 1, 3, L, 64, "bf16", 12, mu=(0.5, 3.0, 9.0))
+    # than the registers hold (re-read from memory); both bit-exact.  A logit
+    # spread of 6 takes every head to spans of 73-90 bits (the double-double round).
+    if sigma > 1.0:
+        w = workloads.custom("lenw", 1, 3, L, 64, "bf16", 13, mu=(0.5, 10.0, 20.0), gate_sigma=sigma)
+    else:
+        w = workloads.custom("len", 1, 3, L, 64, "bf16", 12, mu=(0.5, 3.0, 9.0))
     print(f"case: boundary {w.describe()}", flush=True)
     x = workloads.generate(w, with_grad=False)
     got = _gpu_plan(x, w.eps)

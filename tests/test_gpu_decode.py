@@ -143,6 +143,18 @@ def test_decode_random_setups(B, H, d, dtype, L0, L, C, eps, L_max, mu, seed):
     _check(w, L0, C, eps, L_max)
 
 
+def test_decode_wide_gate_spans_stay_exact():
+    """Logits N(mu, 8): the prompt's cumulative sums span 69-94 bits and the
+    running sum reaches 99 bits during the steps, past the 53 bits a float64 holds.
+    The set-up's double-double scan and each step's pair addition keep c and the
+    running sum exact (no flag), and the outputs follow the oracle."""
+    w = workloads.custom("decw", 1, 4, 448, 64, "bf16", 45, mu=(5.0, 15.0, 25.0, 35.0),
+                         gate_sigma=8.0, qk_norm=True)
+    lf = workloads.generate(w, with_grad=False)["log_f"].numpy()
+    assert min(orc.cumsum_span_bits(lf[0, h, :333]) for h in range(w.H)) > 53
+    _check(w, 333, 512, EPS, 4096, expect_lost=False)
+
+
 def test_decode_ring_smaller_than_window():
     """C = 128: heads with a long kept window lose keys (flag bit 4) and attend to
     the kept keys the ring still holds; the fast-decaying head fits."""
