@@ -324,6 +324,9 @@ acp_status acp_decode_init(const void* K, const void* V, const float* log_f,
  * ring, advances the pointer, and writes the attention output of query q [B,H,d]
  * over its kept keys (eq. 1-2 restricted by the block test above):
  *   O [B,H,d] dt, lse [B,H] float (natural-log log-sum-exp of the kept logits).
+ * The running sum is a double-double pair, and c_t the float32 rounding of it;
+ * flag bit 2 is set if adding log f_t rounds the pair (it stays exact while the
+ * sums span at most 105 bits), bits 0 and 1 for a positive or non-finite log f_t.
  * Requires 1 <= t < L_max (checked against the L_max the caller states again). */
 acp_status fox_attn_decode(const void* q, const void* k, const void* v, const float* log_f,
                            acp_dtype dt, int B, int H, int t, int C, int d, int64_t L_max,

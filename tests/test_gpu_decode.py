@@ -183,6 +183,27 @@ def test_decode_flags_a_positive_gate():
     assert all(int(fl[0, 1]) & 1 == (1 if t >= 100 else 0) for t, _, _, _, fl in steps)
 
 
+def test_decode_flags_a_rounding_step():
+    """Flag bit 2 in the steps: a gate of -1e-30 fits into the running pair's low
+    part exactly (no flag); a later gate of -3e-20 would need 59 bits there, so that
+    addition rounds and the flag is set from that step on.  The other head stays
+    clean."""
+    w = workloads.custom("dec", 1, 2, 128, 64, "bf16", 46, mu=(1.0, 3.0), qk_norm=True)
+
+    def poke(t, lf):
+        if t == 80:
+            lf[0, 1] = -1e-30
+        if t == 90:
+            lf[0, 1] = -3e-20
+
+    print("case: decode flag bit 2 at a rounding step", flush=True)
+    _, init, steps, fin = _run(w, 64, 128, EPS, 4096, poke=poke)
+    assert int(init["flags"].max()) == 0
+    for t, _, _, _, fl in steps:
+        assert int(fl[0, 0]) == 0, t
+        assert int(fl[0, 1]) == (acp.FLAG_INEXACT_CUMSUM if t >= 90 else 0), (t, int(fl[0, 1]))
+
+
 def test_decode_steps_captured_in_a_graph_match_eager():
     """Eight steps captured in a HIP graph: each replay (after an eager re-init of
     the state in between) must give exactly the eager outputs and state."""
