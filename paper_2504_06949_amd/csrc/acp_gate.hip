@@ -299,7 +299,8 @@ __global__ __launch_bounds__(kGateThreads) void gate_kernel(
                     DD v{0.0, 0.0};
                     if (lane < stop && i >= 0) v = DD{bits_f64(qq), bits_f64(ql)};
                     if (lane == stop) v = DD{bits_f64(p), bits_f64(pl)};
-                    run = dd_add(run, wave_sum_dd(v));
+                    double sum;
+                    run = dd_add(run, wave_sum_f64_if_exact(v, sum) ? DD{sum, 0.0} : wave_sum_dd(v));
                     if (stop < 64) break;
                     i0 -= 64;
                     spins = 0;

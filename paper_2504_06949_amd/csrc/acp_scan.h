@@ -240,6 +240,26 @@ __device__ __forceinline__ DD wave_sum_dd(DD v) {
     return dd_add(dd_add(readlane_dd(r, 0), readlane_dd(r, 16)),
                   dd_add(readlane_dd(r, 32), readlane_dd(r, 48)));
 }
+// Sum over the 64 lanes in float64 when that is exact: every lane's low part is
+// zero and no addition rounds (each one's TwoSum error is checked off the
+// critical path).  Returns false, uniformly over the wave, otherwise; the caller
+// then takes wave_sum_dd.
+__device__ __forceinline__ bool wave_sum_f64_if_exact(DD v, double& out) {
+    bool inexact = v.lo != 0.0;
+    double s = v.hi;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+        const DD t = two_sum(s, dpp_f64(s, c));
+        inexact = inexact || t.lo != 0.0;
+        s = t.hi;
+    }
+    const DD a = two_sum(readlane_f64(s, 0), readlane_f64(s, 16));
+    const DD b = two_sum(readlane_f64(s, 32), readlane_f64(s, 48));
+    const DD r = two_sum(a.hi, b.hi);
+    inexact = inexact || a.lo != 0.0 || b.lo != 0.0 || r.lo != 0.0;
+    out = r.hi;
+    return __ballot(inexact) == 0ull;
+}
 // Inclusive prefix sum over the 1024-thread workgroup (s_hi, s_lo: kPlanWaves each).
 __device__ inline DD block_inclusive_scan_dd(DD v, double* s_hi, double* s_lo) {
     const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
