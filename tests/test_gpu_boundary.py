@@ -241,3 +241,31 @@ def test_gate_spreads_near_105_bits():
             np.testing.assert_array_equal(got["col_end"][b, h], ce)
     print(f"  {flagged} heads flagged, {exact} exact", flush=True)
     assert flagged > 0 and exact > 0
+
+
+def test_wide_spreads_at_the_760m_shape():
+    """The 760M-shaped layer (B = 2, H = 24, L = 16384, the longest held-in-register
+    runs) with logit spreads of 8: every head goes through the double-double round;
+    flag bit 2 exactly from 105 bits on, c and the boundary bit-exact below."""
+    w = workloads.custom("wide760", 2, 24, 16384, 64, "bf16", 95,
+                         mu=tuple(float(m) for m in np.linspace(0.0, 36.0, 24)), gate_sigma=8.0)
+    print(f"case: boundary {w.describe()}", flush=True)
+    x = workloads.generate(w, with_grad=False)
+    got = _gpu_plan(x, w.eps)
+    lf = x["log_f"].numpy()
+    c_ref = orc.cumsum_log_gates(lf)
+    spans = np.array([[orc.cumsum_span_bits(lf[b, h]) for h in range(w.H)] for b in range(w.B)])
+    assert spans.min() > 53
+    np.testing.assert_array_equal(got["flags"], np.where(spans >= 105, acp.FLAG_INEXACT_CUMSUM, 0))
+    for b in range(w.B):
+        for h in range(w.H):
+            if spans[b, h] >= 105:
+                continue
+            np.testing.assert_array_equal(got["c"][b, h], c_ref[b, h])
+            q = x["q"][b, h].float().numpy()
+            k = x["k"][b, h].float().numpy()
+            U = orc.logit_bound(orc.row_norm_sq_max(q), orc.row_norm_sq_max(k), w.d)
+            delta = orc.threshold(U, w.L, w.eps)
+            rs, ce = orc.boundary_from_block_keep(orc.block_keep_topright(c_ref[b, h], delta))
+            np.testing.assert_array_equal(got["row_start"][b, h], rs)
+            np.testing.assert_array_equal(got["col_end"][b, h], ce)
