@@ -35,6 +35,15 @@ COMMON = [
 ]
 
 
+# Per-source additions.  The forward kernels are scheduled for instruction-level
+# parallelism: measured about 1% faster than the default scheduler on the 760M
+# layer, which leaves the backward kernels slightly slower, so it applies to this
+# file alone.
+PER_SOURCE = {
+    "fox_fwd.hip": ["-mllvm", "-amdgpu-sched-strategy=max-ilp"],
+}
+
+
 def hipcc() -> str:
     for cand in (os.environ.get("HIPCC"), "/opt/rocm/bin/hipcc", shutil.which("hipcc")):
         if cand and os.path.exists(cand):
@@ -57,7 +66,8 @@ def build(verbose: bool = False) -> str:
     for src in SOURCES:
         obj = os.path.join(BUILD_DIR, os.path.splitext(src)[0] + ".o")
         lang = ["-x", "hip"] if src.endswith(".hip") else []
-        jobs.append(([cc] + COMMON + lang + ["-c", os.path.join(CSRC, src), "-o", obj], obj))
+        extra = PER_SOURCE.get(src, [])
+        jobs.append(([cc] + COMMON + extra + lang + ["-c", os.path.join(CSRC, src), "-o", obj], obj))
     with concurrent.futures.ThreadPoolExecutor(max_workers=len(jobs)) as ex:
         for cmd, _ in jobs:
             if verbose:
