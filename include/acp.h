@@ -44,8 +44,8 @@
  *              total just above a power of two down to it beyond 105 bits, which
  *              would then read one bit short.  Clear bit 2 thus guarantees that c
  *              is the float32 rounding of the exact sum; set, c may differ in its
- *              last bit.  (At L <= 131072 a span of 105 bits needs a ratio of
- *              2^65 or more between the largest and the smallest nonzero |log f|.)
+ *              last bit.  (At L <= 131072 a span of 105 bits needs a ratio of about
+ *              2^64 or more between the largest and the smallest nonzero |log f|.)
  *       bit 3  rho_q^2 or rho_k^2 is not finite (Q or K holds NaN/Inf or overflows),
  *              or, in the QK-norm variants, a scale bound is negative or not finite
  *       bit 4  (decoding only) a key that ACP keeps had already left the ring cache,
