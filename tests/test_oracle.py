@@ -3,6 +3,7 @@ error bound, independent derivations (exact rationals, autograd, finite
 differences) and brute force.  None of these re-types the oracle's own formula.
 """
 import math
+from fractions import Fraction
 
 import numpy as np
 import pytest
@@ -75,7 +76,6 @@ def _span_gates(span):
 
 def _float64_prefix_sums_exact(lf) -> bool:
     """Every float64 running partial sum equals the exact rational one."""
-    from fractions import Fraction
     acc, exact = 0.0, Fraction(0)
     for v in np.asarray(lf, dtype=np.float32).astype(np.float64):
         acc += float(v)
@@ -111,7 +111,6 @@ def test_cumsum_span_bits_power_of_two_total_and_subnormal():
 def test_fraction_rounding_is_single_rounding():
     # 1 + 2^-24 + 2^-60 must round up to 1 + 2^-23 (a float64 detour would round
     # 1 + 2^-24 + 2^-60 to 1 + 2^-24 and then tie to even, giving 1).
-    from fractions import Fraction
     from oracle.acp_oracle import _fraction_to_f32
     x = Fraction(1) + Fraction(1, 2 ** 24) + Fraction(1, 2 ** 60)
     assert _fraction_to_f32(x) == np.float32(1 + 2.0 ** -23)
@@ -603,7 +602,6 @@ def test_qk_projection_by_a_permutation_moves_columns():
 def test_gate_logits_dyadic_closed_form():
     # dyadic x and w whose partial sums all stay exact in float32: the logit is
     # the exact dot product plus the bias
-    from fractions import Fraction
     rng = _rng(11)
     T, Dm, H = 5, 64, 3
     x = rng.integers(-8, 9, size=(T, Dm)) / 8.0
@@ -650,3 +648,25 @@ def test_gate_log_forget_layout_and_head_permutation():
     perm = [2, 0, 1]
     lf2 = orc.gate_log_forget(x, w[:, perm], b[perm], 2)
     np.testing.assert_array_equal(lf2, lf[:, perm])
+
+
+def test_exact_roundings_agree_with_ieee_casts():
+    """The oracle's two exact roundings to float32 (from a rational, from an
+    integer times a power of two) against numpy's IEEE float64 -> float32 cast
+    (round to nearest, ties to even) on values a float64 holds exactly: normal,
+    subnormal, near the overflow threshold, and float32 midpoints."""
+    from oracle.acp_oracle import _fraction_to_f32, _int_to_f32
+    rng = np.random.default_rng(17)
+    vals = list(rng.standard_normal(2000) * np.exp2(rng.integers(-160, 128, 2000).astype(np.float64)))
+    for e in (-149, -140, -126, -1, 0, 60, 127):
+        for m in range(1 << 23, (1 << 23) + 40):
+            vals.append(math.ldexp(m + 0.5, e - 23))     # a float32 midpoint (float64 holds it)
+    vals += [3.4028235677973366e38, -3.4028235677973366e38, 3.40282356779733e38, 2.0 ** -150, 2.0 ** -151]
+    with np.errstate(over="ignore"):
+        for v in vals:
+            want = np.float32(v)
+            assert _fraction_to_f32(Fraction(v)) == want, v
+            m, e = math.frexp(v)
+            n, lsb = int(m * 2 ** 53), e - 53                 # v = n * 2^lsb exactly
+            got = _int_to_f32(n, lsb)
+            assert got == want or (np.isinf(got) and np.isinf(want) and np.sign(got) == np.sign(want)), v
